@@ -1,0 +1,253 @@
+/*
+ * ar.h -- C ABI of libar, a simulated-ring AllReduce for AMD MI355X (gfx950).
+ *
+ * What it computes.  AllReduce-sum over N rank buffers that all live in one
+ * GPU's memory: afterwards every rank's buffer holds
+ *     y[i] = x_0[i] + x_1[i] + ... + x_{N-1}[i].
+ * The paper steers exactly this collective: its tuner picks the algorithm
+ * (ring), the protocol (LL, LL128, Simple) and the channel count for every
+ * AllReduce call (paper, section 2 "NCCL and its plugin system"; section 3.3,
+ * the policy programming model; section 5.3, Table 2 and Figure 2, where a
+ * message-size-aware choice of ring protocol and channels beats the default).
+ *
+ * How.  A ring reduce-scatter followed by a ring all-gather.  Each simulated
+ * rank is one group of workgroups; consecutive ranks exchange chunks through
+ * FIFOs in device memory, with flags as the "link".  Segment-major layout:
+ * with A = 16 / element bytes, seg = roundup(ceil(count / N), A); segment s
+ * covers elements [s*seg, min((s+1)*seg, count)) and is summed along the
+ * ring starting at rank s (acc = x_s, then + x_{s+1}, ... + x_{s+N-1}), each
+ * addition one binary32 round-to-nearest-even operation; rank s-1 owns the
+ * result and the all-gather copies it around.  The result bits therefore
+ * depend only on (N, count, dtype), never on protocol, channels or chunk.
+ * bf16: inputs widen exactly to fp32, partial sums travel as fp32, and the
+ * owner rounds once to bf16 (round to nearest even, NaN -> 0x7FC0).
+ *
+ * Conventions.  All sizes are in elements unless named *_bytes.  Device
+ * pointers are HIP device pointers on the current device; `stream` is a
+ * hipStream_t passed as void* (NULL = the null stream).  Functions that
+ * return int return AR_OK (0) or an AR_ERR_* code; functions that return a
+ * pointer return NULL on error and leave the code in ar_last_error().
+ * Nothing here is thread-safe for one plan: use a plan from one host thread
+ * and keep at most one ar_run of a plan in flight (its FIFOs and flag epoch
+ * are shared by all its runs).  Different plans are independent.
+ */
+#ifndef AR_H
+#define AR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AR_VERSION 1
+#define AR_MAX_RANKS 16
+#define AR_MAX_CHANNELS 256
+#define AR_MAX_WAVES 16
+
+/* Element types. */
+enum { AR_FLOAT32 = 0, AR_BFLOAT16 = 1 };
+
+/* Protocols (paper, section 2: the tuner chooses among LL, LL128, Simple).
+ *   LL     8-byte lines: 4 bytes of data + 4-byte flag in one word; the
+ *          reader checks the flag in the same load that brings the data.
+ *   LL128  128-byte lines: 120 bytes of data + 8-byte flag.
+ *   Simple bulk chunks behind separate ready (tail) / free (head) counters. */
+enum { AR_PROTO_AUTO = -1, AR_PROTO_LL = 0, AR_PROTO_LL128 = 1, AR_PROTO_SIMPLE = 2 };
+
+/* Collective type seen by the tuner (only AllReduce is implemented). */
+enum { AR_COLL_ALLREDUCE = 0 };
+
+/* Workgroup placement: how the grid index maps to (channel c, rank r).
+ *   AR_PLACE_RANK_SPREAD   block = c*N + r (consecutive ranks on different XCDs)
+ *   AR_PLACE_CHANNEL_LOCAL block = r*C + c (one channel's ranks share an XCD
+ *                          when C is a multiple of 8)
+ * Results are identical; only speed differs. */
+enum { AR_PLACE_RANK_SPREAD = 0, AR_PLACE_CHANNEL_LOCAL = 1 };
+
+/* Status codes. */
+enum {
+    AR_OK = 0,
+    AR_ERR_ARG = 1,          /* bad argument (NULL, range, alignment, overlap) */
+    AR_ERR_UNSUPPORTED = 2,  /* valid request this build does not implement */
+    AR_ERR_NOMEM = 3,        /* device or host allocation failed */
+    AR_ERR_HIP = 4,          /* a HIP runtime call failed */
+    AR_ERR_OCCUPANCY = 5,    /* grid cannot be co-resident on the device */
+    AR_ERR_TIMEOUT = 6,      /* a flag wait exceeded the watchdog (sticky) */
+    AR_ERR_STATE = 7         /* plan is in an error state; call ar_plan_reset */
+};
+
+/* Debug knobs (ar_plan_desc.debug_flags); zero in normal use.
+ *   AR_DEBUG_SKIP_POST  channel 0 / wave 0 / rank 0 never announces its
+ *                       first message, so its successor's wait runs into the
+ *                       watchdog: every wave still exits and the run reports
+ *                       AR_ERR_TIMEOUT.
+ *   AR_DEBUG_JITTER     pseudo-random short sleeps before flag posts, to
+ *                       shake out ordering races. */
+enum { AR_DEBUG_SKIP_POST = 1u, AR_DEBUG_JITTER = 2u };
+
+typedef struct ar_plan_s ar_plan_t;
+
+/* Full plan description.  Zero fields take the tuner's choice or the
+ * library default, so a zero-initialised struct plus {nranks, count, dtype,
+ * proto = AR_PROTO_AUTO} is a valid request. */
+typedef struct ar_plan_desc {
+    int nranks;            /* 1 .. AR_MAX_RANKS; N = 1 is a no-op */
+    int dtype;             /* AR_FLOAT32 or AR_BFLOAT16 */
+    size_t count;          /* elements per rank; 0 is a valid no-op */
+    int proto;             /* AR_PROTO_*; AUTO asks the tuner */
+    int nchannels;         /* 1 .. AR_MAX_CHANNELS; 0 asks the tuner */
+    size_t chunk_bytes;    /* data bytes per ring step per (segment, channel);
+                              0 asks the tuner / default */
+    int fifo_depth;        /* FIFO slots per connection (2..16); 0 = default */
+    int nwaves;            /* wavefronts per workgroup (1..AR_MAX_WAVES); 0 = default */
+    int placement;         /* AR_PLACE_* */
+    uint32_t timeout_us;   /* watchdog per flag wait; 0 = default (2 s) */
+    uint32_t debug_flags;  /* AR_DEBUG_*; 0 in normal use */
+    int max_channels;      /* geometry query only: device channel capacity
+                              (0 = AR_MAX_CHANNELS); plans use the device's */
+} ar_plan_desc;
+
+/* Resolved plan geometry (after the tuner and defaults). */
+typedef struct ar_plan_info {
+    int nranks, dtype, proto, nchannels, nwaves, fifo_depth, placement;
+    int grid;              /* workgroups = nchannels * nranks */
+    int block;             /* threads per workgroup = 64 * nwaves */
+    size_t count;
+    size_t seg_elems;      /* segment length: roundup(ceil(count/N), A) */
+    size_t chan_elems;     /* per-channel sub-range of a segment */
+    size_t chunk_elems;    /* per-(segment, channel) ring step */
+    size_t wave_elems;     /* one wave's share of a chunk step */
+    size_t nchunks;        /* chunk steps per channel sub-range */
+    size_t slot_bytes;     /* one FIFO slot of one (connection, wave) */
+    size_t fifo_bytes;     /* all FIFO slots */
+    size_t flag_bytes;     /* head/tail counters and control words */
+    uint64_t msgs_per_run; /* messages per connection per run: nchunks*(2N-2) */
+    uint64_t wire_bytes_per_run; /* FIFO payload+flag bytes written per run (all connections) */
+} ar_plan_info;
+
+/* ---- plans -------------------------------------------------------------- */
+
+/* Create a plan for AllReduce of `count` elements of `dtype` over `nranks`
+ * simulated ranks on the current HIP device.  proto = AR_PROTO_AUTO or
+ * nchannels = 0 consults the active tuner with msg_bytes = count * element
+ * size.  The plan owns its FIFO, flag and status memory (device memory on
+ * the current device, zeroed here, freed by ar_destroy).  Returns NULL on
+ * error (see ar_last_error): AR_ERR_ARG for out-of-range arguments,
+ * AR_ERR_OCCUPANCY if nchannels * nranks workgroups cannot be co-resident,
+ * AR_ERR_NOMEM / AR_ERR_HIP for allocation or device failures. */
+ar_plan_t *ar_plan(int nranks, size_t count, int dtype, int proto, int nchannels);
+
+/* Same as ar_plan with every knob of ar_plan_desc. */
+ar_plan_t *ar_plan_ex(const ar_plan_desc *desc);
+
+/* In-place AllReduce.  `bufs` is a host array of nranks device pointers,
+ * each to `count` elements of the plan's dtype, 16-byte aligned and pairwise
+ * non-overlapping; on completion each holds y.  The pointer array is copied;
+ * the buffers stay owned by the caller.  Enqueued asynchronously on `stream`:
+ * errors found on the host are returned (AR_ERR_ARG, AR_ERR_STATE,
+ * AR_ERR_HIP); a watchdog timeout inside the kernel is reported later by
+ * ar_plan_status.  Safe in place: a rank reads each element of its input
+ * before it writes the result to that element. */
+int ar_run(ar_plan_t *plan, void *const *bufs, void *stream);
+
+/* Out-of-place AllReduce: reads send[r], writes recv[r].  recv buffers must
+ * not overlap each other or any other rank's send buffer; recv[r] may equal
+ * send[r].  Same numerics as ar_run. */
+int ar_run_oop(ar_plan_t *plan, const void *const *send, void *const *recv, void *stream);
+
+/* Watchdog status, to be read after the stream has been synchronised:
+ * AR_OK, or AR_ERR_TIMEOUT if any wave's flag wait exceeded the watchdog in
+ * any run since creation or the last ar_plan_reset (sticky).  While sticky,
+ * ar_run returns AR_ERR_STATE without launching. */
+int ar_plan_status(ar_plan_t *plan);
+
+/* Re-zero the plan's FIFOs, flags and status and restart its flag epoch.
+ * Synchronous (waits for the device); call when no run is in flight. */
+int ar_plan_reset(ar_plan_t *plan);
+
+/* Debug: fill every FIFO data byte with 0xFF (a NaN pattern and an invalid
+ * LL/LL128 flag) on `stream`, leaving the flags intact, so that a reader that
+ * consumed a slot before it was written would see NaN.  Call between runs. */
+int ar_plan_poison(ar_plan_t *plan, void *stream);
+
+/* Free the plan.  The caller must have synchronised every stream that ran
+ * it.  NULL is ignored. */
+void ar_destroy(ar_plan_t *plan);
+
+/* Resolved geometry of an existing plan. */
+int ar_plan_get_info(const ar_plan_t *plan, ar_plan_info *out);
+
+/* Device memory the plan holds (FIFO + flags + control words), bytes. */
+size_t ar_plan_workspace_bytes(const ar_plan_t *plan);
+
+/* Resolve a description to its geometry on the host alone (tuner, defaults,
+ * segment / channel / chunk split, FIFO sizes) without touching a GPU.
+ * Uses desc->max_channels (0 = AR_MAX_CHANNELS) as the channel capacity. */
+int ar_plan_geometry(const ar_plan_desc *desc, ar_plan_info *out);
+
+/* ---- tuner (paper, section 3.3, policy programming model; section 4,
+ *      cost-table fallback and channel clamp; section 5.3, size-aware policy) */
+
+/* Input of a tuning decision: mirrors the paper's policy context
+ * (collective type, message size, rank count) plus dtype and the channel
+ * capacity the decision must respect. */
+typedef struct ar_tune_ctx {
+    int coll;              /* AR_COLL_ALLREDUCE */
+    size_t msg_bytes;      /* bytes per rank */
+    int nranks;
+    int dtype;
+    int max_channels;      /* the decision is clamped to [1, max_channels] */
+    uint64_t comm_id;      /* caller-chosen communicator key (0 if unused) */
+} ar_tune_ctx;
+
+/* Output of a tuning decision. */
+typedef struct ar_tune_out {
+    int proto;             /* AR_PROTO_LL / LL128 / SIMPLE; AUTO = no opinion */
+    int nchannels;         /* 0 = no opinion */
+    size_t chunk_bytes;    /* 0 = protocol default */
+    int nwaves;            /* 0 = protocol default */
+} ar_tune_out;
+
+/* A tuner: fill *out from *ctx; return 0 on success.  A non-zero return, or
+ * an output outside the valid ranges, makes ar_tune fall back to the fixed
+ * default (Simple, 16 channels) -- the analogue of the paper's cost table,
+ * where unavailable choices fall back to the library's own. */
+typedef int (*ar_tuner_fn)(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);
+
+/* Make fn (with its user pointer) the active tuner; NULL restores the built-in
+ * MI355X table.  The swap is one atomic pointer store: a decision already in
+ * progress finishes with the old tuner.  fn and user must stay valid until
+ * replaced. */
+int ar_set_tuner(ar_tuner_fn fn, void *user);
+
+/* Run the active tuner on *ctx, validate and clamp, and write a complete
+ * decision to *out (proto, nchannels, chunk_bytes and nwaves all set).
+ * Returns AR_ERR_ARG for a NULL or invalid ctx; otherwise AR_OK, also when
+ * the tuner's answer was replaced by the fallback. */
+int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out);
+
+/* Built-in tuners. */
+int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);         /* MI355X size table */
+int ar_tuner_fixed_default(const ar_tune_ctx *ctx, ar_tune_out *out, void *user); /* Simple, 16 channels */
+int ar_tuner_noop(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);          /* defers: no opinion */
+
+/* ---- errors and version ------------------------------------------------- */
+
+const char *ar_strerror(int code);
+int ar_last_error(void);   /* code of the last failed call on this thread */
+int ar_version(void);
+
+/* ---- device self-checks ------------------------------------------------- */
+
+/* Round n floats to bf16 bits with the library's device conversion (round to
+ * nearest even, NaN -> 0x7FC0): in and out are device pointers, enqueued on
+ * stream.  Lets tests compare the device rounding with other conversions. */
+int ar_debug_bf16_round(const float *in, uint16_t *out, size_t n, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AR_H */

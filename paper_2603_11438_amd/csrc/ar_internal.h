@@ -1,0 +1,63 @@
+// Internal declarations shared by the host runtime and the HIP kernels of
+// libar.  Not part of the C ABI (see include/ar.h).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "ar.h"
+
+namespace ar {
+
+// Flag memory layout: every connection (channel c, wave w, sender rank r,
+// i.e. the link r -> r+1 of one wave's ring) owns two 128-byte lines, so no
+// two counters written by different waves share a cache line.
+//   tail: messages the sender has published on the link (sender writes)
+//   head: messages the receiver has consumed on the link (receiver writes)
+constexpr int kFlagLineU64 = 16;                 // 128 bytes
+constexpr int kConnFlagU64 = 2 * kFlagLineU64;   // tail line + head line
+constexpr int kCtlU32 = 64;                      // control block: 256 bytes
+constexpr int kCtlAbort = 0;                     // nonzero: every wave must leave
+constexpr int kCtlStatus = 32;                   // sticky AR_ERR_* bit set
+
+// Status bits written by the kernel into ctl[kCtlStatus].
+constexpr uint32_t kStatusTimeout = 1u;
+
+// Everything a ring kernel launch needs; passed by value as the kernel
+// argument.  Counts are in elements of the plan's dtype.
+struct RingArgs {
+    const char *src[AR_MAX_RANKS];   // rank inputs
+    char *dst[AR_MAX_RANKS];         // rank outputs (== src for in place)
+    char *fifo;                      // all FIFO slots
+    uint64_t *flags;                 // per-connection head/tail lines
+    uint32_t *ctl;                   // abort word + status word
+    uint64_t count;                  // elements per rank
+    uint64_t seg;                    // segment length
+    uint64_t cs;                     // per-channel sub-range of a segment
+    uint64_t chunk;                  // per-(segment, channel) ring step
+    uint64_t kw;                     // one wave's share of a chunk step
+    uint64_t slot_bytes;             // bytes of one FIFO slot
+    uint64_t epoch;                  // absolute index of this run's first message
+    uint64_t timeout_ticks;          // watchdog, in 100 MHz real-time ticks
+    uint32_t nranks, nchannels, nwaves, depth, nchunks, placement, debug;
+};
+
+// Resolved plan geometry.  Computed on the host only.
+int resolve_geometry(const ar_plan_desc *desc, int max_channels, ar_plan_info *out);
+
+// Protocol defaults.
+int default_nwaves(int proto);
+int default_depth(int proto);
+size_t default_chunk_bytes(int proto);
+
+// Kernel launchers (ar_kernels.hip).
+int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream);
+int launch_fill_u32(uint32_t *p, size_t n, uint32_t value, void *stream);
+int launch_copy(const void *src, void *dst, size_t bytes, void *stream);
+int ring_occupancy(int proto, int dtype, int block, int *blocks_per_cu);
+int launch_bf16_round(const float *in, uint16_t *out, size_t n, void *stream);
+
+// Thread-local last error.
+void set_last_error(int code);
+
+}  // namespace ar

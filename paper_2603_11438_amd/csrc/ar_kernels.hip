@@ -1,0 +1,1018 @@
+// Ring AllReduce kernels for gfx950 (MI355X): reduce-scatter then
+// all-gather around a ring of N simulated ranks whose buffers all live in
+// one GPU's memory, under one of three protocols (LL, LL128, Simple).
+//
+// Work decomposition.  Grid = nchannels * nranks workgroups; workgroup
+// (channel c, rank r) holds `nwaves` wavefronts and each wavefront is an
+// independent ring member: wave w of rank r talks only to wave w of ranks
+// r-1 and r+1 of the same channel, through its own FIFO slots and its own
+// head/tail counters, so no wave ever waits on a workgroup barrier.
+//
+// Segment-major schedule (the same order the oracle follows).  Element
+// ranges: seg = roundup(ceil(count/N), A) per segment, then a channel's
+// sub-range of cs elements, then chunk steps of `chunk` elements, of which
+// wave w takes kw elements.  For every chunk step j, rank r runs ring steps
+// k = 0 .. 2N-2 on segment s = (r - k) mod N:
+//   k = 0         send its own input           (reduce-scatter start)
+//   0 < k < N-1   recv + own input -> send      (recvReduceSend)
+//   k = N-1       recv + own input -> y; write y, send y  (recvReduceCopySend)
+//   N-1 < k < 2N-2  recv y; write y, send y     (recvCopySend)
+//   k = 2N-2      recv y; write y               (recvCopy)
+// so segment s is summed x_s + x_{s+1} + ... + x_{s+N-1} in that order.
+//
+// Memory model.  A FIFO slot written by one wave is read by a wave that can
+// sit on another XCD, i.e. behind another L2.  Every FIFO access therefore
+// uses the device-scope coherence bit (sc1) -- the same encoding the
+// compiler uses for device-scope atomic loads and stores on this target --
+// and every counter is a device-scope atomic.  A sender makes its slot
+// writes complete (s_waitcnt vmcnt(0)) before it stores the counter or
+// flag that publishes them; a receiver issues its slot reads only after it
+// has observed that counter or flag.  Inputs and outputs are plain accesses:
+// each rank touches only its own buffers, from the same wave, in program
+// order (the read of an element always precedes the write of its result).
+//
+// Every wait is bounded by a watchdog on the 100 MHz real-time counter; a
+// wave that times out raises the plan's abort word and status bit, and all
+// waves leave their loops when they see the abort word, so the kernel always
+// drains.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ar_internal.h"
+
+namespace ar {
+namespace dev {
+
+typedef uint32_t u32x4 __attribute__((__vector_size__(16)));
+typedef uint32_t u32x2 __attribute__((__vector_size__(8)));
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+
+// Cache-policy operand of gfx950 buffer instructions.
+enum : int { kPolPlain = 0, kPolNt = 2, kPolSc1 = 16 };
+constexpr int kFifoPol = kPolSc1;   // device-coherent FIFO traffic
+constexpr int kInPol = kPolPlain;   // rank inputs
+constexpr int kOutPol = kPolPlain;  // rank outputs
+
+enum Kind : int { kSend = 0, kRecvReduceSend, kRecvReduceCopySend, kRecvCopySend, kRecvCopy };
+
+template <int DT> struct Elem;
+template <> struct Elem<AR_FLOAT32> { static constexpr uint32_t E = 4, A = 4; };
+template <> struct Elem<AR_BFLOAT16> { static constexpr uint32_t E = 2, A = 8; };
+
+__device__ __forceinline__ Rsrc make_rsrc(const void *p, uint64_t bytes)
+{
+    // Word 3 = 0x00020000: raw 32-bit dword format, as on the rest of CDNA.
+    uint32_t n = bytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)bytes;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)n, 0x00020000);
+}
+
+template <int POL> __device__ __forceinline__ u32x4 ld128(Rsrc r, uint32_t off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, POL);
+}
+template <int POL> __device__ __forceinline__ u32x2 ld64(Rsrc r, uint32_t off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, POL);
+}
+template <int POL> __device__ __forceinline__ uint32_t ld32(Rsrc r, uint32_t off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, POL);
+}
+template <int POL> __device__ __forceinline__ uint32_t ld16(Rsrc r, uint32_t off)
+{
+    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, POL);
+}
+template <int POL> __device__ __forceinline__ void st128(Rsrc r, uint32_t off, u32x4 v)
+{
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)off, 0, POL);
+}
+template <int POL> __device__ __forceinline__ void st64(Rsrc r, uint32_t off, u32x2 v)
+{
+    __builtin_amdgcn_raw_buffer_store_b64(v, r, (int)off, 0, POL);
+}
+template <int POL> __device__ __forceinline__ void st32(Rsrc r, uint32_t off, uint32_t v)
+{
+    __builtin_amdgcn_raw_buffer_store_b32(v, r, (int)off, 0, POL);
+}
+template <int POL> __device__ __forceinline__ void st16(Rsrc r, uint32_t off, uint32_t v)
+{
+    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)v, r, (int)off, 0, POL);
+}
+
+__device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & 63u; }
+
+__device__ __forceinline__ uint64_t uniform64(uint64_t v)
+{
+    uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// ---- fp32 / bf16 ------------------------------------------------------------
+
+__device__ __forceinline__ float as_f32(uint32_t u) { return __builtin_bit_cast(float, u); }
+__device__ __forceinline__ uint32_t as_u32(float f) { return __builtin_bit_cast(uint32_t, f); }
+
+// bf16 -> fp32 is exact: the bf16 bits are the top half of the fp32 word.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return as_f32(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return as_f32(w & 0xFFFF0000u); }
+
+// fp32 -> bf16, round to nearest even; NaN -> quiet NaN 0x7FC0.
+__device__ __forceinline__ uint32_t bf16_rne(float f)
+{
+    uint32_t u = as_u32(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
+{
+    return bf16_rne(lo) | (bf16_rne(hi) << 16);
+}
+
+// ---- flags, fences, watchdog ----------------------------------------------
+
+__device__ __forceinline__ uint64_t flag_load(const uint64_t *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void flag_store(uint64_t *p, uint64_t v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Make every earlier memory operation of this wave complete before what
+// follows is issued: s_waitcnt vmcnt(0) (expcnt and lgkmcnt left alone),
+// with compiler fences on both sides so no access is moved across it.
+__device__ __forceinline__ void drain_vmem()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// Keep later loads behind an observed flag (compiler ordering; the hardware
+// issues them after the flag value has been tested).
+__device__ __forceinline__ void after_observe() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup"); }
+
+struct Watchdog {
+    uint64_t start = 0;
+    uint32_t iter = 0;
+};
+
+// Returns true when the wave must give up: another wave aborted, or this
+// wait has exceeded the timeout (then this wave raises the abort itself).
+__device__ __forceinline__ bool watchdog_expired(const RingArgs &a, Watchdog &wd)
+{
+    if ((++wd.iter & 31u) != 0) return false;
+    uint32_t ab = __hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (__builtin_amdgcn_readfirstlane(ab) != 0) return true;
+    uint64_t now = wall_clock64();
+    if (wd.start == 0) {
+        wd.start = now;
+        return false;
+    }
+    if (now - wd.start > a.timeout_ticks) {
+        if (lane_id() == 0) {
+            __hip_atomic_fetch_or(a.ctl + kCtlStatus, kStatusTimeout, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.ctl + kCtlAbort, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        return true;
+    }
+    return false;
+}
+
+// Wait until *flag >= target.  `cache` holds the last value seen.
+__device__ __forceinline__ bool wait_geq(const RingArgs &a, const uint64_t *flag, uint64_t target,
+                                         uint64_t &cache)
+{
+    if (cache >= target) return true;
+    Watchdog wd;
+    while (true) {
+        uint64_t v = uniform64(flag_load(flag));
+        if (v >= target) {
+            cache = v;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        if (watchdog_expired(a, wd)) return false;
+    }
+    after_observe();
+    return true;
+}
+
+__device__ __forceinline__ void debug_jitter(const RingArgs &a, uint64_t salt)
+{
+    if (!(a.debug & AR_DEBUG_JITTER)) return;
+    uint64_t h = salt * 0x9E3779B97F4A7C15ull;
+    h ^= h >> 29;
+    uint32_t n = (uint32_t)(h & 63u);
+    for (uint32_t i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(8);
+}
+
+// ---- per-wave ring state ---------------------------------------------------
+
+struct Ring {
+    const RingArgs *a;
+    uint32_t N, r, c, w;
+    uint64_t *tail_out, *head_out;  // link r -> r+1: I write tail, read head
+    uint64_t *tail_in, *head_in;    // link r-1 -> r: I read tail, write head
+    char *fifo_out;
+    const char *fifo_in;
+    uint64_t m_out, m_in;           // absolute index of the next message out / in
+    uint64_t head_seen, tail_seen;  // last counter values observed
+};
+
+__device__ __forceinline__ char *slot_ptr(char *base, uint64_t m, const RingArgs &a)
+{
+    return base + (m % a.depth) * a.slot_bytes;
+}
+
+// Sender side: wait until the slot of message m_out is free, i.e. the
+// receiver has consumed message m_out - depth.
+__device__ __forceinline__ bool acquire_send_slot(Ring &g)
+{
+    const uint64_t d = g.a->depth;
+    if (g.m_out + 1 <= d) return true;  // first `depth` messages of the plan's life
+    return wait_geq(*g.a, g.head_out, g.m_out + 1 - d, g.head_seen);
+}
+
+__device__ __forceinline__ bool skip_this_post(const Ring &g)
+{
+    return (g.a->debug & AR_DEBUG_SKIP_POST) && g.c == 0 && g.w == 0 && g.r == 0 &&
+           g.m_out == g.a->epoch;
+}
+
+// ===================================================================== Simple
+//
+// Slot layout: the message's elements back to back, as fp32 partials during
+// the reduce-scatter (A*4 bytes per unit of A elements) and in the data type
+// during the all-gather (16 bytes per unit).  A unit is A elements = 16 bytes
+// of the data type; lanes take consecutive units, U units per lane per batch,
+// all loads of a batch before its stores.
+
+template <int DT, int KIND>
+struct SimpleStep {
+    static constexpr uint32_t A = Elem<DT>::A;
+    static constexpr uint32_t E = Elem<DT>::E;
+    static constexpr uint32_t RSV = A / 4;  // 16-byte fp32 vectors per unit on the RS wire
+    static constexpr bool kRecvRS = KIND == kRecvReduceSend || KIND == kRecvReduceCopySend;
+    static constexpr bool kRecvAG = KIND == kRecvCopySend || KIND == kRecvCopy;
+    static constexpr bool kLoadIn = KIND == kSend || kRecvRS;
+    static constexpr bool kSendRS = KIND == kSend || KIND == kRecvReduceSend;
+    static constexpr bool kSendAG = KIND == kRecvReduceCopySend || KIND == kRecvCopySend;
+    static constexpr bool kWriteOut = KIND == kRecvReduceCopySend || kRecvAG;
+    static constexpr int U = 4;
+
+    // Partial last unit of the buffer: element-wise data accesses.
+    __device__ static u32x4 load_in_partial(Rsrc r, uint32_t off, uint32_t valid)
+    {
+        u32x4 v = {0, 0, 0, 0};
+        if (E == 4) {
+            for (uint32_t i = 0; i < valid; ++i) v[i] = ld32<kInPol>(r, off + 4 * i);
+        } else {
+            for (uint32_t i = 0; i < valid; ++i) {
+                uint32_t h = ld16<kInPol>(r, off + 2 * i);
+                v[i >> 1] |= (i & 1) ? (h << 16) : h;
+            }
+        }
+        return v;
+    }
+    __device__ static void store_out_partial(Rsrc r, uint32_t off, u32x4 v, uint32_t valid)
+    {
+        if (E == 4) {
+            for (uint32_t i = 0; i < valid; ++i) st32<kOutPol>(r, off + 4 * i, v[i]);
+        } else {
+            for (uint32_t i = 0; i < valid; ++i) st16<kOutPol>(r, off + 2 * i, (i & 1) ? (v[i >> 1] >> 16) : (v[i >> 1] & 0xFFFFu));
+        }
+    }
+
+    // acc[A] = RS wire partials + widened input (or just the input at k = 0).
+    __device__ static void reduce(const u32x4 *rs, u32x4 in, float *acc)
+    {
+        if (E == 4) {
+            for (int i = 0; i < 4; ++i) acc[i] = as_f32(in[i]);
+        } else {
+            for (int i = 0; i < 4; ++i) {
+                acc[2 * i] = bf16_lo(in[i]);
+                acc[2 * i + 1] = bf16_hi(in[i]);
+            }
+        }
+        if (kRecvRS) {
+            for (uint32_t v = 0; v < RSV; ++v)
+                for (int i = 0; i < 4; ++i) acc[4 * v + i] = as_f32(rs[v][i]) + acc[4 * v + i];
+        }
+    }
+
+    __device__ static void unit(Rsrc rin, Rsrc rout, Rsrc wi, Rsrc wo, uint32_t u, uint32_t valid,
+                                const u32x4 &in, const u32x4 *rs, const u32x4 &ag)
+    {
+        (void)rin;
+        float acc[A];
+        if (kSendRS || KIND == kRecvReduceCopySend) reduce(rs, in, acc);
+        if (kSendRS) {
+            for (uint32_t v = 0; v < RSV; ++v) {
+                u32x4 o = {as_u32(acc[4 * v]), as_u32(acc[4 * v + 1]), as_u32(acc[4 * v + 2]),
+                           as_u32(acc[4 * v + 3])};
+                st128<kFifoPol>(wo, u * (A * 4) + 16 * v, o);
+            }
+        }
+        u32x4 y;
+        if (KIND == kRecvReduceCopySend) {
+            if (E == 4) {
+                y = u32x4{as_u32(acc[0]), as_u32(acc[1]), as_u32(acc[2]), as_u32(acc[3])};
+            } else {
+                for (int i = 0; i < 4; ++i) y[i] = pack_bf16(acc[2 * i], acc[2 * i + 1]);
+            }
+        } else {
+            y = ag;
+        }
+        if (kWriteOut) {
+            if (valid == A) st128<kOutPol>(rout, u * 16, y);
+            else store_out_partial(rout, u * 16, y, valid);
+        }
+        if (kSendAG) st128<kFifoPol>(wo, u * 16, y);
+        (void)wi;
+    }
+
+    __device__ static void run(const RingArgs &a, const char *src, char *dst, const char *rslot,
+                               char *wslot, uint32_t len)
+    {
+        const uint32_t lane = lane_id();
+        const uint32_t nfull = len / A, rem = len % A;
+        const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
+        const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
+        const Rsrc wi = make_rsrc(rslot, a.slot_bytes);
+        const Rsrc wo = make_rsrc(wslot, a.slot_bytes);
+        for (uint32_t base = 0; base < nfull; base += 64 * U) {
+            u32x4 in[U], rs[U][RSV], ag[U];
+#pragma unroll
+            for (int t = 0; t < U; ++t) {
+                const uint32_t u = base + 64 * t + lane;
+                if (u < nfull) {
+                    if (kLoadIn) in[t] = ld128<kInPol>(rin, u * 16);
+                    if (kRecvRS)
+                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoPol>(wi, u * (A * 4) + 16 * v);
+                    if (kRecvAG) ag[t] = ld128<kFifoPol>(wi, u * 16);
+                }
+            }
+#pragma unroll
+            for (int t = 0; t < U; ++t) {
+                const uint32_t u = base + 64 * t + lane;
+                if (u < nfull) unit(rin, rout, wi, wo, u, A, in[t], rs[t], ag[t]);
+            }
+        }
+        if (rem && lane == (nfull & 63u)) {
+            const uint32_t u = nfull;
+            u32x4 in = {0, 0, 0, 0}, rs[RSV], ag = {0, 0, 0, 0};
+            if (kLoadIn) in = load_in_partial(rin, u * 16, rem);
+            if (kRecvRS)
+                for (uint32_t v = 0; v < RSV; ++v) rs[v] = ld128<kFifoPol>(wi, u * (A * 4) + 16 * v);
+            if (kRecvAG) ag = ld128<kFifoPol>(wi, u * 16);
+            unit(rin, rout, wi, wo, u, rem, in, rs, ag);
+        }
+    }
+};
+
+template <int DT, int KIND>
+__device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst, uint32_t len)
+{
+    const RingArgs &a = *g.a;
+    constexpr bool recv = KIND != kSend;
+    constexpr bool send = KIND != kRecvCopy;
+    const char *rslot = nullptr;
+    char *wslot = nullptr;
+    if (recv) {
+        if (!wait_geq(a, g.tail_in, g.m_in + 1, g.tail_seen)) return false;
+        rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.m_in, a);
+    }
+    if (send) {
+        if (!acquire_send_slot(g)) return false;
+        wslot = slot_ptr(g.fifo_out, g.m_out, a);
+    }
+    SimpleStep<DT, KIND>::run(a, src, dst, rslot, wslot, len);
+    // Slot writes (and slot reads) complete before either counter moves.
+    drain_vmem();
+    if (send) {
+        debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
+        if (!skip_this_post(g) && lane_id() == 0) flag_store(g.tail_out, g.m_out + 1);
+        ++g.m_out;
+    }
+    if (recv) {
+        if (lane_id() == 0) flag_store(g.head_in, g.m_in + 1);
+        ++g.m_in;
+    }
+    return true;
+}
+
+// ========================================================================= LL
+//
+// 8-byte lines {u32 data, u32 flag}; flag = low 32 bits of (message index +
+// 1), never 0 (fresh memory) nor 0xFFFFFFFF (poison) because the host
+// restarts the epoch before it could wrap.  One 16-byte store carries two
+// lines, so a lane's 16-byte access is two complete lines.  Reduce-scatter
+// lines carry one fp32 partial each; all-gather lines carry one fp32 or two
+// bf16 values.  Lanes take "groups" of 8 data bytes (2 fp32 or 4 bf16):
+// input/output 8 bytes, RS wire G lines, AG wire 2 lines (16 bytes).
+
+template <int DT, int KIND>
+struct LLStep {
+    static constexpr uint32_t E = Elem<DT>::E;
+    static constexpr uint32_t G = 8 / E;         // elements per group
+    static constexpr uint32_t RSV = G / 2;       // 16-byte wire ops per group on the RS wire
+    static constexpr bool kRecvRS = KIND == kRecvReduceSend || KIND == kRecvReduceCopySend;
+    static constexpr bool kRecvAG = KIND == kRecvCopySend || KIND == kRecvCopy;
+    static constexpr bool kLoadIn = KIND == kSend || kRecvRS;
+    static constexpr bool kSendRS = KIND == kSend || KIND == kRecvReduceSend;
+    static constexpr bool kSendAG = KIND == kRecvReduceCopySend || KIND == kRecvCopySend;
+    static constexpr bool kWriteOut = KIND == kRecvReduceCopySend || kRecvAG;
+    static constexpr int U = 4;
+
+    __device__ static u32x2 load_in(Rsrc r, uint32_t q, uint32_t valid)
+    {
+        if (valid == G) return ld64<kInPol>(r, q * 8);
+        u32x2 v = {0, 0};
+        for (uint32_t i = 0; i < valid; ++i) {
+            if (E == 4) v[i] = ld32<kInPol>(r, q * 8 + 4 * i);
+            else v[i >> 1] |= ld16<kInPol>(r, q * 8 + 2 * i) << ((i & 1) * 16);
+        }
+        return v;
+    }
+    __device__ static void store_out(Rsrc r, uint32_t q, u32x2 v, uint32_t valid)
+    {
+        if (valid == G) {
+            st64<kOutPol>(r, q * 8, v);
+            return;
+        }
+        for (uint32_t i = 0; i < valid; ++i) {
+            if (E == 4) st32<kOutPol>(r, q * 8 + 4 * i, v[i]);
+            else st16<kOutPol>(r, q * 8 + 2 * i, (v[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu);
+        }
+    }
+
+    __device__ static bool lines_ok(const u32x4 &l, uint32_t tag) { return l[1] == tag && l[3] == tag; }
+
+    __device__ static bool run(const RingArgs &a, const char *src, char *dst, const char *rslot,
+                               char *wslot, uint32_t len, uint32_t tag_in, uint32_t tag_out)
+    {
+        const uint32_t lane = lane_id();
+        const uint32_t ng = (len + G - 1) / G;
+        const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
+        const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
+        const Rsrc wi = make_rsrc(rslot, a.slot_bytes);
+        const Rsrc wo = make_rsrc(wslot, a.slot_bytes);
+        for (uint32_t base = 0; base < ng; base += 64 * U) {
+            u32x2 in[U];
+            u32x4 rs[U][RSV], ag[U];
+            uint32_t valid[U];
+#pragma unroll
+            for (int t = 0; t < U; ++t) {
+                const uint32_t q = base + 64 * t + lane;
+                valid[t] = q < ng ? (len - q * G < G ? len - q * G : G) : 0;
+                if (valid[t]) {
+                    if (kLoadIn) in[t] = load_in(rin, q, valid[t]);
+                    if (kRecvRS)
+                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoPol>(wi, q * (G * 8) + 16 * v);
+                    if (kRecvAG) ag[t] = ld128<kFifoPol>(wi, q * 16);
+                }
+            }
+            if (kRecvRS || kRecvAG) {
+                // Spin until every line this wave needs carries the expected flag;
+                // only lanes with stale lines reload.
+                Watchdog wd;
+                while (true) {
+                    bool bad = false;
+#pragma unroll
+                    for (int t = 0; t < U; ++t) {
+                        if (!valid[t]) continue;
+                        if (kRecvRS)
+                            for (uint32_t v = 0; v < RSV; ++v) bad |= !lines_ok(rs[t][v], tag_in);
+                        if (kRecvAG) bad |= !lines_ok(ag[t], tag_in);
+                    }
+                    if (!__any(bad)) break;
+                    __builtin_amdgcn_s_sleep(1);
+                    if (watchdog_expired(a, wd)) return false;
+#pragma unroll
+                    for (int t = 0; t < U; ++t) {
+                        const uint32_t q = base + 64 * t + lane;
+                        if (!valid[t]) continue;
+                        if (kRecvRS)
+                            for (uint32_t v = 0; v < RSV; ++v)
+                                if (!lines_ok(rs[t][v], tag_in)) rs[t][v] = ld128<kFifoPol>(wi, q * (G * 8) + 16 * v);
+                        if (kRecvAG)
+                            if (!lines_ok(ag[t], tag_in)) ag[t] = ld128<kFifoPol>(wi, q * 16);
+                    }
+                }
+            }
+#pragma unroll
+            for (int t = 0; t < U; ++t) {
+                const uint32_t q = base + 64 * t + lane;
+                if (!valid[t]) continue;
+                float acc[G];
+                if (kSendRS || KIND == kRecvReduceCopySend) {
+                    if (E == 4) {
+                        acc[0] = as_f32(in[t][0]);
+                        acc[1] = as_f32(in[t][1]);
+                    } else {
+                        acc[0] = bf16_lo(in[t][0]);
+                        acc[1] = bf16_hi(in[t][0]);
+                        acc[2] = bf16_lo(in[t][1]);
+                        acc[3] = bf16_hi(in[t][1]);
+                    }
+                    if (kRecvRS) {
+                        for (uint32_t v = 0; v < RSV; ++v) {
+                            acc[2 * v] = as_f32(rs[t][v][0]) + acc[2 * v];
+                            acc[2 * v + 1] = as_f32(rs[t][v][2]) + acc[2 * v + 1];
+                        }
+                    }
+                }
+                if (kSendRS) {
+                    for (uint32_t v = 0; v < RSV; ++v) {
+                        u32x4 o = {as_u32(acc[2 * v]), tag_out, as_u32(acc[2 * v + 1]), tag_out};
+                        st128<kFifoPol>(wo, q * (G * 8) + 16 * v, o);
+                    }
+                }
+                u32x2 y;
+                if (KIND == kRecvReduceCopySend) {
+                    if (E == 4) y = u32x2{as_u32(acc[0]), as_u32(acc[1])};
+                    else y = u32x2{pack_bf16(acc[0], acc[1]), pack_bf16(acc[2], acc[3])};
+                } else {
+                    y = u32x2{ag[t][0], ag[t][2]};
+                }
+                if (kWriteOut) store_out(rout, q, y, valid[t]);
+                if (kSendAG) st128<kFifoPol>(wo, q * 16, u32x4{y[0], tag_out, y[1], tag_out});
+            }
+        }
+        return true;
+    }
+};
+
+template <int DT, int KIND>
+__device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uint32_t len)
+{
+    const RingArgs &a = *g.a;
+    constexpr bool recv = KIND != kSend;
+    constexpr bool send = KIND != kRecvCopy;
+    const char *rslot = nullptr;
+    char *wslot = nullptr;
+    if (recv) rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.m_in, a);
+    if (send) {
+        if (!acquire_send_slot(g)) return false;
+        wslot = slot_ptr(g.fifo_out, g.m_out, a);
+    }
+    if (send) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
+    // A skipped post writes the lines with the previous message's flag, which
+    // the receiver never accepts.
+    const bool skip = send && skip_this_post(g);
+    const uint32_t tag_out = (uint32_t)(skip ? g.m_out : g.m_out + 1);
+    if (!LLStep<DT, KIND>::run(a, src, dst, rslot, wslot, len, (uint32_t)(g.m_in + 1), tag_out)) return false;
+    if (send) ++g.m_out;
+    if (recv) {
+        // Every line of the message has been loaded and checked: the slot is free.
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        if (lane_id() == 0) flag_store(g.head_in, g.m_in + 1);
+        ++g.m_in;
+    }
+    return true;
+}
+
+// ====================================================================== LL128
+//
+// 128-byte lines: bytes 0..119 data, 120..127 a 64-bit flag (message index
+// + 1).  Eight lanes own one line: lanes p = 0..6 move 16 data bytes each,
+// lane 7 moves the last 8 data bytes and the flag.  A wave moves 8 lines per
+// instruction.  The writer stores the data of a batch of lines, waits for
+// those stores to complete, then stores the lines' flags; the reader loads
+// whole lines and accepts a batch once every line's flag matches.
+// Reduce-scatter lines hold 30 fp32 partials; all-gather lines hold 30 fp32
+// or 60 bf16 values.  A bf16 recvReduceCopySend re-lays its results from the
+// 30-per-line to the 60-per-line format through LDS.
+
+constexpr uint32_t kLL128Data = 120;
+
+template <int DT, int KIND>
+struct LL128Step {
+    static constexpr uint32_t E = Elem<DT>::E;
+    static constexpr bool kRecvRS = KIND == kRecvReduceSend || KIND == kRecvReduceCopySend;
+    static constexpr bool kRecvAG = KIND == kRecvCopySend || KIND == kRecvCopy;
+    static constexpr bool kLoadIn = KIND == kSend || kRecvRS;
+    static constexpr bool kSendRS = KIND == kSend || KIND == kRecvReduceSend;
+    static constexpr bool kSendAG = KIND == kRecvReduceCopySend || KIND == kRecvCopySend;
+    static constexpr bool kWriteOut = KIND == kRecvReduceCopySend || kRecvAG;
+    // bf16 recvReduceCopySend changes the line format on the way through.
+    static constexpr bool kRelayout = DT == AR_BFLOAT16 && KIND == kRecvReduceCopySend;
+    static constexpr int U = 4;
+
+    // Elements per line on the wire this step reads / writes.
+    static constexpr uint32_t kEplRS = kLL128Data / 4;  // 30 fp32 partials
+    static constexpr uint32_t kEplAG = kLL128Data / E;  // 30 fp32 or 60 bf16
+
+    // Data bytes lane p carries of one line, and the element count that is.
+    __device__ static uint32_t part_bytes(uint32_t p) { return p < 7 ? 16u : 8u; }
+
+    // Load `n` elements of size E from r at byte offset off into a 16-byte
+    // vector; n == full size uses one vector load.
+    __device__ static u32x4 load_elems(Rsrc r, uint32_t off, uint32_t n, uint32_t full)
+    {
+        u32x4 v = {0, 0, 0, 0};
+        if (n == full) {
+            const uint32_t bytes = full * E;
+            if (bytes == 16) return ld128<kInPol>(r, off);
+            if (bytes == 8) {
+                u32x2 h = ld64<kInPol>(r, off);
+                v[0] = h[0];
+                v[1] = h[1];
+                return v;
+            }
+            v[0] = ld32<kInPol>(r, off);
+            return v;
+        }
+        for (uint32_t i = 0; i < n; ++i) {
+            if (E == 4) v[i] = ld32<kInPol>(r, off + 4 * i);
+            else v[i >> 1] |= ld16<kInPol>(r, off + 2 * i) << ((i & 1) * 16);
+        }
+        return v;
+    }
+    __device__ static void store_elems(Rsrc r, uint32_t off, u32x4 v, uint32_t n, uint32_t full)
+    {
+        if (n == full) {
+            const uint32_t bytes = full * E;
+            if (bytes == 16) st128<kOutPol>(r, off, v);
+            else if (bytes == 8) st64<kOutPol>(r, off, u32x2{v[0], v[1]});
+            else st32<kOutPol>(r, off, v[0]);
+            return;
+        }
+        for (uint32_t i = 0; i < n; ++i) {
+            if (E == 4) st32<kOutPol>(r, off + 4 * i, v[i]);
+            else st16<kOutPol>(r, off + 2 * i, (v[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu);
+        }
+    }
+
+    // Write one lane's part of a line (data only; lane 7's flag comes later).
+    __device__ static void put_data(Rsrc wo, uint32_t line, uint32_t p, u32x4 d)
+    {
+        if (p < 7) st128<kFifoPol>(wo, line * 128 + 16 * p, d);
+        else st64<kFifoPol>(wo, line * 128 + 112, u32x2{d[0], d[1]});
+    }
+    __device__ static void put_flag(Rsrc wo, uint32_t line, uint64_t tag)
+    {
+        st64<kFifoPol>(wo, line * 128 + 120, u32x2{(uint32_t)tag, (uint32_t)(tag >> 32)});
+    }
+
+    // Reduce-scatter arithmetic for one lane part: n fp32 partials (<= 4)
+    // plus the lane's input elements.
+    __device__ static u32x4 rs_reduce(const u32x4 &wire, const u32x4 &in, uint32_t n)
+    {
+        float acc[4];
+        for (int i = 0; i < 4; ++i) {
+            if (E == 4) acc[i] = as_f32(in[i]);
+            else acc[i] = (i & 1) ? bf16_hi(in[i >> 1]) : bf16_lo(in[i >> 1]);
+        }
+        if (kRecvRS)
+            for (int i = 0; i < 4; ++i) acc[i] = as_f32(wire[i]) + acc[i];
+        (void)n;
+        return u32x4{as_u32(acc[0]), as_u32(acc[1]), as_u32(acc[2]), as_u32(acc[3])};
+    }
+
+    // Spin until the flags of the lines held in lines[] match tag.  Lane 7 of
+    // each line carries the flag in words 2..3; every lane of a line reloads
+    // when its line is stale.
+    template <int NB>
+    __device__ static bool await_lines(const RingArgs &a, Rsrc wi, u32x4 *lines, const uint32_t *line_of,
+                                       const bool *act, uint64_t tag)
+    {
+        const uint32_t lane = lane_id();
+        const uint32_t p = lane & 7u;
+        Watchdog wd;
+        while (true) {
+            uint64_t stale = 0;
+#pragma unroll
+            for (int t = 0; t < NB; ++t) {
+                bool bad = act[t] && p == 7 &&
+                           (((uint64_t)lines[t][3] << 32) | lines[t][2]) != tag;
+                stale |= __ballot(bad);
+            }
+            if (stale == 0) break;
+            __builtin_amdgcn_s_sleep(1);
+            if (watchdog_expired(a, wd)) return false;
+#pragma unroll
+            for (int t = 0; t < NB; ++t) {
+                bool bad = act[t] && p == 7 &&
+                           (((uint64_t)lines[t][3] << 32) | lines[t][2]) != tag;
+                uint64_t m = __ballot(bad);
+                if (act[t] && ((m >> (lane | 7u)) & 1u)) lines[t] = ld128<kFifoPol>(wi, line_of[t] * 128 + 16 * p);
+            }
+        }
+        after_observe();
+        return true;
+    }
+
+    __device__ static bool run(const RingArgs &a, const char *src, char *dst, const char *rslot,
+                               char *wslot, uint32_t len, uint64_t tag_in, uint64_t tag_out, uint32_t *lds)
+    {
+        const uint32_t lane = lane_id();
+        const uint32_t p = lane & 7u, ls = lane >> 3;
+        const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
+        const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
+        const Rsrc wi = make_rsrc(rslot, a.slot_bytes);
+        const Rsrc wo = make_rsrc(wslot, a.slot_bytes);
+        if (!kRelayout) {
+            // One line format in and out: the lane part maps to the same elements.
+            constexpr uint32_t epl = (kRecvRS || kSendRS) ? kEplRS : kEplAG;
+            constexpr uint32_t epart = 16 / ((kRecvRS || kSendRS) ? 4 : E);  // elements per full part
+            const uint32_t nlines = (len + epl - 1) / epl;
+            const uint32_t full = p < 7 ? epart : epart / 2;
+            for (uint32_t base = 0; base < nlines; base += 8 * U) {
+                u32x4 in[U], wire[U];
+                uint32_t line_of[U], nval[U];
+                bool act[U];
+#pragma unroll
+                for (int t = 0; t < U; ++t) {
+                    line_of[t] = base + 8 * t + ls;
+                    act[t] = line_of[t] < nlines;
+                    const uint32_t e0 = line_of[t] * epl + p * epart;
+                    nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
+                    if (kLoadIn && nval[t]) in[t] = load_elems(rin, e0 * E, nval[t], full);
+                    else in[t] = u32x4{0, 0, 0, 0};
+                    if ((kRecvRS || kRecvAG) && act[t]) wire[t] = ld128<kFifoPol>(wi, line_of[t] * 128 + 16 * p);
+                }
+                if (kRecvRS || kRecvAG) {
+                    if (!await_lines<U>(a, wi, wire, line_of, act, tag_in)) return false;
+                }
+#pragma unroll
+                for (int t = 0; t < U; ++t) {
+                    if (!act[t]) continue;
+                    const uint32_t e0 = line_of[t] * epl + p * epart;
+                    u32x4 out;
+                    if (kSendRS || KIND == kRecvReduceCopySend) out = rs_reduce(wire[t], in[t], nval[t]);
+                    else out = wire[t];
+                    if (kWriteOut && nval[t]) store_elems(rout, e0 * E, out, nval[t], full);
+                    if (kSendRS || kSendAG) put_data(wo, line_of[t], p, out);
+                }
+                if (kSendRS || kSendAG) {
+                    drain_vmem();
+#pragma unroll
+                    for (int t = 0; t < U; ++t)
+                        if (act[t] && p == 7) put_flag(wo, line_of[t], tag_out);
+                }
+            }
+            return true;
+        }
+        // bf16 recvReduceCopySend: 16 reduce-scatter lines (480 elements, two
+        // wave loads) become 8 all-gather lines (one wave store) per round.
+        const uint32_t nlines_ag = (len + kEplAG - 1) / kEplAG;
+        for (uint32_t agb = 0; agb < nlines_ag; agb += 8) {
+            // Phase 1: receive 16 RS lines, reduce, stage bf16 results in LDS.
+            u32x4 in[2], wire[2];
+            uint32_t line_of[2], nval[2];
+            bool act[2];
+            const uint32_t rs_nlines = (len + kEplRS - 1) / kEplRS;
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                line_of[t] = 2 * agb + 8 * t + ls;
+                act[t] = line_of[t] < rs_nlines;
+                const uint32_t e0 = line_of[t] * kEplRS + p * 4;
+                const uint32_t full = p < 7 ? 4u : 2u;
+                nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
+                in[t] = nval[t] ? load_elems(rin, e0 * E, nval[t], full) : u32x4{0, 0, 0, 0};
+                if (act[t]) wire[t] = ld128<kFifoPol>(wi, line_of[t] * 128 + 16 * p);
+            }
+            if (!await_lines<2>(a, wi, wire, line_of, act, tag_in)) return false;
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                // Element index of this lane's first value within the 480-block.
+                const uint32_t loc = (8 * t + ls) * kEplRS + p * 4;
+                u32x4 acc = rs_reduce(wire[t], in[t], nval[t]);
+                lds[loc / 2] = pack_bf16(as_f32(acc[0]), as_f32(acc[1]));
+                if (p < 7) lds[loc / 2 + 1] = pack_bf16(as_f32(acc[2]), as_f32(acc[3]));
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+            // Phase 2: read back in the 60-per-line layout, write output and AG line.
+            const uint32_t line = agb + ls;
+            const bool act2 = line < nlines_ag;
+            const uint32_t full = p < 7 ? 8u : 4u;
+            const uint32_t e0 = line * kEplAG + p * 8;
+            const uint32_t n2 = act2 && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
+            const uint32_t loc = ls * kEplAG + p * 8;
+            u32x4 y = {lds[loc / 2], lds[loc / 2 + 1], 0, 0};
+            if (p < 7) {
+                y[2] = lds[loc / 2 + 2];
+                y[3] = lds[loc / 2 + 3];
+            }
+            if (n2) store_elems(rout, e0 * E, y, n2, full);
+            if (act2) put_data(wo, line, p, y);
+            drain_vmem();
+            if (act2 && p == 7) put_flag(wo, line, tag_out);
+            // LDS is rewritten by the next round only after every lane has read it.
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        }
+        return true;
+    }
+};
+
+constexpr uint32_t kLdsWordsPerWave = 240;  // 480 bf16 values
+
+template <int DT, int KIND>
+__device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, uint32_t len, uint32_t *lds)
+{
+    const RingArgs &a = *g.a;
+    constexpr bool recv = KIND != kSend;
+    constexpr bool send = KIND != kRecvCopy;
+    const char *rslot = nullptr;
+    char *wslot = nullptr;
+    if (recv) rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.m_in, a);
+    if (send) {
+        if (!acquire_send_slot(g)) return false;
+        wslot = slot_ptr(g.fifo_out, g.m_out, a);
+    }
+    if (send) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
+    const bool skip = send && skip_this_post(g);
+    // A skipped post: write the data but a flag from the previous message.
+    const uint64_t tag_out = skip ? g.m_out : g.m_out + 1;
+    if (!LL128Step<DT, KIND>::run(a, src, dst, rslot, wslot, len, g.m_in + 1, tag_out, lds)) return false;
+    if (send) ++g.m_out;
+    if (recv) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        if (lane_id() == 0) flag_store(g.head_in, g.m_in + 1);
+        ++g.m_in;
+    }
+    return true;
+}
+
+// ===================================================================== kernel
+
+template <int PROTO, int DT, int KIND>
+__device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, uint32_t len, uint32_t *lds)
+{
+    if (PROTO == AR_PROTO_SIMPLE) return simple_step<DT, KIND>(g, src, dst, len);
+    if (PROTO == AR_PROTO_LL) return ll_step<DT, KIND>(g, src, dst, len);
+    return ll128_step<DT, KIND>(g, src, dst, len, lds);
+}
+
+template <int PROTO, int DT>
+__global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
+{
+    __shared__ uint32_t lds_all[(PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? AR_MAX_WAVES * kLdsWordsPerWave : 1];
+    constexpr uint32_t E = Elem<DT>::E;
+    const uint32_t N = a.nranks, C = a.nchannels, W = a.nwaves;
+    const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t b = blockIdx.x;
+    uint32_t c, r;
+    if (a.placement == AR_PLACE_CHANNEL_LOCAL) {
+        r = b / C;
+        c = b % C;
+    } else {
+        c = b / N;
+        r = b % N;
+    }
+    const uint32_t rprev = (r + N - 1) % N;
+    const uint64_t conn_out = ((uint64_t)c * W + w) * N + r;
+    const uint64_t conn_in = ((uint64_t)c * W + w) * N + rprev;
+
+    Ring g;
+    g.a = &a;
+    g.N = N;
+    g.r = r;
+    g.c = c;
+    g.w = w;
+    g.tail_out = a.flags + conn_out * kConnFlagU64;
+    g.head_out = g.tail_out + kFlagLineU64;
+    g.tail_in = a.flags + conn_in * kConnFlagU64;
+    g.head_in = g.tail_in + kFlagLineU64;
+    g.fifo_out = a.fifo + conn_out * a.depth * a.slot_bytes;
+    g.fifo_in = a.fifo + conn_in * a.depth * a.slot_bytes;
+    g.m_out = a.epoch;
+    g.m_in = a.epoch;
+    g.head_seen = 0;
+    g.tail_seen = 0;
+    uint32_t *lds = lds_all + ((PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? w * kLdsWordsPerWave : 0);
+
+    // A previous run that timed out leaves the abort word raised: do nothing.
+    if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT)) != 0)
+        return;
+
+    const char *src = a.src[r];
+    char *dst = a.dst[r];
+    for (uint32_t j = 0; j < a.nchunks; ++j) {
+        for (uint32_t k = 0; k <= 2 * N - 2; ++k) {
+            const uint32_t s = (r + 2 * N - k) % N;
+            const uint64_t seg_lo = (uint64_t)s * a.seg;
+            const uint64_t seg_hi = seg_lo + a.seg < a.count ? seg_lo + a.seg : a.count;
+            const uint64_t ch_lo = seg_lo + (uint64_t)c * a.cs;
+            uint64_t hi = ch_lo + a.cs < seg_hi ? ch_lo + a.cs : seg_hi;
+            const uint64_t ck_lo = ch_lo + (uint64_t)j * a.chunk;
+            if (ck_lo + a.chunk < hi) hi = ck_lo + a.chunk;
+            const uint64_t lo = ck_lo + (uint64_t)w * a.kw;
+            if (lo + a.kw < hi) hi = lo + a.kw;
+            const uint32_t len = hi > lo ? (uint32_t)(hi - lo) : 0u;
+            const uint64_t boff = (hi > lo ? lo : 0) * E;
+            const char *s_ptr = src + boff;
+            char *d_ptr = dst + boff;
+            bool ok;
+            if (k == 0) ok = do_step<PROTO, DT, kSend>(g, s_ptr, d_ptr, len, lds);
+            else if (k < N - 1) ok = do_step<PROTO, DT, kRecvReduceSend>(g, s_ptr, d_ptr, len, lds);
+            else if (k == N - 1) ok = do_step<PROTO, DT, kRecvReduceCopySend>(g, s_ptr, d_ptr, len, lds);
+            else if (k < 2 * N - 2) ok = do_step<PROTO, DT, kRecvCopySend>(g, s_ptr, d_ptr, len, lds);
+            else ok = do_step<PROTO, DT, kRecvCopy>(g, s_ptr, d_ptr, len, lds);
+            if (!ok) return;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ helpers
+
+__global__ void fill_u32_kernel(uint32_t *p, size_t n, uint32_t v)
+{
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+__global__ void copy_kernel(const uint32_t *src, uint32_t *dst, size_t nwords, const uint8_t *bsrc,
+                            uint8_t *bdst, size_t tail)
+{
+    const size_t i0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = i0; i < nwords; i += stride) dst[i] = src[i];
+    if (i0 < tail) bdst[i0] = bsrc[i0];
+}
+
+__global__ void bf16_round_kernel(const float *in, uint16_t *out, size_t n)
+{
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        out[i] = (uint16_t)bf16_rne(in[i]);
+}
+
+typedef void (*RingFn)(RingArgs);
+
+__host__ RingFn ring_fn(int proto, int dtype)
+{
+    if (dtype == AR_FLOAT32) {
+        if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, AR_FLOAT32>;
+        if (proto == AR_PROTO_LL128) return ring_kernel<AR_PROTO_LL128, AR_FLOAT32>;
+        return ring_kernel<AR_PROTO_SIMPLE, AR_FLOAT32>;
+    }
+    if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, AR_BFLOAT16>;
+    if (proto == AR_PROTO_LL128) return ring_kernel<AR_PROTO_LL128, AR_BFLOAT16>;
+    return ring_kernel<AR_PROTO_SIMPLE, AR_BFLOAT16>;
+}
+
+}  // namespace dev
+
+int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
+{
+    dev::RingFn fn = dev::ring_fn(info.proto, info.dtype);
+    RingArgs a = args;
+    void *kargs[] = {&a};
+    hipError_t e = hipLaunchKernel((const void *)fn, dim3((unsigned)info.grid), dim3((unsigned)info.block), kargs,
+                                   0, (hipStream_t)stream);
+    return e == hipSuccess ? AR_OK : AR_ERR_HIP;
+}
+
+int ring_occupancy(int proto, int dtype, int block, int *blocks_per_cu)
+{
+    dev::RingFn fn = dev::ring_fn(proto, dtype);
+    int n = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, (const void *)fn, block, 0);
+    if (e != hipSuccess) return AR_ERR_HIP;
+    *blocks_per_cu = n;
+    return AR_OK;
+}
+
+int launch_fill_u32(uint32_t *p, size_t n, uint32_t value, void *stream)
+{
+    if (n == 0) return AR_OK;
+    size_t blocks = (n + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(dev::fill_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, p, n, value);
+    return hipGetLastError() == hipSuccess ? AR_OK : AR_ERR_HIP;
+}
+
+int launch_copy(const void *src, void *dst, size_t bytes, void *stream)
+{
+    if (bytes == 0 || src == dst) return AR_OK;
+    const size_t nwords = bytes / 4, tail = bytes % 4;
+    size_t blocks = (nwords + 255) / 256;
+    if (blocks < 1) blocks = 1;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(dev::copy_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+                       (const uint32_t *)src, (uint32_t *)dst, nwords, (const uint8_t *)src + nwords * 4,
+                       (uint8_t *)dst + nwords * 4, tail);
+    return hipGetLastError() == hipSuccess ? AR_OK : AR_ERR_HIP;
+}
+
+int launch_bf16_round(const float *in, uint16_t *out, size_t n, void *stream)
+{
+    if (n == 0) return AR_OK;
+    size_t blocks = (n + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(dev::bf16_round_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, in, out, n);
+    return hipGetLastError() == hipSuccess ? AR_OK : AR_ERR_HIP;
+}
+
+}  // namespace ar

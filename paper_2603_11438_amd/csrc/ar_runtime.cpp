@@ -1,0 +1,298 @@
+// Plan lifetime, argument checking and launches of libar (C ABI in ar.h).
+#include <hip/hip_runtime.h>
+
+#include <new>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "ar.h"
+#include "ar_internal.h"
+
+using namespace ar;
+
+struct ar_plan_s {
+    ar_plan_info info;
+    ar_plan_desc desc;
+    int device;
+    char *ws;            // one allocation: control block, flags, FIFO
+    size_t ws_bytes;
+    uint32_t *ctl;
+    uint64_t *flags;
+    char *fifo;
+    uint64_t epoch;      // absolute index of the next run's first message
+    uint64_t timeout_ticks;
+    int sticky;          // host-side copy of a timeout seen by ar_plan_status
+};
+
+namespace {
+
+constexpr uint32_t kDefaultTimeoutUs = 2000000;  // 2 s per flag wait
+constexpr uint64_t kTicksPerUs = 100;            // 100 MHz real-time counter
+constexpr uint64_t kLLTagLimit = 0xFFFFFFF0ull;  // restart the epoch before 32-bit tags wrap
+
+template <typename T>
+T *fail(int code)
+{
+    set_last_error(code);
+    return nullptr;
+}
+
+int ret(int code)
+{
+    if (code != AR_OK) set_last_error(code);
+    return code;
+}
+
+size_t round_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
+
+int zero_workspace(ar_plan_t *p, void *stream)
+{
+    if (!p->ws) return AR_OK;
+    return launch_fill_u32((uint32_t *)p->ws, p->ws_bytes / 4, 0u, stream);
+}
+
+bool ranges_overlap(uintptr_t a, uintptr_t b, size_t n)
+{
+    return a < b + n && b < a + n;
+}
+
+// Validate rank buffers: non-NULL, 16-byte aligned, and no recv buffer
+// overlapping another rank's send or recv buffer.
+int check_buffers(const ar_plan_t *p, const void *const *send, void *const *recv)
+{
+    if (!send || !recv) return AR_ERR_ARG;
+    const int n = p->info.nranks;
+    const size_t bytes = p->info.count * (p->info.dtype == AR_FLOAT32 ? 4 : 2);
+    if (bytes == 0) return AR_OK;
+    for (int r = 0; r < n; ++r) {
+        if (!send[r] || !recv[r]) return AR_ERR_ARG;
+        if (((uintptr_t)send[r] | (uintptr_t)recv[r]) & 15u) return AR_ERR_ARG;
+        if (send[r] != recv[r] && ranges_overlap((uintptr_t)send[r], (uintptr_t)recv[r], bytes)) return AR_ERR_ARG;
+    }
+    for (int r = 0; r < n; ++r) {
+        for (int q = 0; q < n; ++q) {
+            if (q == r) continue;
+            if (ranges_overlap((uintptr_t)recv[r], (uintptr_t)recv[q], bytes)) return AR_ERR_ARG;
+            if (ranges_overlap((uintptr_t)recv[r], (uintptr_t)send[q], bytes)) return AR_ERR_ARG;
+        }
+    }
+    return AR_OK;
+}
+
+int device_channel_capacity(int proto, int dtype, int nranks, int nwaves, int *cap)
+{
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return AR_ERR_HIP;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return AR_ERR_HIP;
+    int rc = ring_occupancy(proto, dtype, 64 * nwaves, &per_cu);
+    if (rc != AR_OK) return rc;
+    long total = (long)per_cu * cus;
+    long ch = total / nranks;
+    if (ch > AR_MAX_CHANNELS) ch = AR_MAX_CHANNELS;
+    *cap = (int)ch;
+    return AR_OK;
+}
+
+int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *stream)
+{
+    if (!p) return ret(AR_ERR_ARG);
+    if (p->sticky) return ret(AR_ERR_STATE);
+    int rc = check_buffers(p, send, recv);
+    if (rc != AR_OK) return ret(rc);
+    const ar_plan_info &g = p->info;
+    const size_t bytes = g.count * (g.dtype == AR_FLOAT32 ? 4 : 2);
+    if (bytes == 0) return AR_OK;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev != p->device) return ret(AR_ERR_ARG);
+    if (g.grid == 0) {
+        // One rank: the sum is the input itself.
+        rc = launch_copy(send[0], recv[0], bytes, stream);
+        return ret(rc);
+    }
+    if (g.proto == AR_PROTO_LL && p->epoch + g.msgs_per_run + 2 >= kLLTagLimit) {
+        // 32-bit LL flags are about to wrap: start again from zeroed memory.
+        rc = zero_workspace(p, stream);
+        if (rc != AR_OK) return ret(rc);
+        p->epoch = 0;
+    }
+    RingArgs a;
+    memset(&a, 0, sizeof a);
+    for (int r = 0; r < g.nranks; ++r) {
+        a.src[r] = (const char *)send[r];
+        a.dst[r] = (char *)recv[r];
+    }
+    a.fifo = p->fifo;
+    a.flags = p->flags;
+    a.ctl = p->ctl;
+    a.count = g.count;
+    a.seg = g.seg_elems;
+    a.cs = g.chan_elems;
+    a.chunk = g.chunk_elems;
+    a.kw = g.wave_elems;
+    a.slot_bytes = g.slot_bytes;
+    a.epoch = p->epoch;
+    a.timeout_ticks = p->timeout_ticks;
+    a.nranks = (uint32_t)g.nranks;
+    a.nchannels = (uint32_t)g.nchannels;
+    a.nwaves = (uint32_t)g.nwaves;
+    a.depth = (uint32_t)g.fifo_depth;
+    a.nchunks = (uint32_t)g.nchunks;
+    a.placement = (uint32_t)g.placement;
+    a.debug = p->desc.debug_flags;
+    rc = launch_ring(g, a, stream);
+    if (rc != AR_OK) return ret(rc);
+    p->epoch += g.msgs_per_run;
+    return AR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ar_plan_t *ar_plan_ex(const ar_plan_desc *desc)
+{
+    if (!desc) return fail<ar_plan_t>(AR_ERR_ARG);
+    ar_plan_desc d = *desc;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return fail<ar_plan_t>(AR_ERR_HIP);
+
+    // Channel capacity for the tuner: co-resident workgroups / nranks, for
+    // the wave count the request implies (the default when the tuner picks).
+    int cap = AR_MAX_CHANNELS;
+    if (d.nranks >= 1 && d.nranks <= AR_MAX_RANKS && (d.dtype == AR_FLOAT32 || d.dtype == AR_BFLOAT16)) {
+        int probe_proto = d.proto == AR_PROTO_AUTO ? AR_PROTO_SIMPLE : d.proto;
+        if (probe_proto != AR_PROTO_LL && probe_proto != AR_PROTO_LL128 && probe_proto != AR_PROTO_SIMPLE)
+            return fail<ar_plan_t>(AR_ERR_ARG);
+        int rc = device_channel_capacity(probe_proto, d.dtype, d.nranks,
+                                         d.nwaves > 0 && d.nwaves <= AR_MAX_WAVES ? d.nwaves : default_nwaves(probe_proto),
+                                         &cap);
+        if (rc != AR_OK) return fail<ar_plan_t>(rc);
+        if (cap < 1) return fail<ar_plan_t>(AR_ERR_OCCUPANCY);
+    }
+    ar_plan_info info;
+    int rc = resolve_geometry(&d, cap, &info);
+    if (rc != AR_OK) return fail<ar_plan_t>(rc);
+    if (info.grid > 0) {
+        // Re-check co-residency for the resolved protocol and wave count.
+        int cap2 = 0;
+        rc = device_channel_capacity(info.proto, info.dtype, info.nranks, info.nwaves, &cap2);
+        if (rc != AR_OK) return fail<ar_plan_t>(rc);
+        if (info.nchannels > cap2) {
+            if (d.nchannels != 0) return fail<ar_plan_t>(AR_ERR_OCCUPANCY);
+            d.nchannels = cap2;
+            d.proto = info.proto;
+            d.chunk_bytes = info.chunk_elems * (info.dtype == AR_FLOAT32 ? 4 : 2);
+            d.nwaves = info.nwaves;
+            rc = resolve_geometry(&d, cap2, &info);
+            if (rc != AR_OK) return fail<ar_plan_t>(rc);
+        }
+    }
+
+    ar_plan_t *p = new (std::nothrow) ar_plan_t;
+    if (!p) return fail<ar_plan_t>(AR_ERR_NOMEM);
+    memset(p, 0, sizeof *p);
+    p->info = info;
+    p->desc = d;
+    p->device = dev;
+    const uint32_t tus = d.timeout_us ? d.timeout_us : kDefaultTimeoutUs;
+    p->timeout_ticks = (uint64_t)tus * kTicksPerUs;
+    if (info.grid > 0) {
+        const size_t ctl_bytes = 256;
+        const size_t flag_bytes = round_up(info.flag_bytes - kCtlU32 * 4, 256);
+        p->ws_bytes = ctl_bytes + flag_bytes + info.fifo_bytes;
+        if (hipMalloc((void **)&p->ws, p->ws_bytes) != hipSuccess) {
+            delete p;
+            return fail<ar_plan_t>(AR_ERR_NOMEM);
+        }
+        p->ctl = (uint32_t *)p->ws;
+        p->flags = (uint64_t *)(p->ws + ctl_bytes);
+        p->fifo = p->ws + ctl_bytes + flag_bytes;
+        if (hipMemset(p->ws, 0, p->ws_bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+            (void)hipFree(p->ws);
+            delete p;
+            return fail<ar_plan_t>(AR_ERR_HIP);
+        }
+    }
+    return p;
+}
+
+ar_plan_t *ar_plan(int nranks, size_t count, int dtype, int proto, int nchannels)
+{
+    ar_plan_desc d;
+    memset(&d, 0, sizeof d);
+    d.nranks = nranks;
+    d.count = count;
+    d.dtype = dtype;
+    d.proto = proto;
+    d.nchannels = nchannels;
+    return ar_plan_ex(&d);
+}
+
+int ar_run(ar_plan_t *plan, void *const *bufs, void *stream)
+{
+    return run_impl(plan, (const void *const *)bufs, bufs, stream);
+}
+
+int ar_run_oop(ar_plan_t *plan, const void *const *send, void *const *recv, void *stream)
+{
+    return run_impl(plan, send, recv, stream);
+}
+
+int ar_plan_status(ar_plan_t *p)
+{
+    if (!p) return ret(AR_ERR_ARG);
+    if (p->sticky) return AR_ERR_TIMEOUT;
+    if (!p->ctl) return AR_OK;
+    uint32_t st = 0;
+    if (hipMemcpy(&st, p->ctl + kCtlStatus, sizeof st, hipMemcpyDeviceToHost) != hipSuccess) return ret(AR_ERR_HIP);
+    if (st & kStatusTimeout) {
+        p->sticky = 1;
+        return AR_ERR_TIMEOUT;
+    }
+    return AR_OK;
+}
+
+int ar_plan_reset(ar_plan_t *p)
+{
+    if (!p) return ret(AR_ERR_ARG);
+    if (p->ws) {
+        if (hipDeviceSynchronize() != hipSuccess) return ret(AR_ERR_HIP);
+        if (hipMemset(p->ws, 0, p->ws_bytes) != hipSuccess) return ret(AR_ERR_HIP);
+        if (hipDeviceSynchronize() != hipSuccess) return ret(AR_ERR_HIP);
+    }
+    p->epoch = 0;
+    p->sticky = 0;
+    return AR_OK;
+}
+
+int ar_plan_poison(ar_plan_t *p, void *stream)
+{
+    if (!p) return ret(AR_ERR_ARG);
+    if (!p->fifo || p->info.fifo_bytes == 0) return AR_OK;
+    return ret(launch_fill_u32((uint32_t *)p->fifo, p->info.fifo_bytes / 4, 0xFFFFFFFFu, stream));
+}
+
+void ar_destroy(ar_plan_t *p)
+{
+    if (!p) return;
+    if (p->ws) (void)hipFree(p->ws);
+    delete p;
+}
+
+int ar_plan_get_info(const ar_plan_t *p, ar_plan_info *out)
+{
+    if (!p || !out) return ret(AR_ERR_ARG);
+    *out = p->info;
+    return AR_OK;
+}
+
+size_t ar_plan_workspace_bytes(const ar_plan_t *p) { return p ? p->ws_bytes : 0; }
+
+int ar_debug_bf16_round(const float *in, uint16_t *out, size_t n, void *stream)
+{
+    if (n && (!in || !out)) return ret(AR_ERR_ARG);
+    return ret(launch_bf16_round(in, out, n, stream));
+}
+
+}  // extern "C"

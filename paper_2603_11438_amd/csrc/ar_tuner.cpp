@@ -1,0 +1,303 @@
+// Tuner, plan geometry and error strings of libar: host-only C++ with no
+// HIP dependency, so it also builds (and is sanitizer-tested) with g++.
+//
+// Tuner semantics follow the paper's policy model (section 3.3: a policy
+// reads collective type, message size and rank count and writes algorithm,
+// protocol and channel count; section 4: outputs that cannot be honoured
+// fall back to the library's own choice, and the requested channel count is
+// clamped to the maximum the library passes in; section 5.3: the
+// size-aware policy picks one ring protocol for mid sizes and another for
+// large sizes).
+#include <atomic>
+#include <new>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "ar.h"
+#include "ar_internal.h"
+
+namespace ar {
+
+namespace {
+
+thread_local int g_last_error = AR_OK;
+
+struct TableRow {
+    int log2_bytes;
+    int proto;
+    int nchannels;
+    size_t chunk_bytes;
+    int nwaves;
+};
+
+#include "tuner_table.inc"
+
+constexpr int kTableRows = (int)(sizeof(kTable) / sizeof(kTable[0]));
+
+constexpr int kDefaultProto = AR_PROTO_SIMPLE;
+constexpr int kDefaultChannels = 16;
+constexpr size_t kMaxChunkBytes = 64u << 20;
+constexpr size_t kMinChunkBytes = 16;
+
+struct TunerSlot {
+    ar_tuner_fn fn;
+    void *user;
+};
+
+const TunerSlot kBuiltinSlot = {ar_tuner_table, nullptr};
+std::atomic<const TunerSlot *> g_active{&kBuiltinSlot};
+
+inline uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
+inline uint64_t round_up(uint64_t a, uint64_t b) { return ceil_div(a, b) * b; }
+
+bool valid_proto(int p) { return p == AR_PROTO_LL || p == AR_PROTO_LL128 || p == AR_PROTO_SIMPLE; }
+
+int clamp_int(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+size_t clamp_chunk(size_t c)
+{
+    if (c < kMinChunkBytes) c = kMinChunkBytes;
+    if (c > kMaxChunkBytes) c = kMaxChunkBytes;
+    return c / 16 * 16;
+}
+
+}  // namespace
+
+void set_last_error(int code) { g_last_error = code; }
+
+int default_nwaves(int proto)
+{
+    (void)proto;
+    return 4;
+}
+
+int default_depth(int proto) { return proto == AR_PROTO_SIMPLE ? 2 : 4; }
+
+size_t default_chunk_bytes(int proto)
+{
+    switch (proto) {
+    case AR_PROTO_LL: return 16u << 10;
+    case AR_PROTO_LL128: return 60u << 10;
+    default: return 256u << 10;
+    }
+}
+
+int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
+{
+    if (!d || !out) return AR_ERR_ARG;
+    if (d->nranks < 1 || d->nranks > AR_MAX_RANKS) return AR_ERR_ARG;
+    if (d->dtype != AR_FLOAT32 && d->dtype != AR_BFLOAT16) return AR_ERR_ARG;
+    if (d->proto != AR_PROTO_AUTO && !valid_proto(d->proto)) return AR_ERR_ARG;
+    if (d->nchannels < 0 || d->nchannels > AR_MAX_CHANNELS) return AR_ERR_ARG;
+    if (d->fifo_depth != 0 && (d->fifo_depth < 2 || d->fifo_depth > 16)) return AR_ERR_ARG;
+    if (d->nwaves < 0 || d->nwaves > AR_MAX_WAVES) return AR_ERR_ARG;
+    if (d->placement != AR_PLACE_RANK_SPREAD && d->placement != AR_PLACE_CHANNEL_LOCAL) return AR_ERR_ARG;
+    if (d->chunk_bytes > kMaxChunkBytes) return AR_ERR_ARG;
+    if (max_channels < 1) max_channels = 1;
+    if (max_channels > AR_MAX_CHANNELS) max_channels = AR_MAX_CHANNELS;
+    if (d->nchannels > max_channels) return AR_ERR_OCCUPANCY;
+
+    const uint64_t e = d->dtype == AR_FLOAT32 ? 4 : 2;
+    const uint64_t A = 16 / e;
+    // Per-rank byte counts stay below 2^46 so every byte offset fits easily.
+    if (d->count > (1ull << 44)) return AR_ERR_ARG;
+
+    int proto = d->proto, nch = d->nchannels, nw = d->nwaves;
+    size_t chunk = d->chunk_bytes;
+    if (proto == AR_PROTO_AUTO || nch == 0 || chunk == 0 || nw == 0) {
+        ar_tune_ctx ctx = {AR_COLL_ALLREDUCE, (size_t)(d->count * e), d->nranks, d->dtype,
+                           max_channels, 0};
+        ar_tune_out t;
+        int rc = ar_tune(&ctx, &t);
+        if (rc != AR_OK) return rc;
+        if (proto == AR_PROTO_AUTO) {
+            proto = t.proto;
+            // Channels, chunk and waves from the tuner belong to its protocol.
+            if (nch == 0) nch = t.nchannels;
+            if (chunk == 0) chunk = t.chunk_bytes;
+            if (nw == 0) nw = t.nwaves;
+        } else {
+            if (nch == 0) nch = t.proto == proto ? t.nchannels : clamp_int(kDefaultChannels, 1, max_channels);
+            if (chunk == 0) chunk = t.proto == proto ? t.chunk_bytes : default_chunk_bytes(proto);
+            if (nw == 0) nw = t.proto == proto ? t.nwaves : default_nwaves(proto);
+        }
+    }
+    chunk = clamp_chunk(chunk);
+    const int depth = d->fifo_depth ? d->fifo_depth : default_depth(proto);
+
+    ar_plan_info g = {};
+    g.nranks = d->nranks;
+    g.dtype = d->dtype;
+    g.proto = proto;
+    g.nchannels = nch;
+    g.nwaves = nw;
+    g.fifo_depth = depth;
+    g.placement = d->placement;
+    g.count = d->count;
+    g.block = 64 * nw;
+
+    const uint64_t N = (uint64_t)d->nranks;
+    g.seg_elems = round_up(ceil_div(d->count, N), A);
+    if (N == 1 || d->count == 0) {
+        // Nothing moves between ranks: no FIFOs, no launch of the ring kernel.
+        g.grid = 0;
+        *out = g;
+        return AR_OK;
+    }
+    g.grid = nch * d->nranks;
+    g.chan_elems = round_up(ceil_div(g.seg_elems, (uint64_t)nch), A);
+    uint64_t ck = round_up(chunk / e, A);
+    if (ck < A) ck = A;
+    if (ck > g.chan_elems) ck = g.chan_elems;
+    g.chunk_elems = ck;
+    g.nchunks = ceil_div(g.chan_elems, ck);
+    g.wave_elems = round_up(ceil_div(ck, (uint64_t)nw), A);
+
+    // Reduce-scatter partials are fp32 on the wire for both dtypes, so a slot
+    // is sized for wave_elems fp32 values in the protocol's line format.
+    uint64_t slot;
+    switch (proto) {
+    case AR_PROTO_LL: slot = g.wave_elems * 8; break;          // 4 B data + 4 B flag
+    case AR_PROTO_LL128: slot = ceil_div(g.wave_elems * 4, 120) * 128; break;
+    default: slot = g.wave_elems * 4; break;
+    }
+    g.slot_bytes = round_up(slot, 256);
+    const uint64_t conns = (uint64_t)nch * N * (uint64_t)nw;
+    g.fifo_bytes = conns * (uint64_t)depth * g.slot_bytes;
+    g.flag_bytes = conns * kConnFlagU64 * 8 + kCtlU32 * 4;
+    g.msgs_per_run = g.nchunks * (2 * N - 2);
+
+    // Wire bytes actually written per run: each element crosses 2(N-1) links,
+    // N-1 of them as an fp32 partial and N-1 as a finished value.
+    const uint64_t elems = d->count;
+    const double ag_e = (double)e;
+    double rs_bytes = (double)elems * 4.0 * (double)(N - 1);
+    double ag_bytes = (double)elems * ag_e * (double)(N - 1);
+    double w = proto == AR_PROTO_LL ? 2.0 : (proto == AR_PROTO_LL128 ? 128.0 / 120.0 : 1.0);
+    g.wire_bytes_per_run = (uint64_t)((rs_bytes + ag_bytes) * w);
+
+    // Sanity limits: 32-bit byte offsets inside a slot, bounded FIFO memory.
+    if (g.slot_bytes > (1ull << 31)) return AR_ERR_ARG;
+    if (g.fifo_bytes > (16ull << 30)) return AR_ERR_ARG;
+    *out = g;
+    return AR_OK;
+}
+
+}  // namespace ar
+
+using namespace ar;
+
+extern "C" {
+
+int ar_tuner_fixed_default(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
+{
+    (void)user;
+    if (!ctx || !out) return -1;
+    out->proto = kDefaultProto;
+    out->nchannels = kDefaultChannels;
+    out->chunk_bytes = 0;
+    out->nwaves = 0;
+    return 0;
+}
+
+int ar_tuner_noop(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
+{
+    (void)ctx;
+    (void)user;
+    if (!out) return -1;
+    out->proto = AR_PROTO_AUTO;
+    out->nchannels = 0;
+    out->chunk_bytes = 0;
+    out->nwaves = 0;
+    return 0;
+}
+
+int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
+{
+    (void)user;
+    if (!ctx || !out) return -1;
+    if (ctx->coll != AR_COLL_ALLREDUCE) {
+        // Only AllReduce is tabulated: defer to the default.
+        return ar_tuner_noop(ctx, out, nullptr);
+    }
+    int lg = 0;
+    while (lg < 63 && (1ull << lg) < (unsigned long long)ctx->msg_bytes) ++lg;
+    const TableRow *row = &kTable[0];
+    for (int i = 0; i < kTableRows; ++i) {
+        row = &kTable[i];
+        if (kTable[i].log2_bytes >= lg) break;
+    }
+    out->proto = row->proto;
+    out->nchannels = row->nchannels;
+    out->chunk_bytes = row->chunk_bytes;
+    out->nwaves = row->nwaves;
+    return 0;
+}
+
+int ar_set_tuner(ar_tuner_fn fn, void *user)
+{
+    if (!fn) {
+        g_active.store(&kBuiltinSlot, std::memory_order_release);
+        return AR_OK;
+    }
+    // Slots are immutable once published and never freed, so a decision
+    // that loaded the previous slot can still read it after the swap.
+    TunerSlot *s = new (std::nothrow) TunerSlot{fn, user};
+    if (!s) return AR_ERR_NOMEM;
+    g_active.store(s, std::memory_order_release);
+    return AR_OK;
+}
+
+int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out)
+{
+    if (!ctx || !out) return AR_ERR_ARG;
+    if (ctx->nranks < 1 || ctx->nranks > AR_MAX_RANKS) return AR_ERR_ARG;
+    if (ctx->dtype != AR_FLOAT32 && ctx->dtype != AR_BFLOAT16) return AR_ERR_ARG;
+    const int max_ch = clamp_int(ctx->max_channels > 0 ? ctx->max_channels : AR_MAX_CHANNELS, 1,
+                                 AR_MAX_CHANNELS);
+    const TunerSlot *slot = g_active.load(std::memory_order_acquire);
+    ar_tune_out t = {AR_PROTO_AUTO, 0, 0, 0};
+    int rc = slot->fn(ctx, &t, slot->user);
+
+    bool fallback = rc != 0 || !valid_proto(t.proto) || t.nchannels < 0 || t.nwaves < 0;
+    if (fallback) {
+        t.proto = kDefaultProto;
+        t.nchannels = kDefaultChannels;
+        t.chunk_bytes = 0;
+        t.nwaves = 0;
+    }
+    if (t.nchannels == 0) t.nchannels = kDefaultChannels;
+    t.nchannels = clamp_int(t.nchannels, 1, max_ch);
+    t.chunk_bytes = t.chunk_bytes ? clamp_chunk(t.chunk_bytes) : default_chunk_bytes(t.proto);
+    t.nwaves = t.nwaves ? clamp_int(t.nwaves, 1, AR_MAX_WAVES) : default_nwaves(t.proto);
+    *out = t;
+    return AR_OK;
+}
+
+int ar_plan_geometry(const ar_plan_desc *desc, ar_plan_info *out)
+{
+    if (!desc || !out) return AR_ERR_ARG;
+    int maxc = desc->max_channels > 0 ? desc->max_channels : AR_MAX_CHANNELS;
+    return resolve_geometry(desc, maxc, out);
+}
+
+const char *ar_strerror(int code)
+{
+    switch (code) {
+    case AR_OK: return "success";
+    case AR_ERR_ARG: return "invalid argument";
+    case AR_ERR_UNSUPPORTED: return "unsupported request";
+    case AR_ERR_NOMEM: return "out of memory";
+    case AR_ERR_HIP: return "HIP runtime error";
+    case AR_ERR_OCCUPANCY: return "grid cannot be co-resident on the device";
+    case AR_ERR_TIMEOUT: return "flag wait exceeded the watchdog";
+    case AR_ERR_STATE: return "plan is in an error state";
+    default: return "unknown error";
+    }
+}
+
+int ar_last_error(void) { return g_last_error; }
+
+int ar_version(void) { return AR_VERSION; }
+
+}  // extern "C"

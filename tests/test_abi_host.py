@@ -1,0 +1,230 @@
+"""Host-side checks of libar that need no GPU: the library loads and exports
+every entry point include/ar.h declares; the tuner validates, clamps and
+falls back; the plan geometry matches the oracle's segment rule; the
+bus-bandwidth formula matches the paper's own pair of numbers."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+import time
+
+import numpy as np
+import pytest
+
+import paper_2603_11438_amd as ar
+from oracle import ring_oracle as ro
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ar.h")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built_lib():
+    if not os.path.exists(ar.LIB_PATH):
+        import __graft_entry__
+
+        __graft_entry__.build()
+    ar.lib()
+    yield
+    ar.ar_set_tuner(None)
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = set(re.findall(r"\b(ar_[a-z0-9_]+)\s*\(", text))
+    # typedef'd function pointer type is not a symbol
+    names.discard("ar_tuner_fn")
+    return sorted(names)
+
+
+def test_every_declared_symbol_is_exported():
+    names = header_functions()
+    assert len(names) >= 20
+    L = ctypes.CDLL(ar.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+    # and the binding covers the same set
+    assert set(names) == set(ar.SIGNATURES), set(names) ^ set(ar.SIGNATURES)
+
+
+def test_version_and_strerror():
+    assert ar.ar_version() == 1
+    for code in range(8):
+        assert ar.ar_strerror(code)
+    assert ar.ar_strerror(99) == "unknown error"
+
+
+# ------------------------------------------------------------------ tuner
+
+def test_builtin_table_form():
+    # one decision per power-of-two bucket, small sizes latency-oriented
+    prev = None
+    for k in range(12, 28):
+        d = ar.ar_tune(1 << k)
+        assert d["proto"] in (ar.AR_PROTO_LL, ar.AR_PROTO_LL128, ar.AR_PROTO_SIMPLE)
+        assert 1 <= d["nchannels"] <= ar.AR_MAX_CHANNELS
+        assert d["chunk_bytes"] >= 16 and d["chunk_bytes"] % 16 == 0
+        assert 1 <= d["nwaves"] <= ar.AR_MAX_WAVES
+        # sizes between buckets use the next bucket up
+        if k > 12:
+            assert ar.ar_tune((1 << (k - 1)) + 1) == d
+        prev = d
+    # beyond the table: the last / first rows
+    assert ar.ar_tune(1 << 30) == ar.ar_tune(1 << 27)
+    assert ar.ar_tune(1) == ar.ar_tune(1 << 12)
+    assert prev is not None
+
+
+def test_fixed_default_and_noop():
+    ar.ar_set_tuner("fixed_default")
+    d = ar.ar_tune(1 << 20)
+    assert (d["proto"], d["nchannels"]) == (ar.AR_PROTO_SIMPLE, 16)
+    ar.ar_set_tuner("noop")
+    assert ar.ar_tune(1 << 20) == d  # no opinion -> the default
+    ar.ar_set_tuner(None)
+
+
+def test_max_channel_clamp():
+    ar.ar_set_tuner(lambda ctx: {"proto": ar.AR_PROTO_LL, "nchannels": 1000})
+    d = ar.ar_tune(1 << 20, max_channels=12)
+    assert d["proto"] == ar.AR_PROTO_LL and d["nchannels"] == 12
+    ar.ar_set_tuner(None)
+
+
+@pytest.mark.parametrize("bad", [
+    {"rc": 1, "proto": ar.AR_PROTO_LL, "nchannels": 4},   # tuner reports failure
+    {"proto": 7, "nchannels": 4},                          # protocol out of range
+    {"proto": ar.AR_PROTO_LL, "nchannels": -3},            # negative channels
+    None,                                                  # callback returns nothing
+])
+def test_invalid_tuner_output_falls_back(bad):
+    ar.ar_set_tuner(lambda ctx: bad)
+    d = ar.ar_tune(1 << 22)
+    assert (d["proto"], d["nchannels"]) == (ar.AR_PROTO_SIMPLE, 16)
+    ar.ar_set_tuner(None)
+
+
+def test_tuner_sees_context():
+    seen = {}
+
+    def t(ctx):
+        seen.update(ctx)
+        return {"proto": ar.AR_PROTO_LL128, "nchannels": 3, "chunk_bytes": 1000, "nwaves": 99}
+
+    ar.ar_set_tuner(t)
+    d = ar.ar_tune(12345, nranks=5, dtype="bf16", max_channels=40, comm_id=77)
+    ar.ar_set_tuner(None)
+    assert seen == {"coll": 0, "msg_bytes": 12345, "nranks": 5, "dtype": ar.AR_BFLOAT16,
+                    "max_channels": 40, "comm_id": 77}
+    assert d == {"proto": ar.AR_PROTO_LL128, "proto_name": "ll128", "nchannels": 3,
+                 "chunk_bytes": 992, "nwaves": ar.AR_MAX_WAVES}
+
+
+def test_tune_rejects_bad_context():
+    L = ar.lib()
+    out = ar.ar_tune_out()
+    assert L.ar_tune(None, ctypes.byref(out)) == ar.AR_ERR_ARG
+    ctx = ar.ar_tune_ctx(0, 100, 0, 0, 8, 0)
+    assert L.ar_tune(ctypes.byref(ctx), ctypes.byref(out)) == ar.AR_ERR_ARG
+    ctx = ar.ar_tune_ctx(0, 100, 8, 5, 8, 0)
+    assert L.ar_tune(ctypes.byref(ctx), ctypes.byref(out)) == ar.AR_ERR_ARG
+
+
+def test_tuner_decision_latency_is_small():
+    """Host decision cost (context for the paper's per-decision figures)."""
+    L = ar.lib()
+    ctx = ar.ar_tune_ctx(0, 1 << 23, 8, 0, 64, 0)
+    out = ar.ar_tune_out()
+    f = L.ar_tune
+    pc, po = ctypes.byref(ctx), ctypes.byref(out)
+    t0 = time.perf_counter()
+    for _ in range(20000):
+        f(pc, po)
+    dt = (time.perf_counter() - t0) / 20000
+    # dominated by the ctypes call itself; the C decision is tens of ns
+    assert dt < 50e-6
+
+
+# --------------------------------------------------------------- geometry
+
+@pytest.mark.parametrize("dtype", ("f32", "bf16"))
+def test_geometry_segment_rule_matches_oracle(dtype):
+    e = 4 if dtype == "f32" else 2
+    rng = np.random.default_rng(0)
+    counts = [1, 2, 3, 7, 8, 15, 16, 17, 1000, 1023, 1024, 4099, 65537] + list(rng.integers(1, 1 << 24, 20))
+    for n in (2, 3, 5, 8, 16):
+        for count in counts:
+            for proto in ("ll", "ll128", "simple"):
+                for nch in (1, 3, 16, 64):
+                    g = ar.ar_plan_geometry(ar.make_desc(n, int(count), dtype, proto, nch, 4096))
+                    A = 16 // e
+                    assert g["seg_elems"] == ro.segment_elems(n, int(count), e)
+                    assert g["grid"] == nch * n and g["block"] == 64 * g["nwaves"]
+                    assert g["chan_elems"] % A == 0 and g["chan_elems"] * nch >= g["seg_elems"]
+                    assert g["chunk_elems"] % A == 0 and g["chunk_elems"] <= g["chan_elems"]
+                    assert g["nchunks"] * g["chunk_elems"] >= g["chan_elems"]
+                    assert (g["nchunks"] - 1) * g["chunk_elems"] < g["chan_elems"]
+                    assert g["wave_elems"] * g["nwaves"] >= g["chunk_elems"]
+                    assert g["msgs_per_run"] == g["nchunks"] * (2 * n - 2)
+                    wire = {"ll": 8 * g["wave_elems"], "simple": 4 * g["wave_elems"],
+                            "ll128": -(-4 * g["wave_elems"] // 120) * 128}[proto]
+                    assert g["slot_bytes"] >= wire and g["slot_bytes"] % 256 == 0
+                    conns = nch * n * g["nwaves"]
+                    assert g["fifo_bytes"] == conns * g["fifo_depth"] * g["slot_bytes"]
+
+
+def test_geometry_trivial_cases():
+    g = ar.ar_plan_geometry(ar.make_desc(1, 1000, "f32", "simple", 4))
+    assert g["grid"] == 0 and g["fifo_bytes"] == 0
+    g = ar.ar_plan_geometry(ar.make_desc(8, 0, "f32", "simple", 4))
+    assert g["grid"] == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(nranks=0), ar.AR_ERR_ARG),
+    (dict(nranks=17), ar.AR_ERR_ARG),
+    (dict(dtype=5), ar.AR_ERR_ARG),
+    (dict(proto=9), ar.AR_ERR_ARG),
+    (dict(nchannels=-1), ar.AR_ERR_ARG),
+    (dict(nchannels=300), ar.AR_ERR_ARG),
+    (dict(fifo_depth=1), ar.AR_ERR_ARG),
+    (dict(nwaves=17), ar.AR_ERR_ARG),
+    (dict(placement=3), ar.AR_ERR_ARG),
+    (dict(chunk_bytes=1 << 30), ar.AR_ERR_ARG),
+    (dict(nchannels=20, max_channels=10), ar.AR_ERR_OCCUPANCY),
+])
+def test_geometry_errors(kw, code):
+    base = dict(nranks=8, count=1 << 20, dtype="f32", proto="simple", nchannels=4)
+    base.update(kw)
+    d = ar.make_desc(**base)
+    info = ar.ar_plan_info()
+    assert ar.lib().ar_plan_geometry(ctypes.byref(d), ctypes.byref(info)) == code
+
+
+def test_auto_geometry_uses_tuner():
+    ar.ar_set_tuner(lambda ctx: {"proto": ar.AR_PROTO_LL, "nchannels": 6, "chunk_bytes": 2048, "nwaves": 2})
+    g = ar.ar_plan_geometry(ar.make_desc(8, 1 << 20, "f32", "auto"))
+    ar.ar_set_tuner(None)
+    assert (g["proto"], g["nchannels"], g["chunk_elems"], g["nwaves"]) == (ar.AR_PROTO_LL, 6, 512, 2)
+
+
+# ------------------------------------------------------------- bandwidth
+
+def test_bus_bandwidth_matches_paper_pair():
+    # The paper quotes ~394 us for a 128 MiB 8-GPU AllReduce (section 5.1)
+    # and 596.9 GB/s bus bandwidth for it (section 5.3, Table 2): with
+    # busBW = S/t * 2(N-1)/N the two agree.
+    t = 128 * 2 ** 20 / (596.9e9 / (2 * 7 / 8))
+    assert abs(t * 1e6 - 394) < 1.0
+    assert abs(ar.bus_bandwidth(128 * 2 ** 20, 394e-6, 8) - 596.9) < 1.6
+
+
+def test_ring_byte_counts():
+    S = 1 << 20
+    assert ar.ring_bytes(S, 8, "f32", "simple") == 44 * S
+    assert ar.ring_bytes(S, 8, "f32", "ll") == 72 * S
+    assert abs(ar.ring_bytes(S, 8, "f32", "ll128") - (16 + 28 * 128 / 120) * S) < 1
+    assert ar.ring_bytes(S, 8, "bf16", "simple") == 58 * S
+    assert ar.compulsory_bytes(S, 8) == 16 * S
