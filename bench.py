@@ -1,0 +1,237 @@
+"""Benchmark: simulated-ring AllReduce on one MI355X.
+
+One step = one pass of the hot path on the resident synthetic input: the
+size-aware tuner decision (ar_tune) and one in-place AllReduce (ar_run) of
+8 simulated ranks.  Default workload: 8 ranks x 128 MiB fp32, uniform
+[-1, 1), the plan chosen by the built-in MI355X tuner table.
+
+Prints one JSON line.  `value` is the bus bandwidth (S / t * 2(N-1)/N, in
+GB/s = 1e9 B/s, S = bytes per rank); `roofline` prices the ring kernel's
+algorithmic bytes against MI355X's 8 TB/s HBM peak; `cpu_baseline` times
+the plain-C CPU oracle on the host on the same workload.
+
+Timing: W untimed warm-up steps, then K steps between HIP events recorded
+on the stream the kernel is launched on, with a device synchronisation on
+both sides.  Values grow across in-place steps (each step sums 8 copies);
+the kernel has no data-dependent control flow, so time does not depend on
+them.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SRC = os.path.join(ROOT, "paper_2603_11438_amd", "csrc", "ar_kernels.hip")
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def read_traffic(workload: str, proto: str) -> dict | None:
+    """HBM-side bytes per launch from a committed rocprofv3 counter summary,
+    or None when there is none or the kernel source has changed since."""
+    path = os.path.join(PROFILES, f"ring_{proto}_{workload}_pmc.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return {"bytes": float(vals["traffic_bytes_per_launch"]), "file": os.path.relpath(path, ROOT)}
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, target_s: float) -> dict:
+    """Time the plain-C CPU oracle (as it is) on the same workload."""
+    import numpy as np
+
+    from oracle import c_oracle
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 1)
+    x = wl.draw()
+    out = np.empty(wl.count, dtype=np.float32 if wl.dtype == "f32" else np.uint16)
+    c_oracle.allreduce(x, wl.dtype, nthreads=threads, out=out)  # warm-up (page faults)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        c_oracle.allreduce(x, wl.dtype, nthreads=threads, out=out)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= target_s or reps >= 1000:
+            break
+    t = el / reps
+    s = wl.bytes_per_rank
+    return {"value": round(s / t * 2 * (wl.nranks - 1) / wl.nranks / 1e9, 3), "unit": "GB/s",
+            "cores": threads, "kind": "oracle",
+            "sample": f"{reps} full passes of the plain-C oracle over the {wl.name} input "
+                      f"({wl.nranks} x {s} B {wl.dtype}), {threads} OpenMP threads, {el:.1f} s"}
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="D5", help="D1..D5 or a size in bytes for a D4 point")
+    ap.add_argument("--proto", default="auto")
+    ap.add_argument("--nchannels", type=int, default=0)
+    ap.add_argument("--chunk-bytes", type=int, default=0)
+    ap.add_argument("--nwaves", type=int, default=0)
+    ap.add_argument("--fifo-depth", type=int, default=0)
+    ap.add_argument("--placement", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU-baseline budget (0 = skip)")
+    ap.add_argument("--calibrate-copy", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (counter calibration)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build runs the simulated ring on a single MI355X "
+              f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2603_11438_amd as ar
+    import workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    torch.cuda.set_device(0)
+    ar.lib()
+
+    if args.workload in workloads.WORKLOADS:
+        wl = workloads.WORKLOADS[args.workload]
+    else:
+        wl = workloads.sweep_workload(int(args.workload))
+    n, count, dtype = wl.nranks, wl.count, wl.dtype
+    s_bytes = wl.bytes_per_rank
+
+    x = wl.draw()
+    import numpy as np
+
+    if dtype == "f32":
+        ts = [torch.from_numpy(np.ascontiguousarray(x[r])).to("cuda:0") for r in range(n)]
+    else:
+        ts = [torch.from_numpy(np.ascontiguousarray(x[r]).view(np.int16)).view(torch.bfloat16).to("cuda:0")
+              for r in range(n)]
+    del x
+
+    plan = ar.Plan(n, count, dtype, proto=args.proto, nchannels=args.nchannels, chunk_bytes=args.chunk_bytes,
+                   nwaves=args.nwaves, fifo_depth=args.fifo_depth, placement=args.placement)
+    info = plan.info
+    proto = info["proto_name"]
+    stream = torch.cuda.current_stream()
+    L = ar.lib()
+    import ctypes
+
+    ptrs = ar._ptr_array(ts)
+    ctx = ar.ar_tune_ctx(ar.AR_COLL_ALLREDUCE, s_bytes, n, ar.DTYPES[dtype], info["nchannels"], 0)
+    tout = ar.ar_tune_out()
+    sptr = stream.cuda_stream
+
+    def step():
+        L.ar_tune(ctypes.byref(ctx), ctypes.byref(tout))
+        rc = L.ar_run(plan.handle, ptrs, sptr)
+        if rc != ar.AR_OK:
+            raise ar.ARError(rc, "ar_run")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if plan.status() != ar.AR_OK:
+        raise RuntimeError("warm-up runs timed out")
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    # One untimed step keeps the GPU busy while the start event is enqueued,
+    # so the events bracket exactly the K timed kernels and no launch gap.
+    step()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = (time.perf_counter() - t_wall) / (args.steps + 1)
+    ms = e0.elapsed_time(e1) / args.steps
+    if plan.status() != ar.AR_OK:
+        raise RuntimeError("timed runs timed out")
+
+    if args.calibrate_copy:
+        nb = args.calibrate_copy << 20
+        src = torch.empty(nb // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        cp = ar.Plan(1, nb // 4, "f32", proto="simple", nchannels=1)
+        for _ in range(3):
+            cp.run_oop([src], [dst])
+        torch.cuda.synchronize()
+        cp.destroy()
+
+    t = ms / 1e3
+    busbw = ar.bus_bandwidth(s_bytes, t, n)
+    algbw = ar.alg_bandwidth(s_bytes, t)
+    b_ring = ar.ring_bytes(s_bytes, n, dtype, proto)
+    b_comp = ar.compulsory_bytes(s_bytes, n)
+    achieved = b_ring / t / 1e9
+    traffic = read_traffic(wl.name, proto)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": round(traffic["bytes"]) if traffic else None,
+                "kernel": f"ring_kernel<{proto}, {dtype}>",
+                "algorithmic_bytes_per_launch": b_ring,
+                "achieved_compulsory": round(b_comp / t / 1e9, 1),
+                "frac_compulsory": round(b_comp / t / 1e9 / HBM_PEAK_GBS, 4)}
+    if traffic:
+        roofline["traffic_source"] = traffic["file"]
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(wl, args.cpu_seconds)
+
+    line = {
+        "metric": "AllReduce busBW (8 simulated ranks, one MI355X)",
+        "value": round(busbw, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.note}", "nranks": n, "bytes_per_rank": s_bytes,
+                   "proto": proto, "nchannels": info["nchannels"], "chunk_bytes": info["chunk_elems"] * (4 if dtype == "f32" else 2),
+                   "nwaves": info["nwaves"], "fifo_depth": info["fifo_depth"], "placement": info["placement"],
+                   "parallelism": "simulated ring, 1 GPU"},
+        "algbw_gbs": round(algbw, 2),
+        "wall_ms_per_step": round(t_wall * 1e3, 4),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+    plan.destroy()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

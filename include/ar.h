@@ -79,8 +79,8 @@ enum {
 };
 
 /* Debug knobs (ar_plan_desc.debug_flags); zero in normal use.
- *   AR_DEBUG_SKIP_POST  channel 0 / wave 0 / rank 0 never announces its
- *                       first message, so its successor's wait runs into the
+ *   AR_DEBUG_SKIP_POST  channel 0 / wave 0 / rank 0 announces none of its
+ *                       messages, so its successor's wait runs into the
  *                       watchdog: every wave still exits and the run reports
  *                       AR_ERR_TIMEOUT.
  *   AR_DEBUG_JITTER     pseudo-random short sleeps before flag posts, to

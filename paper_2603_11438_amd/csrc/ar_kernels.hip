@@ -48,10 +48,32 @@ typedef uint32_t u32x2 __attribute__((__vector_size__(8)));
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 
 // Cache-policy operand of gfx950 buffer instructions.
-enum : int { kPolPlain = 0, kPolNt = 2, kPolSc1 = 16 };
-constexpr int kFifoPol = kPolSc1;   // device-coherent FIFO traffic
-constexpr int kInPol = kPolPlain;   // rank inputs
-constexpr int kOutPol = kPolPlain;  // rank outputs
+enum : int { kPolPlain = 0, kPolSc0 = 1, kPolNt = 2, kPolSc1 = 16 };
+#ifndef AR_FIFO_POL
+#define AR_FIFO_POL kPolSc1
+#endif
+#ifndef AR_FIFO_LD_POL
+#define AR_FIFO_LD_POL AR_FIFO_POL
+#endif
+#ifndef AR_FIFO_ST_POL
+#define AR_FIFO_ST_POL AR_FIFO_POL
+#endif
+#ifndef AR_IN_POL
+#define AR_IN_POL kPolNt
+#endif
+#ifndef AR_OUT_POL
+#define AR_OUT_POL kPolNt
+#endif
+#ifndef AR_SIMPLE_U
+#define AR_SIMPLE_U 4
+#endif
+#ifndef AR_LL128_GROUP
+#define AR_LL128_GROUP 4
+#endif
+constexpr int kFifoLd = AR_FIFO_LD_POL;  // device-coherent FIFO reads
+constexpr int kFifoSt = AR_FIFO_ST_POL;  // device-coherent FIFO writes
+constexpr int kInPol = AR_IN_POL;      // rank inputs: read once, streamed
+constexpr int kOutPol = AR_OUT_POL;    // rank outputs: written once, streamed
 
 enum Kind : int { kSend = 0, kRecvReduceSend, kRecvReduceCopySend, kRecvCopySend, kRecvCopy };
 
@@ -238,10 +260,12 @@ __device__ __forceinline__ bool acquire_send_slot(Ring &g)
     return wait_geq(*g.a, g.head_out, g.m_out + 1 - d, g.head_seen);
 }
 
+// Debug: channel 0 / wave 0 / rank 0 announces none of its messages, so its
+// successor waits until the watchdog fires (a monotone counter would let a
+// later post cover a single skipped one).
 __device__ __forceinline__ bool skip_this_post(const Ring &g)
 {
-    return (g.a->debug & AR_DEBUG_SKIP_POST) && g.c == 0 && g.w == 0 && g.r == 0 &&
-           g.m_out == g.a->epoch;
+    return (g.a->debug & AR_DEBUG_SKIP_POST) && g.c == 0 && g.w == 0 && g.r == 0;
 }
 
 // ===================================================================== Simple
@@ -263,7 +287,7 @@ struct SimpleStep {
     static constexpr bool kSendRS = KIND == kSend || KIND == kRecvReduceSend;
     static constexpr bool kSendAG = KIND == kRecvReduceCopySend || KIND == kRecvCopySend;
     static constexpr bool kWriteOut = KIND == kRecvReduceCopySend || kRecvAG;
-    static constexpr int U = 4;
+    static constexpr int U = AR_SIMPLE_U;
 
     // Partial last unit of the buffer: element-wise data accesses.
     __device__ static u32x4 load_in_partial(Rsrc r, uint32_t off, uint32_t valid)
@@ -315,7 +339,7 @@ struct SimpleStep {
             for (uint32_t v = 0; v < RSV; ++v) {
                 u32x4 o = {as_u32(acc[4 * v]), as_u32(acc[4 * v + 1]), as_u32(acc[4 * v + 2]),
                            as_u32(acc[4 * v + 3])};
-                st128<kFifoPol>(wo, u * (A * 4) + 16 * v, o);
+                st128<kFifoSt>(wo, u * (A * 4) + 16 * v, o);
             }
         }
         u32x4 y;
@@ -332,7 +356,7 @@ struct SimpleStep {
             if (valid == A) st128<kOutPol>(rout, u * 16, y);
             else store_out_partial(rout, u * 16, y, valid);
         }
-        if (kSendAG) st128<kFifoPol>(wo, u * 16, y);
+        if (kSendAG) st128<kFifoSt>(wo, u * 16, y);
         (void)wi;
     }
 
@@ -353,8 +377,8 @@ struct SimpleStep {
                 if (u < nfull) {
                     if (kLoadIn) in[t] = ld128<kInPol>(rin, u * 16);
                     if (kRecvRS)
-                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoPol>(wi, u * (A * 4) + 16 * v);
-                    if (kRecvAG) ag[t] = ld128<kFifoPol>(wi, u * 16);
+                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoLd>(wi, u * (A * 4) + 16 * v);
+                    if (kRecvAG) ag[t] = ld128<kFifoLd>(wi, u * 16);
                 }
             }
 #pragma unroll
@@ -368,8 +392,8 @@ struct SimpleStep {
             u32x4 in = {0, 0, 0, 0}, rs[RSV], ag = {0, 0, 0, 0};
             if (kLoadIn) in = load_in_partial(rin, u * 16, rem);
             if (kRecvRS)
-                for (uint32_t v = 0; v < RSV; ++v) rs[v] = ld128<kFifoPol>(wi, u * (A * 4) + 16 * v);
-            if (kRecvAG) ag = ld128<kFifoPol>(wi, u * 16);
+                for (uint32_t v = 0; v < RSV; ++v) rs[v] = ld128<kFifoLd>(wi, u * (A * 4) + 16 * v);
+            if (kRecvAG) ag = ld128<kFifoLd>(wi, u * 16);
             unit(rin, rout, wi, wo, u, rem, in, rs, ag);
         }
     }
@@ -473,8 +497,8 @@ struct LLStep {
                 if (valid[t]) {
                     if (kLoadIn) in[t] = load_in(rin, q, valid[t]);
                     if (kRecvRS)
-                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoPol>(wi, q * (G * 8) + 16 * v);
-                    if (kRecvAG) ag[t] = ld128<kFifoPol>(wi, q * 16);
+                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoLd>(wi, q * (G * 8) + 16 * v);
+                    if (kRecvAG) ag[t] = ld128<kFifoLd>(wi, q * 16);
                 }
             }
             if (kRecvRS || kRecvAG) {
@@ -499,9 +523,9 @@ struct LLStep {
                         if (!valid[t]) continue;
                         if (kRecvRS)
                             for (uint32_t v = 0; v < RSV; ++v)
-                                if (!lines_ok(rs[t][v], tag_in)) rs[t][v] = ld128<kFifoPol>(wi, q * (G * 8) + 16 * v);
+                                if (!lines_ok(rs[t][v], tag_in)) rs[t][v] = ld128<kFifoLd>(wi, q * (G * 8) + 16 * v);
                         if (kRecvAG)
-                            if (!lines_ok(ag[t], tag_in)) ag[t] = ld128<kFifoPol>(wi, q * 16);
+                            if (!lines_ok(ag[t], tag_in)) ag[t] = ld128<kFifoLd>(wi, q * 16);
                     }
                 }
             }
@@ -530,7 +554,7 @@ struct LLStep {
                 if (kSendRS) {
                     for (uint32_t v = 0; v < RSV; ++v) {
                         u32x4 o = {as_u32(acc[2 * v]), tag_out, as_u32(acc[2 * v + 1]), tag_out};
-                        st128<kFifoPol>(wo, q * (G * 8) + 16 * v, o);
+                        st128<kFifoSt>(wo, q * (G * 8) + 16 * v, o);
                     }
                 }
                 u32x2 y;
@@ -541,7 +565,7 @@ struct LLStep {
                     y = u32x2{ag[t][0], ag[t][2]};
                 }
                 if (kWriteOut) store_out(rout, q, y, valid[t]);
-                if (kSendAG) st128<kFifoPol>(wo, q * 16, u32x4{y[0], tag_out, y[1], tag_out});
+                if (kSendAG) st128<kFifoSt>(wo, q * 16, u32x4{y[0], tag_out, y[1], tag_out});
             }
         }
         return true;
@@ -563,7 +587,7 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
     }
     if (send) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
     // A skipped post writes the lines with the previous message's flag, which
-    // the receiver never accepts.
+    // the receiver never accepts for this message.
     const bool skip = send && skip_this_post(g);
     const uint32_t tag_out = (uint32_t)(skip ? g.m_out : g.m_out + 1);
     if (!LLStep<DT, KIND>::run(a, src, dst, rslot, wslot, len, (uint32_t)(g.m_in + 1), tag_out)) return false;
@@ -603,6 +627,8 @@ struct LL128Step {
     // bf16 recvReduceCopySend changes the line format on the way through.
     static constexpr bool kRelayout = DT == AR_BFLOAT16 && KIND == kRecvReduceCopySend;
     static constexpr int U = 4;
+    // Batches of U wave-wide line stores per drain-and-flag group.
+    static constexpr uint32_t kGroup = AR_LL128_GROUP;
 
     // Elements per line on the wire this step reads / writes.
     static constexpr uint32_t kEplRS = kLL128Data / 4;  // 30 fp32 partials
@@ -652,12 +678,12 @@ struct LL128Step {
     // Write one lane's part of a line (data only; lane 7's flag comes later).
     __device__ static void put_data(Rsrc wo, uint32_t line, uint32_t p, u32x4 d)
     {
-        if (p < 7) st128<kFifoPol>(wo, line * 128 + 16 * p, d);
-        else st64<kFifoPol>(wo, line * 128 + 112, u32x2{d[0], d[1]});
+        if (p < 7) st128<kFifoSt>(wo, line * 128 + 16 * p, d);
+        else st64<kFifoSt>(wo, line * 128 + 112, u32x2{d[0], d[1]});
     }
     __device__ static void put_flag(Rsrc wo, uint32_t line, uint64_t tag)
     {
-        st64<kFifoPol>(wo, line * 128 + 120, u32x2{(uint32_t)tag, (uint32_t)(tag >> 32)});
+        st64<kFifoSt>(wo, line * 128 + 120, u32x2{(uint32_t)tag, (uint32_t)(tag >> 32)});
     }
 
     // Reduce-scatter arithmetic for one lane part: n fp32 partials (<= 4)
@@ -701,7 +727,7 @@ struct LL128Step {
                 bool bad = act[t] && p == 7 &&
                            (((uint64_t)lines[t][3] << 32) | lines[t][2]) != tag;
                 uint64_t m = __ballot(bad);
-                if (act[t] && ((m >> (lane | 7u)) & 1u)) lines[t] = ld128<kFifoPol>(wi, line_of[t] * 128 + 16 * p);
+                if (act[t] && ((m >> (lane | 7u)) & 1u)) lines[t] = ld128<kFifoLd>(wi, line_of[t] * 128 + 16 * p);
             }
         }
         after_observe();
@@ -723,38 +749,42 @@ struct LL128Step {
             constexpr uint32_t epart = 16 / ((kRecvRS || kSendRS) ? 4 : E);  // elements per full part
             const uint32_t nlines = (len + epl - 1) / epl;
             const uint32_t full = p < 7 ? epart : epart / 2;
-            for (uint32_t base = 0; base < nlines; base += 8 * U) {
-                u32x4 in[U], wire[U];
-                uint32_t line_of[U], nval[U];
-                bool act[U];
+            // Lines are written in groups of kGroup batches; one drain per
+            // group makes the group's data complete before its flags go out.
+            for (uint32_t gbase = 0; gbase < nlines; gbase += 8 * U * kGroup) {
+                for (uint32_t base = gbase; base < gbase + 8 * U * kGroup && base < nlines; base += 8 * U) {
+                    u32x4 in[U], wire[U];
+                    uint32_t line_of[U], nval[U];
+                    bool act[U];
 #pragma unroll
-                for (int t = 0; t < U; ++t) {
-                    line_of[t] = base + 8 * t + ls;
-                    act[t] = line_of[t] < nlines;
-                    const uint32_t e0 = line_of[t] * epl + p * epart;
-                    nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
-                    if (kLoadIn && nval[t]) in[t] = load_elems(rin, e0 * E, nval[t], full);
-                    else in[t] = u32x4{0, 0, 0, 0};
-                    if ((kRecvRS || kRecvAG) && act[t]) wire[t] = ld128<kFifoPol>(wi, line_of[t] * 128 + 16 * p);
-                }
-                if (kRecvRS || kRecvAG) {
-                    if (!await_lines<U>(a, wi, wire, line_of, act, tag_in)) return false;
-                }
+                    for (int t = 0; t < U; ++t) {
+                        line_of[t] = base + 8 * t + ls;
+                        act[t] = line_of[t] < nlines;
+                        const uint32_t e0 = line_of[t] * epl + p * epart;
+                        nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
+                        if (kLoadIn && nval[t]) in[t] = load_elems(rin, e0 * E, nval[t], full);
+                        else in[t] = u32x4{0, 0, 0, 0};
+                        if ((kRecvRS || kRecvAG) && act[t]) wire[t] = ld128<kFifoLd>(wi, line_of[t] * 128 + 16 * p);
+                    }
+                    if (kRecvRS || kRecvAG) {
+                        if (!await_lines<U>(a, wi, wire, line_of, act, tag_in)) return false;
+                    }
 #pragma unroll
-                for (int t = 0; t < U; ++t) {
-                    if (!act[t]) continue;
-                    const uint32_t e0 = line_of[t] * epl + p * epart;
-                    u32x4 out;
-                    if (kSendRS || KIND == kRecvReduceCopySend) out = rs_reduce(wire[t], in[t], nval[t]);
-                    else out = wire[t];
-                    if (kWriteOut && nval[t]) store_elems(rout, e0 * E, out, nval[t], full);
-                    if (kSendRS || kSendAG) put_data(wo, line_of[t], p, out);
+                    for (int t = 0; t < U; ++t) {
+                        if (!act[t]) continue;
+                        const uint32_t e0 = line_of[t] * epl + p * epart;
+                        u32x4 out;
+                        if (kSendRS || KIND == kRecvReduceCopySend) out = rs_reduce(wire[t], in[t], nval[t]);
+                        else out = wire[t];
+                        if (kWriteOut && nval[t]) store_elems(rout, e0 * E, out, nval[t], full);
+                        if (kSendRS || kSendAG) put_data(wo, line_of[t], p, out);
+                    }
                 }
                 if (kSendRS || kSendAG) {
                     drain_vmem();
-#pragma unroll
-                    for (int t = 0; t < U; ++t)
-                        if (act[t] && p == 7) put_flag(wo, line_of[t], tag_out);
+                    const uint32_t gend = gbase + 8 * U * kGroup < nlines ? gbase + 8 * U * kGroup : nlines;
+                    if (p == 7)
+                        for (uint32_t line = gbase + ls; line < gend; line += 8) put_flag(wo, line, tag_out);
                 }
             }
             return true;
@@ -762,7 +792,8 @@ struct LL128Step {
         // bf16 recvReduceCopySend: 16 reduce-scatter lines (480 elements, two
         // wave loads) become 8 all-gather lines (one wave store) per round.
         const uint32_t nlines_ag = (len + kEplAG - 1) / kEplAG;
-        for (uint32_t agb = 0; agb < nlines_ag; agb += 8) {
+        for (uint32_t gbase = 0; gbase < nlines_ag; gbase += 8 * kGroup) {
+        for (uint32_t agb = gbase; agb < gbase + 8 * kGroup && agb < nlines_ag; agb += 8) {
             // Phase 1: receive 16 RS lines, reduce, stage bf16 results in LDS.
             u32x4 in[2], wire[2];
             uint32_t line_of[2], nval[2];
@@ -776,7 +807,7 @@ struct LL128Step {
                 const uint32_t full = p < 7 ? 4u : 2u;
                 nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
                 in[t] = nval[t] ? load_elems(rin, e0 * E, nval[t], full) : u32x4{0, 0, 0, 0};
-                if (act[t]) wire[t] = ld128<kFifoPol>(wi, line_of[t] * 128 + 16 * p);
+                if (act[t]) wire[t] = ld128<kFifoLd>(wi, line_of[t] * 128 + 16 * p);
             }
             if (!await_lines<2>(a, wi, wire, line_of, act, tag_in)) return false;
 #pragma unroll
@@ -804,12 +835,15 @@ struct LL128Step {
             }
             if (n2) store_elems(rout, e0 * E, y, n2, full);
             if (act2) put_data(wo, line, p, y);
-            drain_vmem();
-            if (act2 && p == 7) put_flag(wo, line, tag_out);
             // LDS is rewritten by the next round only after every lane has read it.
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        }
+        drain_vmem();
+        const uint32_t gend = gbase + 8 * kGroup < nlines_ag ? gbase + 8 * kGroup : nlines_ag;
+        if (p == 7)
+            for (uint32_t line = gbase + ls; line < gend; line += 8) put_flag(wo, line, tag_out);
         }
         return true;
     }

@@ -1,0 +1,226 @@
+"""Measure {protocol, channels, chunk, waves} per message size and derive the
+size -> decision table compiled into libar (csrc/tuner_table.inc).
+
+This is how the paper's size-aware policy is obtained (section 5.3: a sweep
+of the ring's choices per message size, then a per-size selection), redone
+on MI355X for the simulated ring.
+
+    python -m paper_2603_11438_amd.sweep measure --out sweep.jsonl
+    python -m paper_2603_11438_amd.sweep table sweep.jsonl --emit csrc/tuner_table.inc
+    python -m paper_2603_11438_amd.sweep validate --out validate.jsonl
+
+Selection rule per size: the highest median bus bandwidth wins; candidates
+within 2 % of the best count as ties and are broken by fewer channels, then
+fewer wire bytes (Simple < LL128 < LL), then smaller chunk, then fewer waves.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import paper_2603_11438_amd as ar
+
+SIZES = [1 << k for k in range(12, 28)]
+DEFAULT_CHUNK = 256 << 10   # the library's Simple chunk when no tuner opinion
+DEFAULT_WAVES = 4
+WIRE_RANK = {"simple": 0, "ll128": 1, "ll": 2}
+CHUNKS = {"ll": (4096, 16384, 65536), "ll128": (15360, 61440, 245760),
+          "simple": (16384, 65536, 262144, 1048576)}
+
+
+def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3):
+    import torch
+
+    for _ in range(warm):
+        plan.run(ts, stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    plan.run(ts, stream)
+    torch.cuda.synchronize()
+    one = max(time.perf_counter() - t0, 1e-6)
+    k = max(10, min(2000, int(min_total_s / one)))
+    out = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(k):
+            plan.run(ts, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out.append(e0.elapsed_time(e1) / k / 1e3)
+    if plan.status() != ar.AR_OK:
+        raise RuntimeError("timeout during sweep")
+    return out
+
+
+def grid(size, protos=("ll", "ll128", "simple"), channels=(1, 2, 4, 8, 16, 32, 64), waves=(2, 4, 8)):
+    for p in protos:
+        for c in channels:
+            for w in waves:
+                for k in CHUNKS[p]:
+                    # chunks far beyond a channel's share repeat the same geometry
+                    if k > 4 * max(size // 8 // c, 16) and k != CHUNKS[p][0]:
+                        continue
+                    yield dict(proto=p, nchannels=c, nwaves=w, chunk_bytes=k)
+
+
+def measure(args):
+    import torch
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    sizes = [int(s) for s in args.sizes.split(",")] if args.sizes else SIZES
+    n = args.nranks
+    with open(args.out, "a") as fo:
+        for size in sizes:
+            count = size // 4
+            g = torch.Generator(device="cuda:0").manual_seed(11438)
+            ts = [torch.rand(count, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
+            for cfg in grid(size):
+                try:
+                    plan = ar.Plan(n, count, "f32", **cfg)
+                except ar.ARError as e:
+                    continue
+                times = _timer(plan, ts, stream)
+                info = plan.info
+                med = statistics.median(times)
+                rec = {"size": size, "nranks": n, **cfg, "chunk_eff": info["chunk_elems"] * 4,
+                       "t_med_us": med * 1e6, "t_min_us": min(times) * 1e6, "t_max_us": max(times) * 1e6,
+                       "busbw": ar.bus_bandwidth(size, med, n)}
+                fo.write(json.dumps(rec) + "\n")
+                plan.destroy()
+            fo.flush()
+            print(f"sweep: size {size} done", flush=True)
+            del ts
+            torch.cuda.empty_cache()
+
+
+def default_row(size, rs, nranks=8):
+    """The measured row that has the fixed default's geometry (Simple, 16
+    channels, default chunk and waves), if the sweep contains it."""
+    g = ar.ar_plan_geometry(ar.make_desc(nranks, size // 4, "f32", "simple", 16, DEFAULT_CHUNK,
+                                         nwaves=DEFAULT_WAVES))
+    for r in rs:
+        if (r["proto"], r["nchannels"], r["nwaves"]) == ("simple", 16, DEFAULT_WAVES) and \
+                r["chunk_eff"] == g["chunk_elems"] * 4:
+            return r
+    return None
+
+
+def select(rows, tie=0.02):
+    """Per size: the highest median bus bandwidth; candidates within `tie` of
+    the best are ties, broken by fewer channels, fewer wire bytes, smaller
+    chunk, fewer waves.  When the fixed default is itself within `tie` of the
+    best, the row defers to it (the paper's policy also leaves sizes where
+    its choice does not help to the library default)."""
+    by = {}
+    for r in rows:
+        by.setdefault(r["size"], []).append(r)
+    table = {}
+    for size, rs in sorted(by.items()):
+        best = max(r["busbw"] for r in rs)
+        dflt = default_row(size, rs)
+        if dflt is not None and dflt["busbw"] >= (1 - tie) * best:
+            table[size] = dict(dflt, proto="default")
+            continue
+        ties = [r for r in rs if r["busbw"] >= (1 - tie) * best]
+        ties.sort(key=lambda r: (r["nchannels"], WIRE_RANK[r["proto"]], r["chunk_bytes"], r["nwaves"]))
+        table[size] = ties[0]
+    return table
+
+
+def emit(table, path):
+    names = {"ll": "AR_PROTO_LL", "ll128": "AR_PROTO_LL128", "simple": "AR_PROTO_SIMPLE",
+             "default": "AR_PROTO_AUTO"}
+    lines = [
+        "// MI355X size -> {protocol, channels, chunk, waves} table for 8-rank fp32",
+        "// AllReduce, one row per power-of-two message size (bytes per rank) from",
+        "// 4 KiB to 128 MiB.  A message of S bytes uses the row of the smallest size",
+        "// >= S (sizes below 4 KiB use the first row, above 128 MiB the last).",
+        "//",
+        "// Same form as the paper's size-aware policy (section 5.3: one protocol for",
+        "// the middle sizes, another for the large sizes); the values were measured",
+        "// on MI355X by paper_2603_11438_amd/sweep.py (highest median bus bandwidth,",
+        "// ties within 2% broken by fewer channels, fewer wire bytes, smaller chunk).",
+        "// AR_PROTO_AUTO rows defer to the fixed default (Simple, 16 channels): there",
+        "// the default measured within 2% of the best choice.",
+        "//",
+        "// columns: log2(size), proto, nchannels, chunk_bytes, nwaves   [busBW GB/s]",
+        "static const TableRow kTable[] = {",
+    ]
+    for size, r in sorted(table.items()):
+        lg = size.bit_length() - 1
+        if r["proto"] == "default":
+            lines.append(f"    {{{lg}, AR_PROTO_AUTO, 0, 0, 0}},  // {r['busbw']:.1f}")
+        else:
+            lines.append(f"    {{{lg}, {names[r['proto']]}, {r['nchannels']}, {r['chunk_bytes']}, {r['nwaves']}}},"
+                         f"  // {r['busbw']:.1f}")
+    lines.append("};")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def table_cmd(args):
+    rows = [json.loads(l) for l in open(args.jsonl) if l.strip()]
+    table = select(rows)
+    for size, r in sorted(table.items()):
+        print(f"{size:>10} {r['proto']:6} C={r['nchannels']:3} chunk={r['chunk_bytes']:8} W={r['nwaves']} "
+              f"busBW={r['busbw']:.1f}")
+    if args.emit:
+        emit(table, args.emit)
+
+
+def validate(args):
+    """Tuned table (ar_plan with AUTO) vs the fixed Simple/16 default, fresh repeats."""
+    import torch
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    n = args.nranks
+    with open(args.out, "a") as fo:
+        for size in SIZES:
+            count = size // 4
+            g = torch.Generator(device="cuda:0").manual_seed(11438 + 100)
+            ts = [torch.rand(count, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
+            res = {}
+            for name, tuner in (("tuned", None), ("default", "fixed_default")):
+                ar.ar_set_tuner(tuner)
+                plan = ar.Plan(n, count, "f32", proto="auto")
+                ar.ar_set_tuner(None)
+                times = _timer(plan, ts, stream, reps=7)
+                med = statistics.median(times)
+                res[name] = {"t_med_us": med * 1e6, "busbw": ar.bus_bandwidth(size, med, n),
+                             "cv": statistics.pstdev(times) / statistics.mean(times),
+                             "proto": plan.info["proto_name"], "nchannels": plan.info["nchannels"],
+                             "chunk": plan.info["chunk_elems"] * 4, "nwaves": plan.info["nwaves"]}
+                plan.destroy()
+            rec = {"size": size, **{f"{k}_{kk}": vv for k, v in res.items() for kk, vv in v.items()},
+                   "ratio": res["tuned"]["busbw"] / res["default"]["busbw"]}
+            fo.write(json.dumps(rec) + "\n")
+            print(json.dumps(rec), flush=True)
+            del ts
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    m = sub.add_parser("measure")
+    m.add_argument("--out", required=True)
+    m.add_argument("--sizes", default="")
+    m.add_argument("--nranks", type=int, default=8)
+    t = sub.add_parser("table")
+    t.add_argument("jsonl")
+    t.add_argument("--emit", default="")
+    v = sub.add_parser("validate")
+    v.add_argument("--out", required=True)
+    v.add_argument("--nranks", type=int, default=8)
+    args = ap.parse_args(argv)
+    {"measure": measure, "table": table_cmd, "validate": validate}[args.cmd](args)
+
+
+if __name__ == "__main__":
+    sys.exit(main())
