@@ -217,10 +217,33 @@ typedef struct ar_tune_out {
 typedef int (*ar_tuner_fn)(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);
 
 /* Make fn (with its user pointer) the active tuner; NULL restores the built-in
- * MI355X table.  The swap is one atomic pointer store: a decision already in
- * progress finishes with the old tuner.  fn and user must stay valid until
- * replaced. */
+ * MI355X table.  The swap is one atomic pointer exchange (paper section 4,
+ * hot reload): a decision already in progress finishes with the old tuner,
+ * the next one uses the new tuner, and no decision is lost.  Returns after
+ * every decision that was using the old tuner has finished, so the caller may
+ * then release the old tuner's code and data.  Thread-safe against
+ * concurrent ar_tune calls; concurrent swaps are serialised by the exchange
+ * (each one drains the tuner it replaced).  Must not be called from inside a
+ * tuner (it would wait for its own decision).  AR_ERR_NOMEM if the slot for
+ * the new tuner cannot be allocated. */
 int ar_set_tuner(ar_tuner_fn fn, void *user);
+
+/* Timings of one reload, nanoseconds. */
+typedef struct ar_reload_stats {
+    uint64_t validate_ns;  /* probing the candidate on the context grid */
+    uint64_t swap_ns;      /* the atomic exchange itself */
+    uint64_t drain_ns;     /* waiting for decisions still using the old tuner */
+    uint64_t probes;       /* contexts the candidate was called on */
+} ar_reload_stats;
+
+/* Checked hot reload (paper section 3.1 T1/T3, section 4): first call the
+ * candidate on a fixed grid of contexts (message sizes 0 B .. 1 GiB, 1..16
+ * ranks, both dtypes, several channel capacities); if any call returns
+ * non-zero or a malformed decision (unknown protocol, negative channels or
+ * waves, waves > AR_MAX_WAVES, chunk > 64 MiB), return AR_ERR_ARG and keep
+ * the current tuner untouched.  Otherwise behave as ar_set_tuner.  stats may
+ * be NULL.  A well-formed tuner that makes poor choices is accepted. */
+int ar_reload_tuner(ar_tuner_fn fn, void *user, ar_reload_stats *stats);
 
 /* Run the active tuner on *ctx, validate and clamp, and write a complete
  * decision to *out (proto, nchannels, chunk_bytes and nwaves all set).

@@ -68,6 +68,11 @@ class ar_tune_out(ctypes.Structure):
                 ("nwaves", ctypes.c_int)]
 
 
+class ar_reload_stats(ctypes.Structure):
+    _fields_ = [("validate_ns", ctypes.c_uint64), ("swap_ns", ctypes.c_uint64), ("drain_ns", ctypes.c_uint64),
+                ("probes", ctypes.c_uint64)]
+
+
 ar_tuner_fn = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.POINTER(ar_tune_ctx), ctypes.POINTER(ar_tune_out),
                                ctypes.c_void_p)
 
@@ -86,6 +91,7 @@ SIGNATURES = {
     "ar_plan_workspace_bytes": (ctypes.c_size_t, [_P]),
     "ar_plan_geometry": (ctypes.c_int, [ctypes.POINTER(ar_plan_desc), ctypes.POINTER(ar_plan_info)]),
     "ar_set_tuner": (ctypes.c_int, [ar_tuner_fn, _P]),
+    "ar_reload_tuner": (ctypes.c_int, [ar_tuner_fn, _P, ctypes.POINTER(ar_reload_stats)]),
     "ar_tune": (ctypes.c_int, [ctypes.POINTER(ar_tune_ctx), ctypes.POINTER(ar_tune_out)]),
     "ar_tuner_table": (ctypes.c_int, [ctypes.POINTER(ar_tune_ctx), ctypes.POINTER(ar_tune_out), _P]),
     "ar_tuner_fixed_default": (ctypes.c_int, [ctypes.POINTER(ar_tune_ctx), ctypes.POINTER(ar_tune_out), _P]),
@@ -179,9 +185,7 @@ def ar_tune(msg_bytes: int, nranks: int = 8, dtype="f32", max_channels: int = AR
 _tuner_refs = []  # keep ctypes callbacks alive while installed
 
 
-def ar_set_tuner(fn=None):
-    """Install a tuner: None (built-in table), a name ("table", "fixed_default",
-    "noop"), or a Python callable fn(ctx: dict) -> dict | None."""
+def _tuner_callback(fn):
     L = lib()
     if fn is None or fn == "table":
         cb = ctypes.cast(L.ar_tuner_table, ar_tuner_fn)
@@ -207,7 +211,21 @@ def ar_set_tuner(fn=None):
 
         cb = ar_tuner_fn(_trampoline)
     _tuner_refs.append(cb)
-    _check(L.ar_set_tuner(cb, None), "ar_set_tuner")
+    return cb
+
+
+def ar_set_tuner(fn=None):
+    """Install a tuner: None (built-in table), a name ("table", "fixed_default",
+    "noop"), or a Python callable fn(ctx: dict) -> dict | None."""
+    _check(lib().ar_set_tuner(_tuner_callback(fn), None), "ar_set_tuner")
+
+
+def ar_reload_tuner(fn=None) -> dict:
+    """Checked hot reload; raises ARError(AR_ERR_ARG) and keeps the current
+    tuner if the candidate answers malformed decisions on the probe grid."""
+    st = ar_reload_stats()
+    _check(lib().ar_reload_tuner(_tuner_callback(fn), None, ctypes.byref(st)), "ar_reload_tuner")
+    return {"validate_ns": st.validate_ns, "swap_ns": st.swap_ns, "drain_ns": st.drain_ns, "probes": st.probes}
 
 
 # ---- torch-facing helpers -------------------------------------------------

@@ -9,7 +9,9 @@
 // size-aware policy picks one ring protocol for mid sizes and another for
 // large sizes).
 #include <atomic>
+#include <chrono>
 #include <new>
+#include <thread>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -39,18 +41,115 @@ constexpr int kDefaultChannels = 16;
 constexpr size_t kMaxChunkBytes = 64u << 20;
 constexpr size_t kMinChunkBytes = 16;
 
+bool valid_proto(int p) { return p == AR_PROTO_LL || p == AR_PROTO_LL128 || p == AR_PROTO_SIMPLE; }
+
+// The active tuner is one atomic pointer to an immutable slot (paper section
+// 4, hot reload: an atomic function-pointer swap; a call already in progress
+// finishes with the old policy, the next call uses the new one).  Each slot
+// counts the decisions running through it, so a reload can wait until the
+// replaced slot has drained; slots are never freed (a late reader may still
+// touch the counter of a replaced slot), which costs one small allocation
+// per reload.
 struct TunerSlot {
     ar_tuner_fn fn;
     void *user;
+    std::atomic<int64_t> inflight{0};
 };
 
-const TunerSlot kBuiltinSlot = {ar_tuner_table, nullptr};
-std::atomic<const TunerSlot *> g_active{&kBuiltinSlot};
+TunerSlot g_builtin_slot{ar_tuner_table, nullptr};
+std::atomic<TunerSlot *> g_active{&g_builtin_slot};
+
+uint64_t now_ns()
+{
+    return (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+               std::chrono::steady_clock::now().time_since_epoch())
+        .count();
+}
+
+// Pin the active slot for one decision.  The increment and the re-check are
+// sequentially consistent, pairing with the exchange and the drain load in
+// install(): either the reload sees this reader in `inflight`, or this reader
+// sees the new slot and backs off.
+TunerSlot *pin_active()
+{
+    for (;;) {
+        TunerSlot *s = g_active.load(std::memory_order_seq_cst);
+        s->inflight.fetch_add(1, std::memory_order_seq_cst);
+        if (g_active.load(std::memory_order_seq_cst) == s) return s;
+        s->inflight.fetch_sub(1, std::memory_order_seq_cst);
+    }
+}
+
+void unpin(TunerSlot *s) { s->inflight.fetch_sub(1, std::memory_order_seq_cst); }
+
+bool out_valid(int rc, const ar_tune_out &o)
+{
+    if (rc != 0) return false;
+    if (o.proto != AR_PROTO_AUTO && !valid_proto(o.proto)) return false;
+    if (o.nchannels < 0 || o.nwaves < 0 || o.nwaves > AR_MAX_WAVES) return false;
+    return o.chunk_bytes <= kMaxChunkBytes;
+}
+
+// Load-time check of a candidate tuner: call it on a grid of contexts and
+// reject it if any answer is malformed (paper section 3.1, T1: verify once
+// at load time; a policy that is well-formed but makes poor choices still
+// passes, as in section 5.3).
+int probe_tuner(ar_tuner_fn fn, void *user, uint64_t *probes)
+{
+    static const size_t sizes[] = {0, 1, 4096, 65536, 1u << 20, 4u << 20, 32u << 20, 128u << 20, 1u << 30};
+    static const int ranks[] = {1, 2, 8, 16};
+    static const int maxch[] = {1, 64, AR_MAX_CHANNELS};
+    uint64_t n = 0;
+    for (size_t sz : sizes)
+        for (int nr : ranks)
+            for (int dt = 0; dt < 2; ++dt)
+                for (int mc : maxch) {
+                    ar_tune_ctx c = {AR_COLL_ALLREDUCE, sz, nr, dt, mc, 0};
+                    ar_tune_out o = {AR_PROTO_AUTO, 0, 0, 0};
+                    int rc = fn(&c, &o, user);
+                    ++n;
+                    if (!out_valid(rc, o)) {
+                        if (probes) *probes = n;
+                        return AR_ERR_ARG;
+                    }
+                }
+    if (probes) *probes = n;
+    return AR_OK;
+}
+
+int install(ar_tuner_fn fn, void *user, bool validate, ar_reload_stats *st)
+{
+    ar_reload_stats z = {0, 0, 0, 0};
+    uint64_t t0 = now_ns();
+    TunerSlot *ns = &g_builtin_slot;
+    if (fn) {
+        if (validate) {
+            int rc = probe_tuner(fn, user, &z.probes);
+            if (rc != AR_OK) {
+                z.validate_ns = now_ns() - t0;
+                if (st) *st = z;
+                return rc;
+            }
+        }
+        ns = new (std::nothrow) TunerSlot{fn, user};
+        if (!ns) return AR_ERR_NOMEM;
+    }
+    uint64_t t1 = now_ns();
+    TunerSlot *old = g_active.exchange(ns, std::memory_order_seq_cst);
+    uint64_t t2 = now_ns();
+    // Drain: decisions that pinned the old slot finish before we return, so
+    // the caller may release the old tuner's code and data afterwards.
+    while (old != ns && old->inflight.load(std::memory_order_seq_cst) != 0) std::this_thread::yield();
+    uint64_t t3 = now_ns();
+    z.validate_ns = t1 - t0;
+    z.swap_ns = t2 - t1;
+    z.drain_ns = t3 - t2;
+    if (st) *st = z;
+    return AR_OK;
+}
 
 inline uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
 inline uint64_t round_up(uint64_t a, uint64_t b) { return ceil_div(a, b) * b; }
-
-bool valid_proto(int p) { return p == AR_PROTO_LL || p == AR_PROTO_LL128 || p == AR_PROTO_SIMPLE; }
 
 int clamp_int(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
 
@@ -234,18 +333,11 @@ int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     return 0;
 }
 
-int ar_set_tuner(ar_tuner_fn fn, void *user)
+int ar_set_tuner(ar_tuner_fn fn, void *user) { return install(fn, user, false, nullptr); }
+
+int ar_reload_tuner(ar_tuner_fn fn, void *user, ar_reload_stats *stats)
 {
-    if (!fn) {
-        g_active.store(&kBuiltinSlot, std::memory_order_release);
-        return AR_OK;
-    }
-    // Slots are immutable once published and never freed, so a decision
-    // that loaded the previous slot can still read it after the swap.
-    TunerSlot *s = new (std::nothrow) TunerSlot{fn, user};
-    if (!s) return AR_ERR_NOMEM;
-    g_active.store(s, std::memory_order_release);
-    return AR_OK;
+    return install(fn, user, true, stats);
 }
 
 int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out)
@@ -255,9 +347,10 @@ int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out)
     if (ctx->dtype != AR_FLOAT32 && ctx->dtype != AR_BFLOAT16) return AR_ERR_ARG;
     const int max_ch = clamp_int(ctx->max_channels > 0 ? ctx->max_channels : AR_MAX_CHANNELS, 1,
                                  AR_MAX_CHANNELS);
-    const TunerSlot *slot = g_active.load(std::memory_order_acquire);
+    TunerSlot *slot = pin_active();
     ar_tune_out t = {AR_PROTO_AUTO, 0, 0, 0};
     int rc = slot->fn(ctx, &t, slot->user);
+    unpin(slot);
 
     bool fallback = rc != 0 || !valid_proto(t.proto) || t.nchannels < 0 || t.nwaves < 0;
     if (fallback) {
