@@ -107,7 +107,18 @@ typedef struct ar_plan_desc {
     uint32_t debug_flags;  /* AR_DEBUG_*; 0 in normal use */
     int max_channels;      /* geometry query only: device channel capacity
                               (0 = AR_MAX_CHANNELS); plans use the device's */
+    uint64_t comm_id;      /* communicator key passed to the tuner and used
+                              by the profiler hook (0 if unused) */
+    uint32_t flags;        /* AR_PLAN_* */
 } ar_plan_desc;
+
+/* Plan flags.
+ *   AR_PLAN_PROFILE  record each run's kernel duration (HIP events around the
+ *                    launch) into the telemetry map under desc.comm_id.  A
+ *                    run's sample is harvested without blocking by a later
+ *                    ar_run, or by ar_plan_status; a run whose predecessor's
+ *                    events are still pending is not timed. */
+enum { AR_PLAN_PROFILE = 1u };
 
 /* Resolved plan geometry (after the tuner and defaults). */
 typedef struct ar_plan_info {
@@ -255,6 +266,50 @@ int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out);
 int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);         /* MI355X size table */
 int ar_tuner_fixed_default(const ar_tune_ctx *ctx, ar_tune_out *out, void *user); /* Simple, 16 channels */
 int ar_tuner_noop(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);          /* defers: no opinion */
+
+/* ---- telemetry and the adaptive tuner (paper section 3.3, Listing 1: a
+ *      profiler writes latency into a shared typed map that the tuner reads;
+ *      section 5.3, composability) ----------------------------------------- */
+
+/* Latest sample of one communicator. */
+typedef struct ar_latency_state {
+    uint64_t comm_id;
+    uint64_t latency_ns;   /* duration of the sampled run (saturates at 2^48-1) */
+    int nchannels;         /* channel count the sampled run used */
+    uint64_t samples;      /* samples recorded for this communicator */
+} ar_latency_state;
+
+/* Profiler hook: store (latency_ns, nchannels) as the latest sample of
+ * comm_id in the fixed-size telemetry map (1024 communicators).  Thread-safe.
+ * AR_ERR_ARG for nchannels outside 0..65535, AR_ERR_NOMEM if the map is
+ * full. */
+int ar_profile_record(uint64_t comm_id, uint64_t latency_ns, int nchannels);
+
+/* Look up comm_id's latest sample; AR_ERR_ARG if it has none (callers must
+ * check, as a map lookup can come back empty). */
+int ar_profile_lookup(uint64_t comm_id, ar_latency_state *out);
+
+/* Forget every communicator (tuner state included).  Call only while no
+ * other thread records, looks up or tunes. */
+void ar_profile_clear(void);
+
+/* Configuration of ar_tuner_adaptive (its user pointer; NULL = defaults
+ * {2, 12, 9000, 4, AR_PROTO_SIMPLE}: 2 -> 12 channels in 90,000 decisions). */
+typedef struct ar_adaptive_cfg {
+    int min_channels;      /* conservative start and back-off level */
+    int max_channels;      /* ramp ceiling */
+    uint32_t ramp_calls;   /* uncontended decisions per +1 channel */
+    uint32_t backoff_ratio;/* contended when latency > ratio x the fastest
+                              latency seen at the same or fewer channels */
+    int proto;             /* protocol of every decision */
+} ar_adaptive_cfg;
+
+/* Closed-loop channel tuner over the telemetry of ctx->comm_id: with no
+ * samples it answers min_channels; otherwise it backs off to min_channels
+ * when the latest sample is contended and adds one channel every ramp_calls
+ * uncontended decisions up to max_channels.  Returns -1 (so ar_tune falls
+ * back) for an invalid configuration. */
+int ar_tuner_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);
 
 /* ---- errors and version ------------------------------------------------- */
 

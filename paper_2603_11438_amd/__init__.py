@@ -25,6 +25,7 @@ AR_PLACE_RANK_SPREAD, AR_PLACE_CHANNEL_LOCAL = 0, 1
 (AR_OK, AR_ERR_ARG, AR_ERR_UNSUPPORTED, AR_ERR_NOMEM, AR_ERR_HIP, AR_ERR_OCCUPANCY,
  AR_ERR_TIMEOUT, AR_ERR_STATE) = range(8)
 AR_DEBUG_SKIP_POST, AR_DEBUG_JITTER = 1, 2
+AR_PLAN_PROFILE = 1
 AR_MAX_RANKS, AR_MAX_CHANNELS, AR_MAX_WAVES = 16, 256, 16
 
 PROTOS = {"ll": AR_PROTO_LL, "ll128": AR_PROTO_LL128, "simple": AR_PROTO_SIMPLE, "auto": AR_PROTO_AUTO}
@@ -39,7 +40,7 @@ class ar_plan_desc(ctypes.Structure):
                 ("proto", ctypes.c_int), ("nchannels", ctypes.c_int), ("chunk_bytes", ctypes.c_size_t),
                 ("fifo_depth", ctypes.c_int), ("nwaves", ctypes.c_int), ("placement", ctypes.c_int),
                 ("timeout_us", ctypes.c_uint32), ("debug_flags", ctypes.c_uint32),
-                ("max_channels", ctypes.c_int)]
+                ("max_channels", ctypes.c_int), ("comm_id", ctypes.c_uint64), ("flags", ctypes.c_uint32)]
 
 
 class ar_plan_info(ctypes.Structure):
@@ -66,6 +67,16 @@ class ar_tune_ctx(ctypes.Structure):
 class ar_tune_out(ctypes.Structure):
     _fields_ = [("proto", ctypes.c_int), ("nchannels", ctypes.c_int), ("chunk_bytes", ctypes.c_size_t),
                 ("nwaves", ctypes.c_int)]
+
+
+class ar_latency_state(ctypes.Structure):
+    _fields_ = [("comm_id", ctypes.c_uint64), ("latency_ns", ctypes.c_uint64), ("nchannels", ctypes.c_int),
+                ("samples", ctypes.c_uint64)]
+
+
+class ar_adaptive_cfg(ctypes.Structure):
+    _fields_ = [("min_channels", ctypes.c_int), ("max_channels", ctypes.c_int), ("ramp_calls", ctypes.c_uint32),
+                ("backoff_ratio", ctypes.c_uint32), ("proto", ctypes.c_int)]
 
 
 class ar_reload_stats(ctypes.Structure):
@@ -96,6 +107,10 @@ SIGNATURES = {
     "ar_tuner_table": (ctypes.c_int, [ctypes.POINTER(ar_tune_ctx), ctypes.POINTER(ar_tune_out), _P]),
     "ar_tuner_fixed_default": (ctypes.c_int, [ctypes.POINTER(ar_tune_ctx), ctypes.POINTER(ar_tune_out), _P]),
     "ar_tuner_noop": (ctypes.c_int, [ctypes.POINTER(ar_tune_ctx), ctypes.POINTER(ar_tune_out), _P]),
+    "ar_profile_record": (ctypes.c_int, [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int]),
+    "ar_profile_lookup": (ctypes.c_int, [ctypes.c_uint64, ctypes.POINTER(ar_latency_state)]),
+    "ar_profile_clear": (None, []),
+    "ar_tuner_adaptive": (ctypes.c_int, [ctypes.POINTER(ar_tune_ctx), ctypes.POINTER(ar_tune_out), _P]),
     "ar_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "ar_last_error": (ctypes.c_int, []),
     "ar_version": (ctypes.c_int, []),
@@ -148,7 +163,7 @@ def _check(rc: int, what: str):
 
 def make_desc(nranks: int, count: int, dtype="f32", proto="auto", nchannels: int = 0, chunk_bytes: int = 0,
               fifo_depth: int = 0, nwaves: int = 0, placement: int = 0, timeout_us: int = 0,
-              debug_flags: int = 0, max_channels: int = 0) -> ar_plan_desc:
+              debug_flags: int = 0, max_channels: int = 0, comm_id: int = 0, flags: int = 0) -> ar_plan_desc:
     d = ar_plan_desc()
     d.nranks = nranks
     d.dtype = DTYPES[dtype] if isinstance(dtype, str) else dtype
@@ -162,6 +177,8 @@ def make_desc(nranks: int, count: int, dtype="f32", proto="auto", nchannels: int
     d.timeout_us = timeout_us
     d.debug_flags = debug_flags
     d.max_channels = max_channels
+    d.comm_id = comm_id
+    d.flags = flags
     return d
 
 
@@ -187,6 +204,8 @@ _tuner_refs = []  # keep ctypes callbacks alive while installed
 
 def _tuner_callback(fn):
     L = lib()
+    if fn == "adaptive":
+        return ctypes.cast(L.ar_tuner_adaptive, ar_tuner_fn)
     if fn is None or fn == "table":
         cb = ctypes.cast(L.ar_tuner_table, ar_tuner_fn)
     elif fn == "fixed_default":
@@ -214,10 +233,36 @@ def _tuner_callback(fn):
     return cb
 
 
-def ar_set_tuner(fn=None):
+_adaptive_cfgs = []
+
+
+def ar_set_tuner(fn=None, adaptive: Optional[dict] = None):
     """Install a tuner: None (built-in table), a name ("table", "fixed_default",
-    "noop"), or a Python callable fn(ctx: dict) -> dict | None."""
-    _check(lib().ar_set_tuner(_tuner_callback(fn), None), "ar_set_tuner")
+    "noop", "adaptive"), or a Python callable fn(ctx: dict) -> dict | None.
+    For "adaptive", `adaptive` may override ar_adaptive_cfg fields."""
+    user = None
+    if fn == "adaptive" and adaptive:
+        cfg = ar_adaptive_cfg(2, 12, 9000, 4, AR_PROTO_SIMPLE)
+        for k, v in adaptive.items():
+            setattr(cfg, k, v)
+        _adaptive_cfgs.append(cfg)
+        user = ctypes.cast(ctypes.byref(cfg), ctypes.c_void_p)
+    _check(lib().ar_set_tuner(_tuner_callback(fn), user), "ar_set_tuner")
+
+
+def ar_profile_record(comm_id: int, latency_ns: int, nchannels: int) -> None:
+    _check(lib().ar_profile_record(comm_id, latency_ns, nchannels), "ar_profile_record")
+
+
+def ar_profile_lookup(comm_id: int) -> Optional[dict]:
+    st = ar_latency_state()
+    if lib().ar_profile_lookup(comm_id, ctypes.byref(st)) != AR_OK:
+        return None
+    return {"comm_id": st.comm_id, "latency_ns": st.latency_ns, "nchannels": st.nchannels, "samples": st.samples}
+
+
+def ar_profile_clear() -> None:
+    lib().ar_profile_clear()
 
 
 def ar_reload_tuner(fn=None) -> dict:
@@ -263,9 +308,9 @@ class Plan:
 
     def __init__(self, nranks: int, count: int, dtype="f32", proto="auto", nchannels: int = 0,
                  chunk_bytes: int = 0, fifo_depth: int = 0, nwaves: int = 0, placement: int = 0,
-                 timeout_us: int = 0, debug_flags: int = 0):
+                 timeout_us: int = 0, debug_flags: int = 0, comm_id: int = 0, flags: int = 0):
         self.desc = make_desc(nranks, count, dtype, proto, nchannels, chunk_bytes, fifo_depth, nwaves,
-                              placement, timeout_us, debug_flags)
+                              placement, timeout_us, debug_flags, 0, comm_id, flags)
         L = lib()
         h = L.ar_plan_ex(ctypes.byref(self.desc))
         if not h:

@@ -23,6 +23,10 @@ struct ar_plan_s {
     uint64_t epoch;      // absolute index of the next run's first message
     uint64_t timeout_ticks;
     int sticky;          // host-side copy of a timeout seen by ar_plan_status
+    // Profiler hook (AR_PLAN_PROFILE): one pair of events around the last
+    // timed launch, harvested without blocking.
+    hipEvent_t ev_start, ev_stop;
+    bool ev_pending;
 };
 
 namespace {
@@ -94,6 +98,18 @@ int device_channel_capacity(int proto, int dtype, int nranks, int nwaves, int *c
     return AR_OK;
 }
 
+// If the last timed run has finished, record its duration as the plan's
+// latest telemetry sample.  Never blocks.
+void harvest_profile(ar_plan_t *p)
+{
+    if (!p->ev_pending) return;
+    if (hipEventQuery(p->ev_stop) != hipSuccess) return;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p->ev_start, p->ev_stop) == hipSuccess && ms >= 0.f)
+        (void)ar_profile_record(p->desc.comm_id, (uint64_t)((double)ms * 1e6), p->info.nchannels);
+    p->ev_pending = false;
+}
+
 int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *stream)
 {
     if (!p) return ret(AR_ERR_ARG);
@@ -140,8 +156,14 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
     a.nchunks = (uint32_t)g.nchunks;
     a.placement = (uint32_t)g.placement;
     a.debug = p->desc.debug_flags;
+    bool timed = false;
+    if (p->desc.flags & AR_PLAN_PROFILE) {
+        harvest_profile(p);
+        if (!p->ev_pending && hipEventRecord(p->ev_start, (hipStream_t)stream) == hipSuccess) timed = true;
+    }
     rc = launch_ring(g, a, stream);
     if (rc != AR_OK) return ret(rc);
+    if (timed && hipEventRecord(p->ev_stop, (hipStream_t)stream) == hipSuccess) p->ev_pending = true;
     p->epoch += g.msgs_per_run;
     return AR_OK;
 }
@@ -197,6 +219,12 @@ ar_plan_t *ar_plan_ex(const ar_plan_desc *desc)
     p->device = dev;
     const uint32_t tus = d.timeout_us ? d.timeout_us : kDefaultTimeoutUs;
     p->timeout_ticks = (uint64_t)tus * kTicksPerUs;
+    if (d.flags & AR_PLAN_PROFILE) {
+        if (hipEventCreate(&p->ev_start) != hipSuccess || hipEventCreate(&p->ev_stop) != hipSuccess) {
+            delete p;
+            return fail<ar_plan_t>(AR_ERR_HIP);
+        }
+    }
     if (info.grid > 0) {
         const size_t ctl_bytes = 256;
         const size_t flag_bytes = round_up(info.flag_bytes - kCtlU32 * 4, 256);
@@ -242,6 +270,7 @@ int ar_run_oop(ar_plan_t *plan, const void *const *send, void *const *recv, void
 int ar_plan_status(ar_plan_t *p)
 {
     if (!p) return ret(AR_ERR_ARG);
+    harvest_profile(p);
     if (p->sticky) return AR_ERR_TIMEOUT;
     if (!p->ctl) return AR_OK;
     uint32_t st = 0;
@@ -276,6 +305,8 @@ int ar_plan_poison(ar_plan_t *p, void *stream)
 void ar_destroy(ar_plan_t *p)
 {
     if (!p) return;
+    if (p->ev_start) (void)hipEventDestroy(p->ev_start);
+    if (p->ev_stop) (void)hipEventDestroy(p->ev_stop);
     if (p->ws) (void)hipFree(p->ws);
     delete p;
 }

@@ -192,6 +192,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     if (d->nwaves < 0 || d->nwaves > AR_MAX_WAVES) return AR_ERR_ARG;
     if (d->placement != AR_PLACE_RANK_SPREAD && d->placement != AR_PLACE_CHANNEL_LOCAL) return AR_ERR_ARG;
     if (d->chunk_bytes > kMaxChunkBytes) return AR_ERR_ARG;
+    if (d->flags & ~(uint32_t)AR_PLAN_PROFILE) return AR_ERR_ARG;
     if (max_channels < 1) max_channels = 1;
     if (max_channels > AR_MAX_CHANNELS) max_channels = AR_MAX_CHANNELS;
     if (d->nchannels > max_channels) return AR_ERR_OCCUPANCY;
@@ -205,7 +206,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     size_t chunk = d->chunk_bytes;
     if (proto == AR_PROTO_AUTO || nch == 0 || chunk == 0 || nw == 0) {
         ar_tune_ctx ctx = {AR_COLL_ALLREDUCE, (size_t)(d->count * e), d->nranks, d->dtype,
-                           max_channels, 0};
+                           max_channels, d->comm_id};
         ar_tune_out t;
         int rc = ar_tune(&ctx, &t);
         if (rc != AR_OK) return rc;

@@ -348,3 +348,57 @@ def test_device_bf16_rounding_matches_oracle(ar):
     torch.cuda.synchronize()
     got = got.cpu().numpy().view(np.uint16)
     assert np.array_equal(got, ro.f32_to_bf16_rne(f))
+
+
+# ------------------------------------------- profiler -> tuner closed loop
+
+def test_plan_profiler_hook_records_kernel_time(ar):
+    import torch
+
+    ar.ar_profile_clear()
+    n, count = 8, 1 << 20
+    x = draw(n, count, "f32", "uniform", seed=3)
+    ts = to_device(x, "f32")
+    plan = ar.Plan(n, count, "f32", proto="simple", nchannels=8, comm_id=777, flags=ar.AR_PLAN_PROFILE)
+    assert ar.ar_profile_lookup(777) is None
+    plan.run(ts)
+    torch.cuda.synchronize()
+    assert plan.status() == ar.AR_OK          # harvests the finished run
+    st = ar.ar_profile_lookup(777)
+    assert st is not None and st["nchannels"] == 8 and 1_000 < st["latency_ns"] < 100_000_000
+    assert_ranks_equal(ts, oracle_bits(x, "f32"), "f32", "profiled run")
+    plan.destroy()
+
+
+def test_closed_loop_adaptive_channels_on_gpu(ar):
+    """Per-call decisions from the adaptive tuner, fed by the plans' own
+    profiler hook: the channel count ramps from 2 to 12 and every result
+    stays bit-exact."""
+    import torch
+
+    ar.ar_profile_clear()
+    ar.ar_set_tuner("adaptive", adaptive={"ramp_calls": 3})
+    n, count, comm = 8, 1 << 20, 4242
+    x = draw(n, count, "f32", "uniform", seed=11)
+    want = oracle_bits(x, "f32")
+    base = to_device(x, "f32")
+    plans, seen = {}, []
+    try:
+        for _ in range(45):
+            d = ar.ar_tune(count * 4, n, "f32", comm_id=comm)
+            key = (d["proto"], d["nchannels"])
+            if key not in plans:
+                plans[key] = ar.Plan(n, count, "f32", proto=d["proto_name"], nchannels=d["nchannels"],
+                                     comm_id=comm, flags=ar.AR_PLAN_PROFILE)
+            p = plans[key]
+            ts = [t.clone() for t in base]
+            p.run(ts)
+            torch.cuda.synchronize()
+            assert p.status() == ar.AR_OK
+            assert_ranks_equal(ts, want, "f32", f"closed loop C={d['nchannels']}")
+            seen.append(d["nchannels"])
+    finally:
+        ar.ar_set_tuner(None)
+        for p in plans.values():
+            p.destroy()
+    assert seen[0] == 2 and seen[-1] == 12, seen
