@@ -3,7 +3,11 @@
 One step = one pass of the hot path on the resident synthetic input: the
 size-aware tuner decision (ar_tune) and one in-place AllReduce (ar_run) of
 8 simulated ranks.  Default workload: 8 ranks x 128 MiB fp32, uniform
-[-1, 1), the plan chosen by the built-in MI355X tuner table.
+[-1, 1).  By default the step runs the ring algorithm (reduce-scatter +
+all-gather through FIFOs) with the protocol, channels, chunk and waves the
+built-in MI355X tuner table chooses for the size; the line also reports the
+direct (two-shot) algorithm on the same input, which produces the same bits
+with only the compulsory bytes (`--algo direct` makes it the step).
 
 Prints one JSON line.  `value` is the bus bandwidth (S / t * 2(N-1)/N, in
 GB/s = 1e9 B/s, S = bytes per rank); `roofline` prices the ring kernel's
@@ -39,10 +43,10 @@ def kernel_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def read_traffic(workload: str, proto: str) -> dict | None:
+def read_traffic(workload: str, kernel: str) -> dict | None:
     """HBM-side bytes per launch from a committed rocprofv3 counter summary,
     or None when there is none or the kernel source has changed since."""
-    path = os.path.join(PROFILES, f"ring_{proto}_{workload}_pmc.txt")
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_pmc.txt")
     if not os.path.exists(path):
         return None
     vals = {}
@@ -90,6 +94,8 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="D5", help="D1..D5 or a size in bytes for a D4 point")
+    ap.add_argument("--algo", default="ring", choices=("ring", "direct", "auto"))
+    ap.add_argument("--compare-direct", type=int, default=1, help="also time the direct algorithm (ring runs)")
     ap.add_argument("--proto", default="auto")
     ap.add_argument("--nchannels", type=int, default=0)
     ap.add_argument("--chunk-bytes", type=int, default=0)
@@ -134,46 +140,71 @@ def main(argv=None) -> int:
               for r in range(n)]
     del x
 
-    plan = ar.Plan(n, count, dtype, proto=args.proto, nchannels=args.nchannels, chunk_bytes=args.chunk_bytes,
-                   nwaves=args.nwaves, fifo_depth=args.fifo_depth, placement=args.placement)
-    info = plan.info
-    proto = info["proto_name"]
     stream = torch.cuda.current_stream()
     L = ar.lib()
     import ctypes
 
     ptrs = ar._ptr_array(ts)
-    ctx = ar.ar_tune_ctx(ar.AR_COLL_ALLREDUCE, s_bytes, n, ar.DTYPES[dtype], info["nchannels"], 0)
-    tout = ar.ar_tune_out()
     sptr = stream.cuda_stream
 
-    def step():
-        L.ar_tune(ctypes.byref(ctx), ctypes.byref(tout))
-        rc = L.ar_run(plan.handle, ptrs, sptr)
-        if rc != ar.AR_OK:
-            raise ar.ARError(rc, "ar_run")
+    def measure(plan):
+        """ms per step over `steps` timed steps (HIP events on the launch stream)."""
+        info = plan.info
+        ctx = ar.ar_tune_ctx(ar.AR_COLL_ALLREDUCE, s_bytes, n, ar.DTYPES[dtype], max(info["nchannels"], 1), 0)
+        tout = ar.ar_tune_out()
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    if plan.status() != ar.AR_OK:
-        raise RuntimeError("warm-up runs timed out")
+        def step():
+            L.ar_tune(ctypes.byref(ctx), ctypes.byref(tout))
+            rc = L.ar_run(plan.handle, ptrs, sptr)
+            if rc != ar.AR_OK:
+                raise ar.ARError(rc, "ar_run")
 
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    # One untimed step keeps the GPU busy while the start event is enqueued,
-    # so the events bracket exactly the K timed kernels and no launch gap.
-    step()
-    e0.record(stream)
-    for _ in range(args.steps):
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        if plan.status() != ar.AR_OK:
+            raise RuntimeError("warm-up runs timed out")
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter()
+        # One untimed step keeps the GPU busy while the start event is enqueued,
+        # so the events bracket exactly the K timed kernels and no launch gap.
         step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    t_wall = (time.perf_counter() - t_wall) / (args.steps + 1)
-    ms = e0.elapsed_time(e1) / args.steps
-    if plan.status() != ar.AR_OK:
-        raise RuntimeError("timed runs timed out")
+        e0.record(stream)
+        for _ in range(args.steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t_wall = (time.perf_counter() - t_wall) / (args.steps + 1)
+        if plan.status() != ar.AR_OK:
+            raise RuntimeError("timed runs timed out")
+        return e0.elapsed_time(e1) / args.steps, t_wall * 1e3
+
+    def roofline_of(info, ms):
+        t = ms / 1e3
+        algo = info["algo_name"]
+        kernel = f"ring_{info['proto_name']}" if algo == "ring" else "direct"
+        b_comp = ar.compulsory_bytes(s_bytes, n)
+        b_alg = ar.ring_bytes(s_bytes, n, dtype, info["proto_name"]) if algo == "ring" else b_comp
+        achieved = b_alg / t / 1e9
+        traffic = read_traffic(wl.name, kernel)
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": round(traffic["bytes"]) if traffic else None,
+                "kernel": (f"ring_kernel<{info['proto_name']}, {dtype}>" if algo == "ring"
+                           else f"direct_kernel<{dtype}>"),
+                "algorithmic_bytes_per_launch": b_alg,
+                "achieved_compulsory": round(b_comp / t / 1e9, 1),
+                "frac_compulsory": round(b_comp / t / 1e9 / HBM_PEAK_GBS, 4)}
+        if traffic:
+            roof["traffic_source"] = traffic["file"]
+        return roof
+
+    plan = ar.Plan(n, count, dtype, proto=args.proto, nchannels=args.nchannels, chunk_bytes=args.chunk_bytes,
+                   nwaves=args.nwaves, fifo_depth=args.fifo_depth, placement=args.placement, algo=args.algo)
+    info = plan.info
+    ms, wall_ms = measure(plan)
+    plan.destroy()
 
     if args.calibrate_copy:
         nb = args.calibrate_copy << 20
@@ -185,22 +216,21 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         cp.destroy()
 
+    other = None
+    if args.algo == "ring" and args.compare_direct:
+        dplan = ar.Plan(n, count, dtype, algo="direct")
+        dms, _ = measure(dplan)
+        dinfo = dplan.info
+        dplan.destroy()
+        other = {"algo": "direct", "value": round(ar.bus_bandwidth(s_bytes, dms / 1e3, n), 2), "unit": "GB/s",
+                 "ms_per_step": round(dms, 4), "parts": dinfo["nchannels"], "nwaves": dinfo["nwaves"],
+                 "roofline": roofline_of(dinfo, dms),
+                 "note": "two-shot direct algorithm on the same input: same result bits, compulsory bytes only"}
+
     t = ms / 1e3
     busbw = ar.bus_bandwidth(s_bytes, t, n)
     algbw = ar.alg_bandwidth(s_bytes, t)
-    b_ring = ar.ring_bytes(s_bytes, n, dtype, proto)
-    b_comp = ar.compulsory_bytes(s_bytes, n)
-    achieved = b_ring / t / 1e9
-    traffic = read_traffic(wl.name, proto)
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": round(traffic["bytes"]) if traffic else None,
-                "kernel": f"ring_kernel<{proto}, {dtype}>",
-                "algorithmic_bytes_per_launch": b_ring,
-                "achieved_compulsory": round(b_comp / t / 1e9, 1),
-                "frac_compulsory": round(b_comp / t / 1e9 / HBM_PEAK_GBS, 4)}
-    if traffic:
-        roofline["traffic_source"] = traffic["file"]
+    roofline = roofline_of(info, ms)
 
     cpu = None
     if args.cpu_seconds > 0:
@@ -220,16 +250,18 @@ def main(argv=None) -> int:
         "dtype": dtype,
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.note}", "nranks": n, "bytes_per_rank": s_bytes,
-                   "proto": proto, "nchannels": info["nchannels"], "chunk_bytes": info["chunk_elems"] * (4 if dtype == "f32" else 2),
+                   "algo": info["algo_name"], "proto": info["proto_name"], "nchannels": info["nchannels"],
+                   "chunk_bytes": info["chunk_elems"] * (4 if dtype == "f32" else 2),
                    "nwaves": info["nwaves"], "fifo_depth": info["fifo_depth"], "placement": info["placement"],
                    "parallelism": "simulated ring, 1 GPU"},
         "algbw_gbs": round(algbw, 2),
-        "wall_ms_per_step": round(t_wall * 1e3, 4),
+        "wall_ms_per_step": round(wall_ms, 4),
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if other:
+        line["direct"] = other
     print(json.dumps(line))
-    plan.destroy()
     return 0
 
 

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define AR_VERSION 1
+#define AR_VERSION 2
 #define AR_MAX_RANKS 16
 #define AR_MAX_CHANNELS 256
 #define AR_MAX_WAVES 16
@@ -55,6 +55,22 @@ enum { AR_FLOAT32 = 0, AR_BFLOAT16 = 1 };
  *   LL128  128-byte lines: 120 bytes of data + 8-byte flag.
  *   Simple bulk chunks behind separate ready (tail) / free (head) counters. */
 enum { AR_PROTO_AUTO = -1, AR_PROTO_LL = 0, AR_PROTO_LL128 = 1, AR_PROTO_SIMPLE = 2 };
+
+/* Algorithms (paper section 2: the tuner chooses the algorithm, e.g. ring
+ * or tree, besides protocol and channels).
+ *   AR_ALGO_AUTO    no preference: a requested protocol implies the ring,
+ *                   otherwise the tuner decides (no opinion = ring)
+ *   AR_ALGO_RING    reduce-scatter + all-gather around the ring, through
+ *                   FIFOs, under a protocol and channel count
+ *   AR_ALGO_DIRECT  two-shot direct reduce: for each segment, one group of
+ *                   workgroups reads that segment of every rank buffer
+ *                   directly, sums it in the same chain order as the ring
+ *                   (x_s + x_{s+1} + ... + x_{s+N-1}) and writes the result
+ *                   to every rank; identical bits, only 2 N S bytes moved,
+ *                   no flags.  Protocols do not apply; nchannels is the
+ *                   number of workgroups per segment (0 = sized to the
+ *                   message). */
+enum { AR_ALGO_AUTO = 0, AR_ALGO_RING = 1, AR_ALGO_DIRECT = 2 };
 
 /* Collective type seen by the tuner (only AllReduce is implemented). */
 enum { AR_COLL_ALLREDUCE = 0 };
@@ -110,6 +126,7 @@ typedef struct ar_plan_desc {
     uint64_t comm_id;      /* communicator key passed to the tuner and used
                               by the profiler hook (0 if unused) */
     uint32_t flags;        /* AR_PLAN_* */
+    int algo;              /* AR_ALGO_* */
 } ar_plan_desc;
 
 /* Plan flags.
@@ -136,6 +153,7 @@ typedef struct ar_plan_info {
     size_t flag_bytes;     /* head/tail counters and control words */
     uint64_t msgs_per_run; /* messages per connection per run: nchunks*(2N-2) */
     uint64_t wire_bytes_per_run; /* FIFO payload+flag bytes written per run (all connections) */
+    int algo;              /* AR_ALGO_RING or AR_ALGO_DIRECT */
 } ar_plan_info;
 
 /* ---- plans -------------------------------------------------------------- */
@@ -219,6 +237,12 @@ typedef struct ar_tune_out {
     int nchannels;         /* 0 = no opinion */
     size_t chunk_bytes;    /* 0 = protocol default */
     int nwaves;            /* 0 = protocol default */
+    int algo;              /* AR_ALGO_*; AUTO = no opinion (ring).  proto,
+                              nchannels, chunk_bytes and nwaves describe the
+                              ring choice, used whenever the ring runs. */
+    int direct_parts;      /* direct algorithm: workgroups per segment
+                              (0 = sized to the message) */
+    int direct_nwaves;     /* direct algorithm: waves per workgroup (0 = 4) */
 } ar_tune_out;
 
 /* A tuner: fill *out from *ctx; return 0 on success.  A non-zero return, or

@@ -26,6 +26,9 @@ AR_PLACE_RANK_SPREAD, AR_PLACE_CHANNEL_LOCAL = 0, 1
  AR_ERR_TIMEOUT, AR_ERR_STATE) = range(8)
 AR_DEBUG_SKIP_POST, AR_DEBUG_JITTER = 1, 2
 AR_PLAN_PROFILE = 1
+AR_ALGO_AUTO, AR_ALGO_RING, AR_ALGO_DIRECT = 0, 1, 2
+ALGOS = {"auto": AR_ALGO_AUTO, "ring": AR_ALGO_RING, "direct": AR_ALGO_DIRECT}
+ALGO_NAMES = {v: k for k, v in ALGOS.items()}
 AR_MAX_RANKS, AR_MAX_CHANNELS, AR_MAX_WAVES = 16, 256, 16
 
 PROTOS = {"ll": AR_PROTO_LL, "ll128": AR_PROTO_LL128, "simple": AR_PROTO_SIMPLE, "auto": AR_PROTO_AUTO}
@@ -40,7 +43,8 @@ class ar_plan_desc(ctypes.Structure):
                 ("proto", ctypes.c_int), ("nchannels", ctypes.c_int), ("chunk_bytes", ctypes.c_size_t),
                 ("fifo_depth", ctypes.c_int), ("nwaves", ctypes.c_int), ("placement", ctypes.c_int),
                 ("timeout_us", ctypes.c_uint32), ("debug_flags", ctypes.c_uint32),
-                ("max_channels", ctypes.c_int), ("comm_id", ctypes.c_uint64), ("flags", ctypes.c_uint32)]
+                ("max_channels", ctypes.c_int), ("comm_id", ctypes.c_uint64), ("flags", ctypes.c_uint32),
+                ("algo", ctypes.c_int)]
 
 
 class ar_plan_info(ctypes.Structure):
@@ -50,11 +54,12 @@ class ar_plan_info(ctypes.Structure):
                 ("count", ctypes.c_size_t), ("seg_elems", ctypes.c_size_t), ("chan_elems", ctypes.c_size_t),
                 ("chunk_elems", ctypes.c_size_t), ("wave_elems", ctypes.c_size_t), ("nchunks", ctypes.c_size_t),
                 ("slot_bytes", ctypes.c_size_t), ("fifo_bytes", ctypes.c_size_t), ("flag_bytes", ctypes.c_size_t),
-                ("msgs_per_run", ctypes.c_uint64), ("wire_bytes_per_run", ctypes.c_uint64)]
+                ("msgs_per_run", ctypes.c_uint64), ("wire_bytes_per_run", ctypes.c_uint64), ("algo", ctypes.c_int)]
 
     def as_dict(self) -> dict:
         d = {name: getattr(self, name) for name, _ in self._fields_}
         d["proto_name"] = PROTO_NAMES.get(d["proto"], str(d["proto"]))
+        d["algo_name"] = ALGO_NAMES.get(d["algo"], str(d["algo"]))
         d["dtype_name"] = DTYPE_NAMES.get(d["dtype"], str(d["dtype"]))
         return d
 
@@ -66,7 +71,8 @@ class ar_tune_ctx(ctypes.Structure):
 
 class ar_tune_out(ctypes.Structure):
     _fields_ = [("proto", ctypes.c_int), ("nchannels", ctypes.c_int), ("chunk_bytes", ctypes.c_size_t),
-                ("nwaves", ctypes.c_int)]
+                ("nwaves", ctypes.c_int), ("algo", ctypes.c_int), ("direct_parts", ctypes.c_int),
+                ("direct_nwaves", ctypes.c_int)]
 
 
 class ar_latency_state(ctypes.Structure):
@@ -163,7 +169,8 @@ def _check(rc: int, what: str):
 
 def make_desc(nranks: int, count: int, dtype="f32", proto="auto", nchannels: int = 0, chunk_bytes: int = 0,
               fifo_depth: int = 0, nwaves: int = 0, placement: int = 0, timeout_us: int = 0,
-              debug_flags: int = 0, max_channels: int = 0, comm_id: int = 0, flags: int = 0) -> ar_plan_desc:
+              debug_flags: int = 0, max_channels: int = 0, comm_id: int = 0, flags: int = 0,
+              algo="auto") -> ar_plan_desc:
     d = ar_plan_desc()
     d.nranks = nranks
     d.dtype = DTYPES[dtype] if isinstance(dtype, str) else dtype
@@ -179,6 +186,7 @@ def make_desc(nranks: int, count: int, dtype="f32", proto="auto", nchannels: int
     d.max_channels = max_channels
     d.comm_id = comm_id
     d.flags = flags
+    d.algo = ALGOS[algo] if isinstance(algo, str) else algo
     return d
 
 
@@ -196,7 +204,9 @@ def ar_tune(msg_bytes: int, nranks: int = 8, dtype="f32", max_channels: int = AR
     out = ar_tune_out()
     _check(lib().ar_tune(ctypes.byref(ctx), ctypes.byref(out)), "ar_tune")
     return {"proto": out.proto, "proto_name": PROTO_NAMES[out.proto], "nchannels": out.nchannels,
-            "chunk_bytes": out.chunk_bytes, "nwaves": out.nwaves}
+            "chunk_bytes": out.chunk_bytes, "nwaves": out.nwaves, "algo": out.algo,
+            "algo_name": ALGO_NAMES[out.algo], "direct_parts": out.direct_parts,
+            "direct_nwaves": out.direct_nwaves}
 
 
 _tuner_refs = []  # keep ctypes callbacks alive while installed
@@ -226,6 +236,9 @@ def _tuner_callback(fn):
             o.nchannels = int(res.get("nchannels", 0))
             o.chunk_bytes = int(res.get("chunk_bytes", 0))
             o.nwaves = int(res.get("nwaves", 0))
+            o.algo = int(res.get("algo", AR_ALGO_AUTO))
+            o.direct_parts = int(res.get("direct_parts", 0))
+            o.direct_nwaves = int(res.get("direct_nwaves", 0))
             return int(res.get("rc", 0))
 
         cb = ar_tuner_fn(_trampoline)
@@ -308,9 +321,9 @@ class Plan:
 
     def __init__(self, nranks: int, count: int, dtype="f32", proto="auto", nchannels: int = 0,
                  chunk_bytes: int = 0, fifo_depth: int = 0, nwaves: int = 0, placement: int = 0,
-                 timeout_us: int = 0, debug_flags: int = 0, comm_id: int = 0, flags: int = 0):
+                 timeout_us: int = 0, debug_flags: int = 0, comm_id: int = 0, flags: int = 0, algo="auto"):
         self.desc = make_desc(nranks, count, dtype, proto, nchannels, chunk_bytes, fifo_depth, nwaves,
-                              placement, timeout_us, debug_flags, 0, comm_id, flags)
+                              placement, timeout_us, debug_flags, 0, comm_id, flags, algo)
         L = lib()
         h = L.ar_plan_ex(ctypes.byref(self.desc))
         if not h:

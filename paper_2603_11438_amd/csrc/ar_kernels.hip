@@ -959,6 +959,143 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
     }
 }
 
+// ===================================================================== direct
+//
+// Two-shot direct AllReduce: workgroup b works on segment s = b mod N (part
+// b / N of its parts); a thread loads one 16-byte unit of segment s from
+// every rank (ranks s, s+1, ..., s+N-1 in that order), sums them in that
+// chain order -- the same additions, in the same order, as the ring's
+// reduce-scatter -- and stores the result to every rank.  Every element is
+// read once per rank and written once per rank: the compulsory 2 N S bytes,
+// no FIFOs, no flags, no waits.  In place is safe: each element is read and
+// then written by the same thread.
+
+template <int DT, int NMAX, int U>
+__global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
+{
+    constexpr uint32_t E = Elem<DT>::E;
+    constexpr uint32_t A = Elem<DT>::A;
+    const uint32_t N = a.nranks;
+    const uint32_t parts = a.nchannels;
+    const uint32_t s = blockIdx.x % N;
+    const uint32_t part = blockIdx.x / N;
+    const uint64_t seg_lo = (uint64_t)s * a.seg;
+    if (seg_lo >= a.count) return;
+    const uint64_t seg_hi = seg_lo + a.seg < a.count ? seg_lo + a.seg : a.count;
+    const uint64_t len = seg_hi - seg_lo;
+    const uint32_t nfull = (uint32_t)(len / A), rem = (uint32_t)(len % A);
+    const uint32_t tid = threadIdx.x, nth = blockDim.x;
+
+    // Rank j of the chain is rank (s + j) mod N.
+    auto in_rsrc = [&](uint32_t j) {
+        const uint32_t r = (s + j) % N;
+        return make_rsrc(a.src[r] + seg_lo * E, len * E);
+    };
+    auto out_rsrc = [&](uint32_t r) { return make_rsrc(a.dst[r] + seg_lo * E, len * E); };
+
+    auto chain = [&](const u32x4 *v, float *acc) {
+        if (E == 4) {
+            for (int i = 0; i < 4; ++i) acc[i] = as_f32(v[0][i]);
+        } else {
+            for (int i = 0; i < 4; ++i) {
+                acc[2 * i] = bf16_lo(v[0][i]);
+                acc[2 * i + 1] = bf16_hi(v[0][i]);
+            }
+        }
+#pragma unroll
+        for (int j = 1; j < NMAX; ++j) {
+            if ((uint32_t)j < N) {
+                if (E == 4) {
+                    for (int i = 0; i < 4; ++i) acc[i] = acc[i] + as_f32(v[j][i]);
+                } else {
+                    for (int i = 0; i < 4; ++i) {
+                        acc[2 * i] = acc[2 * i] + bf16_lo(v[j][i]);
+                        acc[2 * i + 1] = acc[2 * i + 1] + bf16_hi(v[j][i]);
+                    }
+                }
+            }
+        }
+    };
+    auto narrow = [&](const float *acc) {
+        u32x4 y;
+        if (E == 4) {
+            for (int i = 0; i < 4; ++i) y[i] = as_u32(acc[i]);
+        } else {
+            for (int i = 0; i < 4; ++i) y[i] = pack_bf16(acc[2 * i], acc[2 * i + 1]);
+        }
+        return y;
+    };
+
+    for (uint32_t base = part * nth * U; base < nfull; base += parts * nth * U) {
+        u32x4 v[U][NMAX];
+#pragma unroll
+        for (int j = 0; j < NMAX; ++j) {
+            if ((uint32_t)j < N) {
+                const Rsrc rin = in_rsrc(j);
+#pragma unroll
+                for (int t = 0; t < U; ++t) {
+                    const uint32_t u = base + t * nth + tid;
+                    if (u < nfull) v[t][j] = ld128<kInPol>(rin, u * 16);
+                }
+            }
+        }
+        u32x4 y[U];
+#pragma unroll
+        for (int t = 0; t < U; ++t) {
+            float acc[A];
+            chain(v[t], acc);
+            y[t] = narrow(acc);
+        }
+#pragma unroll
+        for (int r = 0; r < NMAX; ++r) {
+            if ((uint32_t)r < N) {
+                const Rsrc rout = out_rsrc(r);
+#pragma unroll
+                for (int t = 0; t < U; ++t) {
+                    const uint32_t u = base + t * nth + tid;
+                    if (u < nfull) st128<kOutPol>(rout, u * 16, y[t]);
+                }
+            }
+        }
+    }
+    if (rem && part == 0 && tid == 0) {
+        // Partial last unit of the buffer: element-wise loads and stores
+        // (every index below is a compile-time constant after unrolling).
+        u32x4 v[NMAX];
+#pragma unroll
+        for (int j = 0; j < NMAX; ++j) {
+            u32x4 x = {0, 0, 0, 0};
+            if ((uint32_t)j < N) {
+                const Rsrc rin = in_rsrc(j);
+#pragma unroll
+                for (int i = 0; i < (int)A; ++i) {
+                    if ((uint32_t)i < rem) {
+                        if (E == 4) x[i] = ld32<kInPol>(rin, nfull * 16 + 4 * i);
+                        else x[i >> 1] |= ld16<kInPol>(rin, nfull * 16 + 2 * i) << ((i & 1) * 16);
+                    }
+                }
+            }
+            v[j] = x;
+        }
+        float acc[A];
+        chain(v, acc);
+        const u32x4 y = narrow(acc);
+#pragma unroll
+        for (int r = 0; r < NMAX; ++r) {
+            if ((uint32_t)r < N) {
+                const Rsrc rout = out_rsrc(r);
+#pragma unroll
+                for (int i = 0; i < (int)A; ++i) {
+                    if ((uint32_t)i < rem) {
+                        if (E == 4) st32<kOutPol>(rout, nfull * 16 + 4 * i, y[i]);
+                        else st16<kOutPol>(rout, nfull * 16 + 2 * i, (y[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu);
+                    }
+                }
+            }
+        }
+    }
+}
+
 // ------------------------------------------------------------------ helpers
 
 __global__ void fill_u32_kernel(uint32_t *p, size_t n, uint32_t v)
@@ -996,11 +1133,22 @@ __host__ RingFn ring_fn(int proto, int dtype)
     return ring_kernel<AR_PROTO_SIMPLE, AR_BFLOAT16>;
 }
 
+__host__ RingFn direct_fn(int dtype, int nranks)
+{
+    if (dtype == AR_FLOAT32) {
+        if (nranks <= 8) return direct_kernel<AR_FLOAT32, 8, 2>;
+        return direct_kernel<AR_FLOAT32, 16, 1>;
+    }
+    if (nranks <= 8) return direct_kernel<AR_BFLOAT16, 8, 2>;
+    return direct_kernel<AR_BFLOAT16, 16, 1>;
+}
+
 }  // namespace dev
 
 int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
 {
-    dev::RingFn fn = dev::ring_fn(info.proto, info.dtype);
+    dev::RingFn fn = info.algo == AR_ALGO_DIRECT ? dev::direct_fn(info.dtype, info.nranks)
+                                                 : dev::ring_fn(info.proto, info.dtype);
     RingArgs a = args;
     void *kargs[] = {&a};
     hipError_t e = hipLaunchKernel((const void *)fn, dim3((unsigned)info.grid), dim3((unsigned)info.block), kargs,

@@ -131,6 +131,9 @@ int ar_tuner_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->proto = cfg.proto;
     out->chunk_bytes = 0;
     out->nwaves = 0;
+    out->algo = AR_ALGO_RING;
+    out->direct_parts = 0;
+    out->direct_nwaves = 0;
     Entry *e = find(ctx->comm_id, false);
     if (!e || e->samples.load(std::memory_order_acquire) == 0) {
         out->nchannels = cfg.min_channels;

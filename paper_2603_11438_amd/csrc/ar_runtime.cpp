@@ -126,7 +126,7 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
         rc = launch_copy(send[0], recv[0], bytes, stream);
         return ret(rc);
     }
-    if (g.proto == AR_PROTO_LL && p->epoch + g.msgs_per_run + 2 >= kLLTagLimit) {
+    if (g.algo == AR_ALGO_RING && g.proto == AR_PROTO_LL && p->epoch + g.msgs_per_run + 2 >= kLLTagLimit) {
         // 32-bit LL flags are about to wrap: start again from zeroed memory.
         rc = zero_workspace(p, stream);
         if (rc != AR_OK) return ret(rc);
@@ -195,7 +195,7 @@ ar_plan_t *ar_plan_ex(const ar_plan_desc *desc)
     ar_plan_info info;
     int rc = resolve_geometry(&d, cap, &info);
     if (rc != AR_OK) return fail<ar_plan_t>(rc);
-    if (info.grid > 0) {
+    if (info.grid > 0 && info.algo == AR_ALGO_RING) {
         // Re-check co-residency for the resolved protocol and wave count.
         int cap2 = 0;
         rc = device_channel_capacity(info.proto, info.dtype, info.nranks, info.nwaves, &cap2);
@@ -225,7 +225,7 @@ ar_plan_t *ar_plan_ex(const ar_plan_desc *desc)
             return fail<ar_plan_t>(AR_ERR_HIP);
         }
     }
-    if (info.grid > 0) {
+    if (info.grid > 0 && info.algo == AR_ALGO_RING) {
         const size_t ctl_bytes = 256;
         const size_t flag_bytes = round_up(info.flag_bytes - kCtlU32 * 4, 256);
         p->ws_bytes = ctl_bytes + flag_bytes + info.fifo_bytes;

@@ -26,10 +26,13 @@ thread_local int g_last_error = AR_OK;
 
 struct TableRow {
     int log2_bytes;
-    int proto;
+    int proto;         // ring choice for this size ...
     int nchannels;
     size_t chunk_bytes;
     int nwaves;
+    int algo;          // ... and the algorithm to run (AUTO = the ring)
+    int direct_parts;  // direct algorithm's workgroups per segment (0 = auto)
+    int direct_nwaves; // direct algorithm's waves per workgroup (0 = default)
 };
 
 #include "tuner_table.inc"
@@ -42,6 +45,7 @@ constexpr size_t kMaxChunkBytes = 64u << 20;
 constexpr size_t kMinChunkBytes = 16;
 
 bool valid_proto(int p) { return p == AR_PROTO_LL || p == AR_PROTO_LL128 || p == AR_PROTO_SIMPLE; }
+bool valid_algo(int a) { return a == AR_ALGO_AUTO || a == AR_ALGO_RING || a == AR_ALGO_DIRECT; }
 
 // The active tuner is one atomic pointer to an immutable slot (paper section
 // 4, hot reload: an atomic function-pointer swap; a call already in progress
@@ -85,8 +89,10 @@ void unpin(TunerSlot *s) { s->inflight.fetch_sub(1, std::memory_order_seq_cst); 
 bool out_valid(int rc, const ar_tune_out &o)
 {
     if (rc != 0) return false;
+    if (!valid_algo(o.algo)) return false;
     if (o.proto != AR_PROTO_AUTO && !valid_proto(o.proto)) return false;
     if (o.nchannels < 0 || o.nwaves < 0 || o.nwaves > AR_MAX_WAVES) return false;
+    if (o.direct_parts < 0 || o.direct_nwaves < 0 || o.direct_nwaves > AR_MAX_WAVES) return false;
     return o.chunk_bytes <= kMaxChunkBytes;
 }
 
@@ -105,7 +111,7 @@ int probe_tuner(ar_tuner_fn fn, void *user, uint64_t *probes)
             for (int dt = 0; dt < 2; ++dt)
                 for (int mc : maxch) {
                     ar_tune_ctx c = {AR_COLL_ALLREDUCE, sz, nr, dt, mc, 0};
-                    ar_tune_out o = {AR_PROTO_AUTO, 0, 0, 0};
+                    ar_tune_out o = {AR_PROTO_AUTO, 0, 0, 0, AR_ALGO_AUTO, 0, 0};
                     int rc = fn(&c, &o, user);
                     ++n;
                     if (!out_valid(rc, o)) {
@@ -172,6 +178,11 @@ int default_nwaves(int proto)
 
 int default_depth(int proto) { return proto == AR_PROTO_SIMPLE ? 2 : 4; }
 
+// Direct algorithm: units (16 bytes of data) per thread per iteration, and
+// the largest grid it is sized to (8 workgroups per CU on 256 CUs).
+constexpr uint64_t kDirectUnroll = 2;
+constexpr uint64_t kDirectMaxGrid = 2048;
+
 size_t default_chunk_bytes(int proto)
 {
     switch (proto) {
@@ -179,6 +190,45 @@ size_t default_chunk_bytes(int proto)
     case AR_PROTO_LL128: return 60u << 10;
     default: return 256u << 10;
     }
+}
+
+// Geometry of the direct algorithm: a group of `parts` workgroups per
+// segment, each striding over the segment's 16-byte units.
+int resolve_direct(const ar_plan_desc *d, const ar_tune_out *t, ar_plan_info *out)
+{
+    const uint64_t e = d->dtype == AR_FLOAT32 ? 4 : 2;
+    const uint64_t A = 16 / e;
+    const uint64_t N = (uint64_t)d->nranks;
+    int nw = d->nwaves ? d->nwaves : (t && t->direct_nwaves ? t->direct_nwaves : 4);
+    ar_plan_info g = {};
+    g.algo = AR_ALGO_DIRECT;
+    g.proto = AR_PROTO_AUTO;
+    g.nranks = d->nranks;
+    g.dtype = d->dtype;
+    g.nwaves = nw;
+    g.placement = d->placement;
+    g.count = d->count;
+    g.block = 64 * nw;
+    g.seg_elems = round_up(ceil_div(d->count, N), A);
+    if (N == 1 || d->count == 0) {
+        g.grid = 0;
+        *out = g;
+        return AR_OK;
+    }
+    const uint64_t seg_units = ceil_div(g.seg_elems, A);
+    uint64_t parts = (uint64_t)(d->nchannels ? d->nchannels : (t ? t->direct_parts : 0));
+    if (parts == 0) {
+        parts = ceil_div(seg_units, 64 * (uint64_t)nw * kDirectUnroll);
+        uint64_t cap = kDirectMaxGrid / N;
+        if (cap < 1) cap = 1;
+        if (parts > cap) parts = cap;
+        if (parts < 1) parts = 1;
+    }
+    g.nchannels = (int)parts;
+    g.grid = (int)(parts * N);
+    g.chan_elems = round_up(ceil_div(g.seg_elems, parts), A);
+    *out = g;
+    return AR_OK;
 }
 
 int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
@@ -193,39 +243,56 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     if (d->placement != AR_PLACE_RANK_SPREAD && d->placement != AR_PLACE_CHANNEL_LOCAL) return AR_ERR_ARG;
     if (d->chunk_bytes > kMaxChunkBytes) return AR_ERR_ARG;
     if (d->flags & ~(uint32_t)AR_PLAN_PROFILE) return AR_ERR_ARG;
+    if (!valid_algo(d->algo)) return AR_ERR_ARG;
     if (max_channels < 1) max_channels = 1;
     if (max_channels > AR_MAX_CHANNELS) max_channels = AR_MAX_CHANNELS;
-    if (d->nchannels > max_channels) return AR_ERR_OCCUPANCY;
 
     const uint64_t e = d->dtype == AR_FLOAT32 ? 4 : 2;
     const uint64_t A = 16 / e;
     // Per-rank byte counts stay below 2^46 so every byte offset fits easily.
     if (d->count > (1ull << 44)) return AR_ERR_ARG;
 
+    // A requested protocol implies the ring.
+    int algo = d->algo;
+    if (algo == AR_ALGO_AUTO && d->proto != AR_PROTO_AUTO) algo = AR_ALGO_RING;
+    if (algo == AR_ALGO_DIRECT && d->proto != AR_PROTO_AUTO) return AR_ERR_ARG;
     int proto = d->proto, nch = d->nchannels, nw = d->nwaves;
     size_t chunk = d->chunk_bytes;
-    if (proto == AR_PROTO_AUTO || nch == 0 || chunk == 0 || nw == 0) {
+    // One decision per plan: the tuner is asked at most once.
+    const bool ring_needs_tuner = proto == AR_PROTO_AUTO || nch == 0 || chunk == 0 || nw == 0;
+    const bool direct_needs_tuner = nch == 0 || nw == 0;
+    ar_tune_out t;
+    bool have_t = false;
+    if (algo == AR_ALGO_AUTO || (algo == AR_ALGO_RING && ring_needs_tuner) ||
+        (algo == AR_ALGO_DIRECT && direct_needs_tuner)) {
         ar_tune_ctx ctx = {AR_COLL_ALLREDUCE, (size_t)(d->count * e), d->nranks, d->dtype,
                            max_channels, d->comm_id};
-        ar_tune_out t;
         int rc = ar_tune(&ctx, &t);
         if (rc != AR_OK) return rc;
-        if (proto == AR_PROTO_AUTO) {
-            proto = t.proto;
-            // Channels, chunk and waves from the tuner belong to its protocol.
-            if (nch == 0) nch = t.nchannels;
-            if (chunk == 0) chunk = t.chunk_bytes;
-            if (nw == 0) nw = t.nwaves;
-        } else {
-            if (nch == 0) nch = t.proto == proto ? t.nchannels : clamp_int(kDefaultChannels, 1, max_channels);
-            if (chunk == 0) chunk = t.proto == proto ? t.chunk_bytes : default_chunk_bytes(proto);
-            if (nw == 0) nw = t.proto == proto ? t.nwaves : default_nwaves(proto);
+        have_t = true;
+        if (algo == AR_ALGO_AUTO) algo = t.algo;
+        if (algo == AR_ALGO_RING) {
+            if (proto == AR_PROTO_AUTO) {
+                proto = t.proto;
+                // Channels, chunk and waves from the tuner belong to its protocol.
+                if (nch == 0) nch = t.nchannels;
+                if (chunk == 0) chunk = t.chunk_bytes;
+                if (nw == 0) nw = t.nwaves;
+            } else {
+                if (nch == 0) nch = t.proto == proto ? t.nchannels : clamp_int(kDefaultChannels, 1, max_channels);
+                if (chunk == 0) chunk = t.proto == proto ? t.chunk_bytes : default_chunk_bytes(proto);
+                if (nw == 0) nw = t.proto == proto ? t.nwaves : default_nwaves(proto);
+            }
         }
     }
+    if (algo == AR_ALGO_DIRECT) return resolve_direct(d, have_t ? &t : nullptr, out);
+    // Ring workgroups wait on each other, so they must all be resident.
+    if (d->nchannels > max_channels) return AR_ERR_OCCUPANCY;
     chunk = clamp_chunk(chunk);
     const int depth = d->fifo_depth ? d->fifo_depth : default_depth(proto);
 
     ar_plan_info g = {};
+    g.algo = AR_ALGO_RING;
     g.nranks = d->nranks;
     g.dtype = d->dtype;
     g.proto = proto;
@@ -297,6 +364,9 @@ int ar_tuner_fixed_default(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->nchannels = kDefaultChannels;
     out->chunk_bytes = 0;
     out->nwaves = 0;
+    out->algo = AR_ALGO_RING;
+    out->direct_parts = 0;
+    out->direct_nwaves = 0;
     return 0;
 }
 
@@ -309,6 +379,9 @@ int ar_tuner_noop(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->nchannels = 0;
     out->chunk_bytes = 0;
     out->nwaves = 0;
+    out->algo = AR_ALGO_AUTO;
+    out->direct_parts = 0;
+    out->direct_nwaves = 0;
     return 0;
 }
 
@@ -331,6 +404,9 @@ int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->nchannels = row->nchannels;
     out->chunk_bytes = row->chunk_bytes;
     out->nwaves = row->nwaves;
+    out->algo = row->algo;
+    out->direct_parts = row->direct_parts;
+    out->direct_nwaves = row->direct_nwaves;
     return 0;
 }
 
@@ -349,17 +425,28 @@ int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out)
     const int max_ch = clamp_int(ctx->max_channels > 0 ? ctx->max_channels : AR_MAX_CHANNELS, 1,
                                  AR_MAX_CHANNELS);
     TunerSlot *slot = pin_active();
-    ar_tune_out t = {AR_PROTO_AUTO, 0, 0, 0};
+    ar_tune_out t = {AR_PROTO_AUTO, 0, 0, 0, AR_ALGO_AUTO, 0, 0};
     int rc = slot->fn(ctx, &t, slot->user);
     unpin(slot);
 
-    bool fallback = rc != 0 || !valid_proto(t.proto) || t.nchannels < 0 || t.nwaves < 0;
+    // No opinion on the protocol means the fixed default's ring choice.
+    if (rc == 0 && t.proto == AR_PROTO_AUTO && valid_algo(t.algo)) {
+        t.proto = kDefaultProto;
+        t.nchannels = t.nchannels > 0 ? t.nchannels : kDefaultChannels;
+    }
+    bool fallback = rc != 0 || !valid_proto(t.proto) || !valid_algo(t.algo) || t.nchannels < 0 || t.nwaves < 0 ||
+                    t.direct_parts < 0 || t.direct_nwaves < 0;
     if (fallback) {
         t.proto = kDefaultProto;
         t.nchannels = kDefaultChannels;
         t.chunk_bytes = 0;
         t.nwaves = 0;
+        t.algo = AR_ALGO_RING;
+        t.direct_parts = 0;
+        t.direct_nwaves = 0;
     }
+    if (t.direct_nwaves > AR_MAX_WAVES) t.direct_nwaves = AR_MAX_WAVES;
+    if (t.algo == AR_ALGO_AUTO) t.algo = AR_ALGO_RING;
     if (t.nchannels == 0) t.nchannels = kDefaultChannels;
     t.nchannels = clamp_int(t.nchannels, 1, max_ch);
     t.chunk_bytes = t.chunk_bytes ? clamp_chunk(t.chunk_bytes) : default_chunk_bytes(t.proto);

@@ -9,9 +9,13 @@ on MI355X for the simulated ring.
     python -m paper_2603_11438_amd.sweep table sweep.jsonl --emit csrc/tuner_table.inc
     python -m paper_2603_11438_amd.sweep validate --out validate.jsonl
 
-Selection rule per size: the highest median bus bandwidth wins; candidates
-within 2 % of the best count as ties and are broken by fewer channels, then
-fewer wire bytes (Simple < LL128 < LL), then smaller chunk, then fewer waves.
+Selection rule per size, for the ring's columns: the highest median bus
+bandwidth wins; candidates within 2 % of the best count as ties and are
+broken by fewer channels, then fewer wire bytes (Simple < LL128 < LL), then
+smaller chunk, then fewer waves; when the fixed default is within 2 % the
+row defers to it.  The direct algorithm's columns take its fastest
+{workgroups per segment, waves}.  The algorithm column picks the faster of
+the two (the direct algorithm on a tie: it moves fewer bytes).
 """
 from __future__ import annotations
 
@@ -57,7 +61,14 @@ def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3):
     return out
 
 
+DIRECT_PARTS = (0, 16, 64, 256)
+DIRECT_WAVES = (2, 4, 8, 16)
+
+
 def grid(size, protos=("ll", "ll128", "simple"), channels=(1, 2, 4, 8, 16, 32, 64), waves=(2, 4, 8)):
+    for parts in DIRECT_PARTS:
+        for w in DIRECT_WAVES:
+            yield dict(algo="direct", nchannels=parts, nwaves=w)
     for p in protos:
         for c in channels:
             for w in waves:
@@ -81,6 +92,8 @@ def measure(args):
             g = torch.Generator(device="cuda:0").manual_seed(11438)
             ts = [torch.rand(count, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
             for cfg in grid(size):
+                if args.algo and cfg.get("algo", "ring") != args.algo:
+                    continue
                 try:
                     plan = ar.Plan(n, count, "f32", **cfg)
                 except ar.ARError as e:
@@ -88,7 +101,8 @@ def measure(args):
                 times = _timer(plan, ts, stream)
                 info = plan.info
                 med = statistics.median(times)
-                rec = {"size": size, "nranks": n, **cfg, "chunk_eff": info["chunk_elems"] * 4,
+                rec = {"size": size, "nranks": n, "proto": info["proto_name"], "chunk_bytes": 0, **cfg,
+                       "algo": info["algo_name"], "parts_eff": info["nchannels"], "chunk_eff": info["chunk_elems"] * 4,
                        "t_med_us": med * 1e6, "t_min_us": min(times) * 1e6, "t_max_us": max(times) * 1e6,
                        "busbw": ar.bus_bandwidth(size, med, n)}
                 fo.write(json.dumps(rec) + "\n")
@@ -112,6 +126,23 @@ def default_row(size, rs, nranks=8):
 
 
 def select(rows, tie=0.02):
+    """Per size: {"ring": ring choice, "direct": direct choice or None, "algo": "ring" | "direct"}."""
+    ring = select_ring([r for r in rows if r.get("algo", "ring") == "ring"], tie)
+    out = {}
+    for size, rr in ring.items():
+        ds = [r for r in rows if r["size"] == size and r.get("algo") == "direct"]
+        d = None
+        if ds:
+            best = max(r["busbw"] for r in ds)
+            ties = [r for r in ds if r["busbw"] >= (1 - tie) * best]
+            ties.sort(key=lambda r: (r["nchannels"], r["nwaves"]))
+            d = ties[0]
+        algo = "direct" if d is not None and d["busbw"] >= (1 - tie) * rr["busbw"] else "ring"
+        out[size] = {"ring": rr, "direct": d, "algo": algo}
+    return out
+
+
+def select_ring(rows, tie=0.02):
     """Per size: the highest median bus bandwidth; candidates within `tie` of
     the best are ties, broken by fewer channels, fewer wire bytes, smaller
     chunk, fewer waves.  When the fixed default is itself within `tie` of the
@@ -137,7 +168,8 @@ def emit(table, path):
     names = {"ll": "AR_PROTO_LL", "ll128": "AR_PROTO_LL128", "simple": "AR_PROTO_SIMPLE",
              "default": "AR_PROTO_AUTO"}
     lines = [
-        "// MI355X size -> {protocol, channels, chunk, waves} table for 8-rank fp32",
+        "// MI355X size -> {algorithm; ring protocol, channels, chunk, waves; direct",
+        "// workgroups per segment, waves} table for 8-rank fp32",
         "// AllReduce, one row per power-of-two message size (bytes per rank) from",
         "// 4 KiB to 128 MiB.  A message of S bytes uses the row of the smallest size",
         "// >= S (sizes below 4 KiB use the first row, above 128 MiB the last).",
@@ -146,30 +178,39 @@ def emit(table, path):
         "// the middle sizes, another for the large sizes); the values were measured",
         "// on MI355X by paper_2603_11438_amd/sweep.py (highest median bus bandwidth,",
         "// ties within 2% broken by fewer channels, fewer wire bytes, smaller chunk).",
-        "// AR_PROTO_AUTO rows defer to the fixed default (Simple, 16 channels): there",
-        "// the default measured within 2% of the best choice.",
+        "// AR_PROTO_AUTO ring columns defer to the fixed default (Simple, 16 channels):",
+        "// there the default measured within 2% of the best ring choice.  The",
+        "// algorithm column picks the faster of the best ring and the best direct",
+        "// choice (direct on a tie, as it moves fewer bytes).",
         "//",
-        "// columns: log2(size), proto, nchannels, chunk_bytes, nwaves   [busBW GB/s]",
+        "// columns: log2(size), ring proto, nchannels, chunk_bytes, nwaves, algorithm,",
+        "//          direct parts, direct waves   [busBW GB/s: ring / direct]",
         "static const TableRow kTable[] = {",
     ]
-    for size, r in sorted(table.items()):
+    for size, row in sorted(table.items()):
         lg = size.bit_length() - 1
-        if r["proto"] == "default":
-            lines.append(f"    {{{lg}, AR_PROTO_AUTO, 0, 0, 0}},  // {r['busbw']:.1f}")
-        else:
-            lines.append(f"    {{{lg}, {names[r['proto']]}, {r['nchannels']}, {r['chunk_bytes']}, {r['nwaves']}}},"
-                         f"  // {r['busbw']:.1f}")
+        r, d = row["ring"], row["direct"]
+        ring_cols = ("AR_PROTO_AUTO, 0, 0, 0" if r["proto"] == "default" else
+                     f"{names[r['proto']]}, {r['nchannels']}, {r['chunk_bytes']}, {r['nwaves']}")
+        algo = "AR_ALGO_DIRECT" if row["algo"] == "direct" else "AR_ALGO_RING"
+        dcols = f"{d['nchannels']}, {d['nwaves']}" if d else "0, 0"
+        dbw = f"{d['busbw']:.1f}" if d else "-"
+        lines.append(f"    {{{lg}, {ring_cols}, {algo}, {dcols}}},  // {r['busbw']:.1f} / {dbw}")
     lines.append("};")
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
 
 
 def table_cmd(args):
-    rows = [json.loads(l) for l in open(args.jsonl) if l.strip()]
+    rows = []
+    for f in args.jsonl:
+        rows += [json.loads(l) for l in open(f) if l.strip()]
     table = select(rows)
-    for size, r in sorted(table.items()):
-        print(f"{size:>10} {r['proto']:6} C={r['nchannels']:3} chunk={r['chunk_bytes']:8} W={r['nwaves']} "
-              f"busBW={r['busbw']:.1f}")
+    for size, row in sorted(table.items()):
+        r, d = row["ring"], row["direct"]
+        ds = f"direct P={d['nchannels']:3} W={d['nwaves']:2} busBW={d['busbw']:7.1f}" if d else "direct -"
+        print(f"{size:>10} {row['algo']:6} | ring {r['proto']:7} C={r['nchannels']:3} chunk={r['chunk_bytes']:8} "
+              f"W={r['nwaves']} busBW={r['busbw']:6.1f} | {ds}")
     if args.emit:
         emit(table, args.emit)
 
@@ -187,19 +228,22 @@ def validate(args):
             g = torch.Generator(device="cuda:0").manual_seed(11438 + 100)
             ts = [torch.rand(count, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
             res = {}
-            for name, tuner in (("tuned", None), ("default", "fixed_default")):
+            for name, tuner, algo in (("tuned", None, "auto"), ("tuned_ring", None, "ring"),
+                                      ("default", "fixed_default", "auto")):
                 ar.ar_set_tuner(tuner)
-                plan = ar.Plan(n, count, "f32", proto="auto")
+                plan = ar.Plan(n, count, "f32", proto="auto", algo=algo)
                 ar.ar_set_tuner(None)
                 times = _timer(plan, ts, stream, reps=7)
                 med = statistics.median(times)
                 res[name] = {"t_med_us": med * 1e6, "busbw": ar.bus_bandwidth(size, med, n),
                              "cv": statistics.pstdev(times) / statistics.mean(times),
+                             "algo": plan.info["algo_name"],
                              "proto": plan.info["proto_name"], "nchannels": plan.info["nchannels"],
                              "chunk": plan.info["chunk_elems"] * 4, "nwaves": plan.info["nwaves"]}
                 plan.destroy()
             rec = {"size": size, **{f"{k}_{kk}": vv for k, v in res.items() for kk, vv in v.items()},
-                   "ratio": res["tuned"]["busbw"] / res["default"]["busbw"]}
+                   "ratio": res["tuned"]["busbw"] / res["default"]["busbw"],
+                   "ratio_ring": res["tuned_ring"]["busbw"] / res["default"]["busbw"]}
             fo.write(json.dumps(rec) + "\n")
             print(json.dumps(rec), flush=True)
             del ts
@@ -212,8 +256,9 @@ def main(argv=None):
     m.add_argument("--out", required=True)
     m.add_argument("--sizes", default="")
     m.add_argument("--nranks", type=int, default=8)
+    m.add_argument("--algo", default="", help="measure only this algorithm (ring or direct)")
     t = sub.add_parser("table")
-    t.add_argument("jsonl")
+    t.add_argument("jsonl", nargs="+")
     t.add_argument("--emit", default="")
     v = sub.add_parser("validate")
     v.add_argument("--out", required=True)

@@ -28,13 +28,19 @@ int main(int argc, char **argv)
         d.nwaves = (int)(rng() % 20) - 1;
         d.placement = (int)(rng() % 3);
         d.max_channels = (int)(rng() % 300);
+        d.algo = (int)(rng() % 4);
         ar_plan_info g;
         int rc = ar_plan_geometry(&d, &g);
         if (rc != AR_OK) continue;
         ++accepted;
         const uint64_t e = g.dtype == AR_FLOAT32 ? 4 : 2, A = 16 / e, N = (uint64_t)g.nranks;
         bool ok = g.seg_elems * N >= g.count && g.seg_elems % A == 0;
-        if (g.grid > 0) {
+        if (g.grid > 0 && g.algo == AR_ALGO_DIRECT) {
+            ok = ok && g.grid == g.nchannels * g.nranks && g.block == 64 * g.nwaves && g.nchannels >= 1;
+            ok = ok && g.chan_elems * (uint64_t)g.nchannels >= g.seg_elems && g.chan_elems % A == 0;
+            ok = ok && g.fifo_bytes == 0 && g.msgs_per_run == 0 && g.nwaves >= 1 && g.nwaves <= AR_MAX_WAVES;
+        } else if (g.grid > 0) {
+            ok = ok && g.algo == AR_ALGO_RING;
             ok = ok && g.grid == g.nchannels * g.nranks && g.block == 64 * g.nwaves;
             ok = ok && g.chan_elems * (uint64_t)g.nchannels >= g.seg_elems && g.chan_elems % A == 0;
             ok = ok && g.chunk_elems >= A && g.chunk_elems <= g.chan_elems && g.chunk_elems % A == 0;
@@ -53,7 +59,8 @@ int main(int argc, char **argv)
         ar_tune_out o;
         if (ar_tune(&c, &o) != AR_OK || (o.proto != AR_PROTO_LL && o.proto != AR_PROTO_LL128 &&
                                          o.proto != AR_PROTO_SIMPLE) ||
-            o.nchannels < 1 || o.nwaves < 1 || o.chunk_bytes < 16)
+            o.nchannels < 1 || o.nwaves < 1 || o.chunk_bytes < 16 ||
+            (o.algo != AR_ALGO_RING && o.algo != AR_ALGO_DIRECT) || o.direct_parts < 0 || o.direct_nwaves < 0)
             ++failures;
     }
     printf("iters %d accepted %ld failures %ld\n", iters, accepted, failures);

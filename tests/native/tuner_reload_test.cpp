@@ -41,6 +41,9 @@ int instance_tuner(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->nchannels = 1 + in->id % 50;
     out->chunk_bytes = 4096u * (size_t)(1 + in->id % 97);
     out->nwaves = 1 + in->id % 16;
+    out->algo = AR_ALGO_RING;
+    out->direct_parts = 0;
+    out->direct_nwaves = 0;
     (void)ctx;
     return 0;
 }
@@ -51,6 +54,9 @@ int malformed_tuner(const ar_tune_ctx *ctx, ar_tune_out *out, void *)
     out->nchannels = 4;
     out->chunk_bytes = 0;
     out->nwaves = 0;
+    out->algo = AR_ALGO_RING;
+    out->direct_parts = 0;
+    out->direct_nwaves = 0;
     return 0;
 }
 
@@ -92,7 +98,7 @@ int main(int argc, char **argv)
             long mine = total_calls / nreaders;
             ar_tune_ctx c = {AR_COLL_ALLREDUCE, (size_t)4096 << (t % 16), 8, AR_FLOAT32, AR_MAX_CHANNELS, (uint64_t)t};
             for (long i = 0; i < mine; ++i) {
-                ar_tune_out o = {-7, -7, 7, -7};
+                ar_tune_out o = {-7, -7, 7, -7, -7, -7, -7};
                 int rc = ar_tune(&c, &o);
                 if (rc != AR_OK) bad.fetch_add(1);
                 else if (!consistent(o)) torn.fetch_add(1);

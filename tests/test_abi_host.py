@@ -50,7 +50,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_version_and_strerror():
-    assert ar.ar_version() == 1
+    assert ar.ar_version() == 2
     for code in range(8):
         assert ar.ar_strerror(code)
     assert ar.ar_strerror(99) == "unknown error"
@@ -119,7 +119,8 @@ def test_tuner_sees_context():
     assert seen == {"coll": 0, "msg_bytes": 12345, "nranks": 5, "dtype": ar.AR_BFLOAT16,
                     "max_channels": 40, "comm_id": 77}
     assert d == {"proto": ar.AR_PROTO_LL128, "proto_name": "ll128", "nchannels": 3,
-                 "chunk_bytes": 992, "nwaves": ar.AR_MAX_WAVES}
+                 "chunk_bytes": 992, "nwaves": ar.AR_MAX_WAVES, "algo": ar.AR_ALGO_RING, "algo_name": "ring",
+                 "direct_parts": 0, "direct_nwaves": 0}
 
 
 def test_tune_rejects_bad_context():
@@ -228,3 +229,29 @@ def test_ring_byte_counts():
     assert abs(ar.ring_bytes(S, 8, "f32", "ll128") - (16 + 28 * 128 / 120) * S) < 1
     assert ar.ring_bytes(S, 8, "bf16", "simple") == 58 * S
     assert ar.compulsory_bytes(S, 8) == 16 * S
+
+
+# ------------------------------------------------------------- algorithms
+
+def test_direct_geometry_and_algorithm_choice():
+    g = ar.ar_plan_geometry(ar.make_desc(8, 1 << 20, "f32", algo="direct"))
+    assert g["algo"] == ar.AR_ALGO_DIRECT and g["fifo_bytes"] == 0 and g["msgs_per_run"] == 0
+    assert g["grid"] == 8 * g["nchannels"] and g["seg_elems"] == ro.segment_elems(8, 1 << 20, 4)
+    assert g["chan_elems"] * g["nchannels"] >= g["seg_elems"]
+    # a requested protocol implies the ring; direct with a protocol is an error
+    g = ar.ar_plan_geometry(ar.make_desc(8, 1 << 20, "f32", "ll", 4))
+    assert g["algo"] == ar.AR_ALGO_RING
+    info = ar.ar_plan_info()
+    d = ar.make_desc(8, 1 << 20, "f32", "simple", 4, algo="direct")
+    assert ar.lib().ar_plan_geometry(ctypes.byref(d), ctypes.byref(info)) == ar.AR_ERR_ARG
+    d = ar.make_desc(8, 1 << 20, "f32", algo=7)
+    assert ar.lib().ar_plan_geometry(ctypes.byref(d), ctypes.byref(info)) == ar.AR_ERR_ARG
+    # the tuner's algorithm choice is honoured under AUTO
+    ar.ar_set_tuner(lambda ctx: {"algo": ar.AR_ALGO_DIRECT, "proto": ar.AR_PROTO_SIMPLE, "nchannels": 5})
+    assert ar.ar_plan_geometry(ar.make_desc(8, 4096, "f32"))["algo"] == ar.AR_ALGO_DIRECT
+    # ... while the ring columns of that answer still serve a forced ring
+    g = ar.ar_plan_geometry(ar.make_desc(8, 4096, "f32", algo="ring"))
+    assert g["algo"] == ar.AR_ALGO_RING and g["nchannels"] == 5
+    ar.ar_set_tuner(lambda ctx: {"algo": 9, "proto": ar.AR_PROTO_LL, "nchannels": 5})
+    assert ar.ar_tune(4096)["algo"] == ar.AR_ALGO_RING and ar.ar_tune(4096)["nchannels"] == 16
+    ar.ar_set_tuner(None)

@@ -402,3 +402,67 @@ def test_closed_loop_adaptive_channels_on_gpu(ar):
         for p in plans.values():
             p.destroy()
     assert seen[0] == 2 and seen[-1] == 12, seen
+
+
+# -------------------------------------------------------- direct algorithm
+#
+# The direct algorithm sums each segment in the ring's chain order, so its
+# results must equal the oracle (and the ring) bit for bit.
+
+@pytest.mark.parametrize("dtype", ("f32", "bf16"))
+@pytest.mark.parametrize("n", (2, 3, 8, 9, 16))
+def test_direct_small_grid(ar, dtype, n):
+    for count in SMALL_COUNTS:
+        x = draw(n, count, dtype, "normal", seed=2000 + n * 31 + count)
+        for parts in (0, 1, 3):
+            run_case(ar, x, dtype, f"direct-{dtype}-{n}-{count}-{parts}", algo="direct", nchannels=parts)
+
+
+def test_direct_order_revealing(ar):
+    vals = np.array([2.0 ** 24, -(2.0 ** 24), 2.0 ** 25, 1.0, -1.0, 3.0, 0.5], np.float32)
+    rng = np.random.default_rng(6)
+    for n in (2, 3, 4, 8, 16):
+        for count in (4, 13, 64, 257, 5000):
+            x = rng.choice(vals, size=(n, count)).astype(np.float32)
+            run_case(ar, x, "f32", f"direct-order-{n}-{count}", algo="direct")
+
+
+@pytest.mark.parametrize("dtype", ("f32", "bf16"))
+def test_direct_equals_ring_bits(ar, dtype):
+    import torch
+
+    n, count = 8, 300007
+    x = draw(n, count, dtype, "normal", seed=4243)
+    want = oracle_bits(x, dtype)
+    base = to_device(x, dtype)
+    for cfg in (dict(algo="direct"), dict(algo="direct", nchannels=1, nwaves=1),
+                dict(algo="direct", nchannels=200, nwaves=16), dict(proto="simple", nchannels=7)):
+        ts = [t.clone() for t in base]
+        plan = ar.Plan(n, count, dtype, **cfg)
+        plan.run(ts)
+        torch.cuda.synchronize()
+        assert_ranks_equal(ts, want, dtype, str(cfg))
+        plan.destroy()
+
+
+def test_direct_full_size(ar):
+    _full_size_sweep(ar, workloads.WORKLOADS["D5"], [dict(algo="direct"), dict(algo="direct", nchannels=64)])
+    _full_size_sweep(ar, workloads.WORKLOADS["D3"], [dict(algo="direct")])
+
+
+def test_direct_out_of_place_and_repeats(ar):
+    import torch
+
+    n, count = 8, 100003
+    x = draw(n, count, "f32", "normal", seed=12)
+    want = oracle_bits(x, "f32")
+    send = to_device(x, "f32")
+    plan = ar.Plan(n, count, "f32", algo="direct")
+    for _ in range(3):
+        recv = [torch.full_like(t, float("nan")) for t in send]
+        plan.run_oop(send, recv)
+        torch.cuda.synchronize()
+        assert_ranks_equal(recv, want, "f32", "direct oop")
+    for r in range(n):
+        assert np.array_equal(to_bits(send[r], "f32"), x[r].view(np.uint32))
+    plan.destroy()
