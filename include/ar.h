@@ -335,6 +335,14 @@ typedef struct ar_adaptive_cfg {
  * back) for an invalid configuration. */
 int ar_tuner_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);
 
+/* The paper's Listing 1 closed-loop policy (section 3.3) over the same
+ * telemetry: no sample for ctx->comm_id -> 4 channels; messages of at most
+ * 32 KiB take the small-message algorithm (here AR_ALGO_DIRECT, in place of
+ * the listing's tree), larger ones the ring; Simple protocol; when the last
+ * sample's latency exceeds 1 ms, one channel more than that run used (at
+ * most 16), otherwise the same count.  user is unused. */
+int ar_tuner_size_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);
+
 /* ---- errors and version ------------------------------------------------- */
 
 const char *ar_strerror(int code);

@@ -117,6 +117,7 @@ SIGNATURES = {
     "ar_profile_lookup": (ctypes.c_int, [ctypes.c_uint64, ctypes.POINTER(ar_latency_state)]),
     "ar_profile_clear": (None, []),
     "ar_tuner_adaptive": (ctypes.c_int, [ctypes.POINTER(ar_tune_ctx), ctypes.POINTER(ar_tune_out), _P]),
+    "ar_tuner_size_adaptive": (ctypes.c_int, [ctypes.POINTER(ar_tune_ctx), ctypes.POINTER(ar_tune_out), _P]),
     "ar_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "ar_last_error": (ctypes.c_int, []),
     "ar_version": (ctypes.c_int, []),
@@ -216,6 +217,8 @@ def _tuner_callback(fn):
     L = lib()
     if fn == "adaptive":
         return ctypes.cast(L.ar_tuner_adaptive, ar_tuner_fn)
+    if fn == "size_adaptive":
+        return ctypes.cast(L.ar_tuner_size_adaptive, ar_tuner_fn)
     if fn is None or fn == "table":
         cb = ctypes.cast(L.ar_tuner_table, ar_tuner_fn)
     elif fn == "fixed_default":

@@ -228,8 +228,9 @@ def validate(args):
             g = torch.Generator(device="cuda:0").manual_seed(11438 + 100)
             ts = [torch.rand(count, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
             res = {}
+            bad = lambda ctx: {"proto": ar.AR_PROTO_SIMPLE, "nchannels": 1, "algo": ar.AR_ALGO_RING}
             for name, tuner, algo in (("tuned", None, "auto"), ("tuned_ring", None, "ring"),
-                                      ("default", "fixed_default", "auto")):
+                                      ("default", "fixed_default", "auto"), ("bad_channels", bad, "auto")):
                 ar.ar_set_tuner(tuner)
                 plan = ar.Plan(n, count, "f32", proto="auto", algo=algo)
                 ar.ar_set_tuner(None)
@@ -243,10 +244,44 @@ def validate(args):
                 plan.destroy()
             rec = {"size": size, **{f"{k}_{kk}": vv for k, v in res.items() for kk, vv in v.items()},
                    "ratio": res["tuned"]["busbw"] / res["default"]["busbw"],
-                   "ratio_ring": res["tuned_ring"]["busbw"] / res["default"]["busbw"]}
+                   "ratio_ring": res["tuned_ring"]["busbw"] / res["default"]["busbw"],
+                   "bad_channels_loss": 1 - res["bad_channels"]["busbw"] / res["default"]["busbw"]}
             fo.write(json.dumps(rec) + "\n")
             print(json.dumps(rec), flush=True)
             del ts
+
+
+def stability(args):
+    """Independent repeats of one size: fresh inputs and a fresh plan per run,
+    mean / standard deviation / coefficient of variation of bus bandwidth
+    (the paper's 20-run stability study, section 5.3)."""
+    import torch
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    n, size = args.nranks, args.size
+    count = size // 4
+    out = {}
+    for name, tuner, algo in (("tuned", None, "auto"), ("tuned_ring", None, "ring"),
+                              ("default", "fixed_default", "auto")):
+        bws = []
+        for run in range(args.runs):
+            g = torch.Generator(device="cuda:0").manual_seed(11438 + 200 + run)
+            ts = [torch.rand(count, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
+            ar.ar_set_tuner(tuner)
+            plan = ar.Plan(n, count, "f32", proto="auto", algo=algo)
+            ar.ar_set_tuner(None)
+            times = _timer(plan, ts, stream, reps=1)
+            bws.append(ar.bus_bandwidth(size, times[0], n))
+            plan.destroy()
+            del ts
+        mean = statistics.mean(bws)
+        sd = statistics.stdev(bws) if len(bws) > 1 else 0.0
+        out[name] = {"mean_busbw": mean, "sd": sd, "cv": sd / mean, "min": min(bws), "max": max(bws),
+                     "runs": len(bws)}
+        print(json.dumps({"size": size, "policy": name, **out[name]}), flush=True)
+    with open(args.out, "a") as fo:
+        fo.write(json.dumps({"size": size, **out}) + "\n")
 
 
 def main(argv=None):
@@ -263,8 +298,13 @@ def main(argv=None):
     v = sub.add_parser("validate")
     v.add_argument("--out", required=True)
     v.add_argument("--nranks", type=int, default=8)
+    st = sub.add_parser("stability")
+    st.add_argument("--out", required=True)
+    st.add_argument("--size", type=int, default=128 << 20)
+    st.add_argument("--runs", type=int, default=20)
+    st.add_argument("--nranks", type=int, default=8)
     args = ap.parse_args(argv)
-    {"measure": measure, "table": table_cmd, "validate": validate}[args.cmd](args)
+    {"measure": measure, "table": table_cmd, "validate": validate, "stability": stability}[args.cmd](args)
 
 
 if __name__ == "__main__":

@@ -104,3 +104,27 @@ def test_telemetry_concurrent_under_tsan(tmp_path):
                        env=dict(os.environ, TSAN_OPTIONS="halt_on_error=1"))
     assert r.returncode == 0, r.stdout + r.stderr
     assert "WARNING: ThreadSanitizer" not in r.stderr
+
+
+def test_listing1_policy():
+    """The paper's Listing 1 rules over the shared telemetry."""
+    ar.ar_set_tuner("size_adaptive")
+    # no map entry: 4 channels; size threshold picks the algorithm
+    d = ar.ar_tune(32 * 1024, comm_id=5)
+    assert (d["nchannels"], d["algo"], d["proto"]) == (4, ar.AR_ALGO_DIRECT, ar.AR_PROTO_SIMPLE)
+    d = ar.ar_tune(32 * 1024 + 1, comm_id=5)
+    assert (d["nchannels"], d["algo"]) == (4, ar.AR_ALGO_RING)
+    # fast runs keep the recorded channel count
+    ar.ar_profile_record(5, 500_000, 6)
+    assert ar.ar_tune(1 << 20, comm_id=5)["nchannels"] == 6
+    # slow runs (> 1 ms) add a channel, up to 16
+    ar.ar_profile_record(5, 2_000_000, 6)
+    assert ar.ar_tune(1 << 20, comm_id=5)["nchannels"] == 7
+    ar.ar_profile_record(5, 2_000_000, 16)
+    assert ar.ar_tune(1 << 20, comm_id=5)["nchannels"] == 16
+    # the closed loop converges upward under sustained slowness
+    ch = 4
+    for _ in range(20):
+        ar.ar_profile_record(8, 5_000_000, ch)
+        ch = ar.ar_tune(1 << 24, comm_id=8)["nchannels"]
+    assert ch == 16
