@@ -72,8 +72,18 @@ enum { AR_PROTO_AUTO = -1, AR_PROTO_LL = 0, AR_PROTO_LL128 = 1, AR_PROTO_SIMPLE 
  *                   message). */
 enum { AR_ALGO_AUTO = 0, AR_ALGO_RING = 1, AR_ALGO_DIRECT = 2 };
 
-/* Collective type seen by the tuner (only AllReduce is implemented). */
-enum { AR_COLL_ALLREDUCE = 0 };
+/* Collectives (paper section 2: the tuner is consulted per collective call;
+ * section 5.3 measures AllReduce and AllGather).  `count` in a plan is, for
+ *   AR_COLL_ALLREDUCE      each rank's buffer: count elements in, count out;
+ *   AR_COLL_REDUCESCATTER  each rank's result block: rank r sends N*count
+ *                          elements and receives count, block r of the sum,
+ *                          summed along the ring chain that ends at rank r
+ *                          (x_{r+1} + x_{r+2} + ... + x_r, binary32 RNE);
+ *   AR_COLL_ALLGATHER      each rank's contribution: rank r sends count
+ *                          elements and receives N*count, [x_0 | ... | x_{N-1}].
+ * ReduceScatter and AllGather need count to be a multiple of 16 bytes of
+ * elements (4 fp32, 8 bf16) so every block starts on a 16-byte boundary. */
+enum { AR_COLL_ALLREDUCE = 0, AR_COLL_REDUCESCATTER = 1, AR_COLL_ALLGATHER = 2 };
 
 /* Workgroup placement: how the grid index maps to (channel c, rank r).
  *   AR_PLACE_RANK_SPREAD   block = c*N + r (consecutive ranks on different XCDs)
@@ -127,6 +137,7 @@ typedef struct ar_plan_desc {
                               by the profiler hook (0 if unused) */
     uint32_t flags;        /* AR_PLAN_* */
     int algo;              /* AR_ALGO_* */
+    int coll;              /* AR_COLL_* (0 = AllReduce) */
 } ar_plan_desc;
 
 /* Plan flags.
@@ -154,6 +165,7 @@ typedef struct ar_plan_info {
     uint64_t msgs_per_run; /* messages per connection per run: nchunks*(2N-2) */
     uint64_t wire_bytes_per_run; /* FIFO payload+flag bytes written per run (all connections) */
     int algo;              /* AR_ALGO_RING or AR_ALGO_DIRECT */
+    int coll;              /* AR_COLL_* */
 } ar_plan_info;
 
 /* ---- plans -------------------------------------------------------------- */
@@ -171,9 +183,12 @@ ar_plan_t *ar_plan(int nranks, size_t count, int dtype, int proto, int nchannels
 /* Same as ar_plan with every knob of ar_plan_desc. */
 ar_plan_t *ar_plan_ex(const ar_plan_desc *desc);
 
-/* In-place AllReduce.  `bufs` is a host array of nranks device pointers,
- * each to `count` elements of the plan's dtype, 16-byte aligned and pairwise
- * non-overlapping; on completion each holds y.  The pointer array is copied;
+/* In-place collective.  `bufs` is a host array of nranks device pointers,
+ * 16-byte aligned and pairwise non-overlapping, each to the plan's full
+ * buffer: count elements (AllReduce) or N*count elements (ReduceScatter:
+ * rank r's result lands in block r of its buffer, at bufs[r] + r*count;
+ * AllGather: rank r's contribution is read from block r of its buffer).
+ * For AllReduce each buffer holds y on completion.  The pointer array is copied;
  * the buffers stay owned by the caller.  Enqueued asynchronously on `stream`:
  * errors found on the host are returned (AR_ERR_ARG, AR_ERR_STATE,
  * AR_ERR_HIP); a watchdog timeout inside the kernel is reported later by
@@ -181,9 +196,11 @@ ar_plan_t *ar_plan_ex(const ar_plan_desc *desc);
  * before it writes the result to that element. */
 int ar_run(ar_plan_t *plan, void *const *bufs, void *stream);
 
-/* Out-of-place AllReduce: reads send[r], writes recv[r].  recv buffers must
- * not overlap each other or any other rank's send buffer; recv[r] may equal
- * send[r].  Same numerics as ar_run. */
+/* Out-of-place collective: reads send[r], writes recv[r] (sizes per
+ * collective as above).  recv buffers must not overlap each other or any
+ * other rank's send buffer; recv[r] may equal send[r] (AllReduce) or sit at
+ * send[r] + r*count (ReduceScatter) / contain send[r] at recv[r] + r*count
+ * (AllGather), the in-place layouts.  Same numerics as ar_run. */
 int ar_run_oop(ar_plan_t *plan, const void *const *send, void *const *recv, void *stream);
 
 /* Watchdog status, to be read after the stream has been synchronised:

@@ -175,3 +175,48 @@ def recursive_sum_gamma(nranks: int) -> float:
     """
     k = max(nranks - 1, 0)
     return k * F32_UNIT_ROUNDOFF / (1.0 - k * F32_UNIT_ROUNDOFF)
+
+
+# --- ReduceScatter and AllGather --------------------------------------------
+#
+# The same ring, run as one half (paper section 2: AllGather is among the
+# collectives the tuner steers; section 5.3 measures it).  With `count`
+# elements per block and N blocks per full buffer:
+#
+# * ReduceScatter: rank r receives block r of the sum.  The ring's
+#   reduce-scatter ends each block's chain at the rank that keeps it, so
+#   block r is summed starting at rank r+1:
+#       acc = x_{r+1}[block r]; acc += x_{r+2}[block r]; ...; acc += x_r[block r]
+#   (indices mod N), each addition one binary32 RNE operation; bf16 inputs
+#   are widened and the result rounded once, as for AllReduce.
+# * AllGather: every rank receives [x_0 | x_1 | ... | x_{N-1}]: copies only.
+
+def reduce_scatter_acc(x: np.ndarray, dtype: str) -> np.ndarray:
+    """(N, N*count) inputs -> (N, count) fp32 chain sums (before bf16 rounding)."""
+    x = np.asarray(x)
+    if x.ndim != 2 or x.shape[1] % x.shape[0]:
+        raise ValueError("expected an (N, N*count) array")
+    n = x.shape[0]
+    count = x.shape[1] // n
+    xf = bf16_to_f32(x) if dtype == "bf16" else np.asarray(x, np.float32)
+    y = np.empty((n, count), np.float32)
+    for r in range(n):
+        lo, hi = r * count, (r + 1) * count
+        start = (r + 1) % n
+        acc = xf[start, lo:hi].copy()
+        for j in range(1, n):
+            acc = acc + xf[(start + j) % n, lo:hi]
+        y[r] = acc
+    return y
+
+
+def reduce_scatter(x: np.ndarray, dtype: str) -> np.ndarray:
+    """ReduceScatter-sum: (N, N*count) -> (N, count) float32 or uint16 bf16 bits."""
+    acc = reduce_scatter_acc(x, dtype)
+    return acc if dtype == "f32" else f32_to_bf16_rne(acc).reshape(acc.shape)
+
+
+def all_gather(x: np.ndarray) -> np.ndarray:
+    """AllGather: (N, count) -> every rank's (N*count) concatenation, shape (N*count,)."""
+    x = np.asarray(x)
+    return x.reshape(-1).copy()

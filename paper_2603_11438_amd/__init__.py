@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(_PKG, "_lib", "libar.so")
 # ---- constants (include/ar.h) -------------------------------------------
 AR_FLOAT32, AR_BFLOAT16 = 0, 1
 AR_PROTO_AUTO, AR_PROTO_LL, AR_PROTO_LL128, AR_PROTO_SIMPLE = -1, 0, 1, 2
-AR_COLL_ALLREDUCE = 0
+AR_COLL_ALLREDUCE, AR_COLL_REDUCESCATTER, AR_COLL_ALLGATHER = 0, 1, 2
+COLLS = {"allreduce": AR_COLL_ALLREDUCE, "reducescatter": AR_COLL_REDUCESCATTER, "allgather": AR_COLL_ALLGATHER}
 AR_PLACE_RANK_SPREAD, AR_PLACE_CHANNEL_LOCAL = 0, 1
 (AR_OK, AR_ERR_ARG, AR_ERR_UNSUPPORTED, AR_ERR_NOMEM, AR_ERR_HIP, AR_ERR_OCCUPANCY,
  AR_ERR_TIMEOUT, AR_ERR_STATE) = range(8)
@@ -44,7 +45,7 @@ class ar_plan_desc(ctypes.Structure):
                 ("fifo_depth", ctypes.c_int), ("nwaves", ctypes.c_int), ("placement", ctypes.c_int),
                 ("timeout_us", ctypes.c_uint32), ("debug_flags", ctypes.c_uint32),
                 ("max_channels", ctypes.c_int), ("comm_id", ctypes.c_uint64), ("flags", ctypes.c_uint32),
-                ("algo", ctypes.c_int)]
+                ("algo", ctypes.c_int), ("coll", ctypes.c_int)]
 
 
 class ar_plan_info(ctypes.Structure):
@@ -54,7 +55,8 @@ class ar_plan_info(ctypes.Structure):
                 ("count", ctypes.c_size_t), ("seg_elems", ctypes.c_size_t), ("chan_elems", ctypes.c_size_t),
                 ("chunk_elems", ctypes.c_size_t), ("wave_elems", ctypes.c_size_t), ("nchunks", ctypes.c_size_t),
                 ("slot_bytes", ctypes.c_size_t), ("fifo_bytes", ctypes.c_size_t), ("flag_bytes", ctypes.c_size_t),
-                ("msgs_per_run", ctypes.c_uint64), ("wire_bytes_per_run", ctypes.c_uint64), ("algo", ctypes.c_int)]
+                ("msgs_per_run", ctypes.c_uint64), ("wire_bytes_per_run", ctypes.c_uint64), ("algo", ctypes.c_int),
+                ("coll", ctypes.c_int)]
 
     def as_dict(self) -> dict:
         d = {name: getattr(self, name) for name, _ in self._fields_}
@@ -171,7 +173,7 @@ def _check(rc: int, what: str):
 def make_desc(nranks: int, count: int, dtype="f32", proto="auto", nchannels: int = 0, chunk_bytes: int = 0,
               fifo_depth: int = 0, nwaves: int = 0, placement: int = 0, timeout_us: int = 0,
               debug_flags: int = 0, max_channels: int = 0, comm_id: int = 0, flags: int = 0,
-              algo="auto") -> ar_plan_desc:
+              algo="auto", coll="allreduce") -> ar_plan_desc:
     d = ar_plan_desc()
     d.nranks = nranks
     d.dtype = DTYPES[dtype] if isinstance(dtype, str) else dtype
@@ -188,6 +190,7 @@ def make_desc(nranks: int, count: int, dtype="f32", proto="auto", nchannels: int
     d.comm_id = comm_id
     d.flags = flags
     d.algo = ALGOS[algo] if isinstance(algo, str) else algo
+    d.coll = COLLS[coll] if isinstance(coll, str) else coll
     return d
 
 
@@ -324,9 +327,10 @@ class Plan:
 
     def __init__(self, nranks: int, count: int, dtype="f32", proto="auto", nchannels: int = 0,
                  chunk_bytes: int = 0, fifo_depth: int = 0, nwaves: int = 0, placement: int = 0,
-                 timeout_us: int = 0, debug_flags: int = 0, comm_id: int = 0, flags: int = 0, algo="auto"):
+                 timeout_us: int = 0, debug_flags: int = 0, comm_id: int = 0, flags: int = 0, algo="auto",
+                 coll="allreduce"):
         self.desc = make_desc(nranks, count, dtype, proto, nchannels, chunk_bytes, fifo_depth, nwaves,
-                              placement, timeout_us, debug_flags, 0, comm_id, flags, algo)
+                              placement, timeout_us, debug_flags, 0, comm_id, flags, algo, coll)
         L = lib()
         h = L.ar_plan_ex(ctypes.byref(self.desc))
         if not h:
@@ -341,24 +345,30 @@ class Plan:
         return self._h
 
     def run(self, tensors: Sequence, stream=None) -> None:
-        """In-place AllReduce over a list of N device tensors."""
-        self._check_tensors(tensors)
+        """In-place collective over a list of N device tensors (each the full buffer)."""
+        self._check_tensors(tensors, self._full)
         rc = lib().ar_run(self._h, _ptr_array(tensors), _stream_ptr(stream))
         _check(rc, "ar_run")
 
     def run_oop(self, send: Sequence, recv: Sequence, stream=None) -> None:
-        self._check_tensors(send)
-        self._check_tensors(recv)
+        coll = self.info["coll"]
+        self._check_tensors(send, self.info["count"] if coll == AR_COLL_ALLGATHER else self._full)
+        self._check_tensors(recv, self.info["count"] if coll == AR_COLL_REDUCESCATTER else self._full)
         rc = lib().ar_run_oop(self._h, _ptr_array(send), _ptr_array(recv), _stream_ptr(stream))
         _check(rc, "ar_run_oop")
 
-    def _check_tensors(self, tensors):
-        n, count, dt = self.info["nranks"], self.info["count"], self.info["dtype"]
+    @property
+    def _full(self) -> int:
+        c = self.info["count"]
+        return c if self.info["coll"] == AR_COLL_ALLREDUCE else c * self.info["nranks"]
+
+    def _check_tensors(self, tensors, numel):
+        n, dt = self.info["nranks"], self.info["dtype"]
         if len(tensors) != n:
             raise ValueError(f"expected {n} tensors, got {len(tensors)}")
         for t in tensors:
-            if not t.is_cuda or not t.is_contiguous() or t.numel() != count or _dtype_of(t) != dt:
-                raise ValueError("each tensor must be a contiguous device tensor of the plan's count and dtype")
+            if not t.is_cuda or not t.is_contiguous() or t.numel() != numel or _dtype_of(t) != dt:
+                raise ValueError("each tensor must be a contiguous device tensor of the collective's size and dtype")
 
     def status(self) -> int:
         return lib().ar_plan_status(self._h)

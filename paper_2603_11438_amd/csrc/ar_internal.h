@@ -31,8 +31,9 @@ struct RingArgs {
     char *fifo;                      // all FIFO slots
     uint64_t *flags;                 // per-connection head/tail lines
     uint32_t *ctl;                   // abort word + status word
-    uint64_t count;                  // elements per rank
-    uint64_t seg;                    // segment length
+    uint64_t count;                  // elements of the segmented buffer (AllReduce: count;
+                                     // ReduceScatter / AllGather: N blocks of count)
+    uint64_t seg;                    // segment length (ReduceScatter / AllGather: one block)
     uint64_t cs;                     // per-channel sub-range of a segment
     uint64_t chunk;                  // per-(segment, channel) ring step
     uint64_t kw;                     // one wave's share of a chunk step
@@ -40,6 +41,7 @@ struct RingArgs {
     uint64_t epoch;                  // absolute index of this run's first message
     uint64_t timeout_ticks;          // watchdog, in 100 MHz real-time ticks
     uint32_t nranks, nchannels, nwaves, depth, nchunks, placement, debug;
+    uint32_t coll;                   // AR_COLL_*: which steps of the ring run
 };
 
 // Resolved plan geometry.  Computed on the host only.

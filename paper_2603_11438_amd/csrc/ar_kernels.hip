@@ -75,7 +75,28 @@ constexpr int kFifoSt = AR_FIFO_ST_POL;  // device-coherent FIFO writes
 constexpr int kInPol = AR_IN_POL;      // rank inputs: read once, streamed
 constexpr int kOutPol = AR_OUT_POL;    // rank outputs: written once, streamed
 
-enum Kind : int { kSend = 0, kRecvReduceSend, kRecvReduceCopySend, kRecvCopySend, kRecvCopy };
+enum Kind : int {
+    kSend = 0,            // own input -> wire (reduce-scatter start)
+    kRecvReduceSend,      // wire + own input -> wire
+    kRecvReduceCopySend,  // wire + own input -> output and wire (AllReduce owner)
+    kRecvCopySend,        // wire -> output and wire
+    kRecvCopy,            // wire -> output
+    kRecvReduceCopy,      // wire + own input -> output (ReduceScatter owner)
+    kCopySend             // own input -> output and wire (AllGather start)
+};
+
+// What a step kind does, shared by the three protocols.
+template <int KIND>
+struct KindTraits {
+    static constexpr bool kRecvRS = KIND == kRecvReduceSend || KIND == kRecvReduceCopySend || KIND == kRecvReduceCopy;
+    static constexpr bool kRecvAG = KIND == kRecvCopySend || KIND == kRecvCopy;
+    static constexpr bool kLoadIn = KIND == kSend || kRecvRS || KIND == kCopySend;
+    static constexpr bool kSendRS = KIND == kSend || KIND == kRecvReduceSend;
+    static constexpr bool kSendAG = KIND == kRecvReduceCopySend || KIND == kRecvCopySend || KIND == kCopySend;
+    static constexpr bool kWriteOut = KIND == kRecvReduceCopySend || kRecvAG || KIND == kRecvReduceCopy || KIND == kCopySend;
+    static constexpr bool kReduceToY = KIND == kRecvReduceCopySend || KIND == kRecvReduceCopy;  // y = rounded sum
+    static constexpr bool kCopyInToY = KIND == kCopySend;                                      // y = own input
+};
 
 template <int DT> struct Elem;
 template <> struct Elem<AR_FLOAT32> { static constexpr uint32_t E = 4, A = 4; };
@@ -281,12 +302,14 @@ struct SimpleStep {
     static constexpr uint32_t A = Elem<DT>::A;
     static constexpr uint32_t E = Elem<DT>::E;
     static constexpr uint32_t RSV = A / 4;  // 16-byte fp32 vectors per unit on the RS wire
-    static constexpr bool kRecvRS = KIND == kRecvReduceSend || KIND == kRecvReduceCopySend;
-    static constexpr bool kRecvAG = KIND == kRecvCopySend || KIND == kRecvCopy;
-    static constexpr bool kLoadIn = KIND == kSend || kRecvRS;
-    static constexpr bool kSendRS = KIND == kSend || KIND == kRecvReduceSend;
-    static constexpr bool kSendAG = KIND == kRecvReduceCopySend || KIND == kRecvCopySend;
-    static constexpr bool kWriteOut = KIND == kRecvReduceCopySend || kRecvAG;
+    static constexpr bool kRecvRS = KindTraits<KIND>::kRecvRS;
+    static constexpr bool kRecvAG = KindTraits<KIND>::kRecvAG;
+    static constexpr bool kLoadIn = KindTraits<KIND>::kLoadIn;
+    static constexpr bool kSendRS = KindTraits<KIND>::kSendRS;
+    static constexpr bool kSendAG = KindTraits<KIND>::kSendAG;
+    static constexpr bool kWriteOut = KindTraits<KIND>::kWriteOut;
+    static constexpr bool kReduceToY = KindTraits<KIND>::kReduceToY;
+    static constexpr bool kCopyInToY = KindTraits<KIND>::kCopyInToY;
     static constexpr int U = AR_SIMPLE_U;
 
     // Partial last unit of the buffer: element-wise data accesses.
@@ -334,7 +357,7 @@ struct SimpleStep {
     {
         (void)rin;
         float acc[A];
-        if (kSendRS || KIND == kRecvReduceCopySend) reduce(rs, in, acc);
+        if (kSendRS || kReduceToY) reduce(rs, in, acc);
         if (kSendRS) {
             for (uint32_t v = 0; v < RSV; ++v) {
                 u32x4 o = {as_u32(acc[4 * v]), as_u32(acc[4 * v + 1]), as_u32(acc[4 * v + 2]),
@@ -343,12 +366,14 @@ struct SimpleStep {
             }
         }
         u32x4 y;
-        if (KIND == kRecvReduceCopySend) {
+        if (kReduceToY) {
             if (E == 4) {
                 y = u32x4{as_u32(acc[0]), as_u32(acc[1]), as_u32(acc[2]), as_u32(acc[3])};
             } else {
                 for (int i = 0; i < 4; ++i) y[i] = pack_bf16(acc[2 * i], acc[2 * i + 1]);
             }
+        } else if (kCopyInToY) {
+            y = in;
         } else {
             y = ag;
         }
@@ -403,8 +428,8 @@ template <int DT, int KIND>
 __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst, uint32_t len)
 {
     const RingArgs &a = *g.a;
-    constexpr bool recv = KIND != kSend;
-    constexpr bool send = KIND != kRecvCopy;
+    constexpr bool recv = KindTraits<KIND>::kRecvRS || KindTraits<KIND>::kRecvAG;
+    constexpr bool send = KindTraits<KIND>::kSendRS || KindTraits<KIND>::kSendAG;
     const char *rslot = nullptr;
     char *wslot = nullptr;
     if (recv) {
@@ -445,12 +470,14 @@ struct LLStep {
     static constexpr uint32_t E = Elem<DT>::E;
     static constexpr uint32_t G = 8 / E;         // elements per group
     static constexpr uint32_t RSV = G / 2;       // 16-byte wire ops per group on the RS wire
-    static constexpr bool kRecvRS = KIND == kRecvReduceSend || KIND == kRecvReduceCopySend;
-    static constexpr bool kRecvAG = KIND == kRecvCopySend || KIND == kRecvCopy;
-    static constexpr bool kLoadIn = KIND == kSend || kRecvRS;
-    static constexpr bool kSendRS = KIND == kSend || KIND == kRecvReduceSend;
-    static constexpr bool kSendAG = KIND == kRecvReduceCopySend || KIND == kRecvCopySend;
-    static constexpr bool kWriteOut = KIND == kRecvReduceCopySend || kRecvAG;
+    static constexpr bool kRecvRS = KindTraits<KIND>::kRecvRS;
+    static constexpr bool kRecvAG = KindTraits<KIND>::kRecvAG;
+    static constexpr bool kLoadIn = KindTraits<KIND>::kLoadIn;
+    static constexpr bool kSendRS = KindTraits<KIND>::kSendRS;
+    static constexpr bool kSendAG = KindTraits<KIND>::kSendAG;
+    static constexpr bool kWriteOut = KindTraits<KIND>::kWriteOut;
+    static constexpr bool kReduceToY = KindTraits<KIND>::kReduceToY;
+    static constexpr bool kCopyInToY = KindTraits<KIND>::kCopyInToY;
     static constexpr int U = 4;
 
     __device__ static u32x2 load_in(Rsrc r, uint32_t q, uint32_t valid)
@@ -534,7 +561,7 @@ struct LLStep {
                 const uint32_t q = base + 64 * t + lane;
                 if (!valid[t]) continue;
                 float acc[G];
-                if (kSendRS || KIND == kRecvReduceCopySend) {
+                if (kSendRS || kReduceToY) {
                     if (E == 4) {
                         acc[0] = as_f32(in[t][0]);
                         acc[1] = as_f32(in[t][1]);
@@ -558,9 +585,11 @@ struct LLStep {
                     }
                 }
                 u32x2 y;
-                if (KIND == kRecvReduceCopySend) {
+                if (kReduceToY) {
                     if (E == 4) y = u32x2{as_u32(acc[0]), as_u32(acc[1])};
                     else y = u32x2{pack_bf16(acc[0], acc[1]), pack_bf16(acc[2], acc[3])};
+                } else if (kCopyInToY) {
+                    y = in[t];
                 } else {
                     y = u32x2{ag[t][0], ag[t][2]};
                 }
@@ -576,8 +605,8 @@ template <int DT, int KIND>
 __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uint32_t len)
 {
     const RingArgs &a = *g.a;
-    constexpr bool recv = KIND != kSend;
-    constexpr bool send = KIND != kRecvCopy;
+    constexpr bool recv = KindTraits<KIND>::kRecvRS || KindTraits<KIND>::kRecvAG;
+    constexpr bool send = KindTraits<KIND>::kSendRS || KindTraits<KIND>::kSendAG;
     const char *rslot = nullptr;
     char *wslot = nullptr;
     if (recv) rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.m_in, a);
@@ -618,12 +647,14 @@ constexpr uint32_t kLL128Data = 120;
 template <int DT, int KIND>
 struct LL128Step {
     static constexpr uint32_t E = Elem<DT>::E;
-    static constexpr bool kRecvRS = KIND == kRecvReduceSend || KIND == kRecvReduceCopySend;
-    static constexpr bool kRecvAG = KIND == kRecvCopySend || KIND == kRecvCopy;
-    static constexpr bool kLoadIn = KIND == kSend || kRecvRS;
-    static constexpr bool kSendRS = KIND == kSend || KIND == kRecvReduceSend;
-    static constexpr bool kSendAG = KIND == kRecvReduceCopySend || KIND == kRecvCopySend;
-    static constexpr bool kWriteOut = KIND == kRecvReduceCopySend || kRecvAG;
+    static constexpr bool kRecvRS = KindTraits<KIND>::kRecvRS;
+    static constexpr bool kRecvAG = KindTraits<KIND>::kRecvAG;
+    static constexpr bool kLoadIn = KindTraits<KIND>::kLoadIn;
+    static constexpr bool kSendRS = KindTraits<KIND>::kSendRS;
+    static constexpr bool kSendAG = KindTraits<KIND>::kSendAG;
+    static constexpr bool kWriteOut = KindTraits<KIND>::kWriteOut;
+    static constexpr bool kReduceToY = KindTraits<KIND>::kReduceToY;
+    static constexpr bool kCopyInToY = KindTraits<KIND>::kCopyInToY;
     // bf16 recvReduceCopySend changes the line format on the way through.
     static constexpr bool kRelayout = DT == AR_BFLOAT16 && KIND == kRecvReduceCopySend;
     static constexpr int U = 4;
@@ -774,9 +805,19 @@ struct LL128Step {
                         if (!act[t]) continue;
                         const uint32_t e0 = line_of[t] * epl + p * epart;
                         u32x4 out;
-                        if (kSendRS || KIND == kRecvReduceCopySend) out = rs_reduce(wire[t], in[t], nval[t]);
+                        if (kSendRS || kReduceToY) out = rs_reduce(wire[t], in[t], nval[t]);
+                        else if (kCopyInToY) out = in[t];
                         else out = wire[t];
-                        if (kWriteOut && nval[t]) store_elems(rout, e0 * E, out, nval[t], full);
+                        if (kWriteOut && nval[t]) {
+                            if (KIND == kRecvReduceCopy && E == 2) {
+                                // bf16 owner: round the fp32 sums once, 4 values per lane part
+                                const u32x4 y = {pack_bf16(as_f32(out[0]), as_f32(out[1])),
+                                                 pack_bf16(as_f32(out[2]), as_f32(out[3])), 0, 0};
+                                store_elems(rout, e0 * E, y, nval[t], full);
+                            } else {
+                                store_elems(rout, e0 * E, out, nval[t], full);
+                            }
+                        }
                         if (kSendRS || kSendAG) put_data(wo, line_of[t], p, out);
                     }
                 }
@@ -855,8 +896,8 @@ template <int DT, int KIND>
 __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, uint32_t len, uint32_t *lds)
 {
     const RingArgs &a = *g.a;
-    constexpr bool recv = KIND != kSend;
-    constexpr bool send = KIND != kRecvCopy;
+    constexpr bool recv = KindTraits<KIND>::kRecvRS || KindTraits<KIND>::kRecvAG;
+    constexpr bool send = KindTraits<KIND>::kSendRS || KindTraits<KIND>::kSendAG;
     const char *rslot = nullptr;
     char *wslot = nullptr;
     if (recv) rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.m_in, a);
@@ -931,11 +972,17 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
                                                          __HIP_MEMORY_SCOPE_AGENT)) != 0)
         return;
 
+    // Step schedule per collective (segment handled at ring step k):
+    //   AllReduce      k = 0 .. 2N-2, segment (r - k) mod N, owner of s is s-1
+    //   ReduceScatter  k = 0 .. N-1,  segment (r - 1 - k) mod N, owner of s is s
+    //   AllGather      k = 0 .. N-1,  segment (r - k) mod N, starting from the own block
     const char *src = a.src[r];
     char *dst = a.dst[r];
+    const uint32_t coll = a.coll;
+    const uint32_t nsteps = coll == AR_COLL_ALLREDUCE ? 2 * N - 1 : N;
     for (uint32_t j = 0; j < a.nchunks; ++j) {
-        for (uint32_t k = 0; k <= 2 * N - 2; ++k) {
-            const uint32_t s = (r + 2 * N - k) % N;
+        for (uint32_t k = 0; k < nsteps; ++k) {
+            const uint32_t s = coll == AR_COLL_REDUCESCATTER ? (r + 2 * N - 1 - k) % N : (r + 2 * N - k) % N;
             const uint64_t seg_lo = (uint64_t)s * a.seg;
             const uint64_t seg_hi = seg_lo + a.seg < a.count ? seg_lo + a.seg : a.count;
             const uint64_t ch_lo = seg_lo + (uint64_t)c * a.cs;
@@ -945,15 +992,27 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
             const uint64_t lo = ck_lo + (uint64_t)w * a.kw;
             if (lo + a.kw < hi) hi = lo + a.kw;
             const uint32_t len = hi > lo ? (uint32_t)(hi - lo) : 0u;
-            const uint64_t boff = (hi > lo ? lo : 0) * E;
-            const char *s_ptr = src + boff;
-            char *d_ptr = dst + boff;
+            // ReduceScatter writes, and AllGather reads, one block-sized buffer.
+            const uint64_t in_e = hi > lo ? (coll == AR_COLL_ALLGATHER ? lo - seg_lo : lo) : 0;
+            const uint64_t out_e = hi > lo ? (coll == AR_COLL_REDUCESCATTER ? lo - seg_lo : lo) : 0;
+            const char *s_ptr = src + in_e * E;
+            char *d_ptr = dst + out_e * E;
             bool ok;
-            if (k == 0) ok = do_step<PROTO, DT, kSend>(g, s_ptr, d_ptr, len, lds);
-            else if (k < N - 1) ok = do_step<PROTO, DT, kRecvReduceSend>(g, s_ptr, d_ptr, len, lds);
-            else if (k == N - 1) ok = do_step<PROTO, DT, kRecvReduceCopySend>(g, s_ptr, d_ptr, len, lds);
-            else if (k < 2 * N - 2) ok = do_step<PROTO, DT, kRecvCopySend>(g, s_ptr, d_ptr, len, lds);
-            else ok = do_step<PROTO, DT, kRecvCopy>(g, s_ptr, d_ptr, len, lds);
+            if (coll == AR_COLL_ALLREDUCE) {
+                if (k == 0) ok = do_step<PROTO, DT, kSend>(g, s_ptr, d_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, kRecvReduceSend>(g, s_ptr, d_ptr, len, lds);
+                else if (k == N - 1) ok = do_step<PROTO, DT, kRecvReduceCopySend>(g, s_ptr, d_ptr, len, lds);
+                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, kRecvCopySend>(g, s_ptr, d_ptr, len, lds);
+                else ok = do_step<PROTO, DT, kRecvCopy>(g, s_ptr, d_ptr, len, lds);
+            } else if (coll == AR_COLL_REDUCESCATTER) {
+                if (k == 0) ok = do_step<PROTO, DT, kSend>(g, s_ptr, d_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, kRecvReduceSend>(g, s_ptr, d_ptr, len, lds);
+                else ok = do_step<PROTO, DT, kRecvReduceCopy>(g, s_ptr, d_ptr, len, lds);
+            } else {
+                if (k == 0) ok = do_step<PROTO, DT, kCopySend>(g, s_ptr, d_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, kRecvCopySend>(g, s_ptr, d_ptr, len, lds);
+                else ok = do_step<PROTO, DT, kRecvCopy>(g, s_ptr, d_ptr, len, lds);
+            }
             if (!ok) return;
         }
     }
@@ -969,6 +1028,11 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
 // read once per rank and written once per rank: the compulsory 2 N S bytes,
 // no FIFOs, no flags, no waits.  In place is safe: each element is read and
 // then written by the same thread.
+//
+// The same kernel runs the other collectives directly: ReduceScatter sums
+// block s along the chain that starts at rank s+1 (the ring's order for a
+// block that ends at rank s) and writes it to rank s only; AllGather copies
+// rank s's block to block s of every rank.
 
 template <int DT, int NMAX, int U>
 __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
@@ -979,6 +1043,10 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
     const uint32_t parts = a.nchannels;
     const uint32_t s = blockIdx.x % N;
     const uint32_t part = blockIdx.x / N;
+    const uint32_t coll = a.coll;
+    const uint32_t nsrc = coll == AR_COLL_ALLGATHER ? 1u : N;       // chain length
+    const uint32_t first = coll == AR_COLL_REDUCESCATTER ? s + 1 : s;  // chain start rank
+    const uint32_t nout = coll == AR_COLL_REDUCESCATTER ? 1u : N;    // ranks written
     const uint64_t seg_lo = (uint64_t)s * a.seg;
     if (seg_lo >= a.count) return;
     const uint64_t seg_hi = seg_lo + a.seg < a.count ? seg_lo + a.seg : a.count;
@@ -986,12 +1054,16 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
     const uint32_t nfull = (uint32_t)(len / A), rem = (uint32_t)(len % A);
     const uint32_t tid = threadIdx.x, nth = blockDim.x;
 
-    // Rank j of the chain is rank (s + j) mod N.
+    // Rank j of the chain is rank (first + j) mod N.  AllGather reads a
+    // block-sized source, ReduceScatter writes a block-sized destination.
     auto in_rsrc = [&](uint32_t j) {
-        const uint32_t r = (s + j) % N;
-        return make_rsrc(a.src[r] + seg_lo * E, len * E);
+        const uint32_t r = (first + j) % N;
+        return make_rsrc(a.src[r] + (coll == AR_COLL_ALLGATHER ? 0 : seg_lo * E), len * E);
     };
-    auto out_rsrc = [&](uint32_t r) { return make_rsrc(a.dst[r] + seg_lo * E, len * E); };
+    auto out_rsrc = [&](uint32_t i) {
+        const uint32_t r = coll == AR_COLL_REDUCESCATTER ? s : i;
+        return make_rsrc(a.dst[r] + (coll == AR_COLL_REDUCESCATTER ? 0 : seg_lo * E), len * E);
+    };
 
     auto chain = [&](const u32x4 *v, float *acc) {
         if (E == 4) {
@@ -1004,7 +1076,7 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
         }
 #pragma unroll
         for (int j = 1; j < NMAX; ++j) {
-            if ((uint32_t)j < N) {
+            if ((uint32_t)j < nsrc) {
                 if (E == 4) {
                     for (int i = 0; i < 4; ++i) acc[i] = acc[i] + as_f32(v[j][i]);
                 } else {
@@ -1030,7 +1102,7 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
         u32x4 v[U][NMAX];
 #pragma unroll
         for (int j = 0; j < NMAX; ++j) {
-            if ((uint32_t)j < N) {
+            if ((uint32_t)j < nsrc) {
                 const Rsrc rin = in_rsrc(j);
 #pragma unroll
                 for (int t = 0; t < U; ++t) {
@@ -1042,13 +1114,17 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
         u32x4 y[U];
 #pragma unroll
         for (int t = 0; t < U; ++t) {
-            float acc[A];
-            chain(v[t], acc);
-            y[t] = narrow(acc);
+            if (coll == AR_COLL_ALLGATHER) {
+                y[t] = v[t][0];  // a copy keeps every bit, NaN payloads included
+            } else {
+                float acc[A];
+                chain(v[t], acc);
+                y[t] = narrow(acc);
+            }
         }
 #pragma unroll
         for (int r = 0; r < NMAX; ++r) {
-            if ((uint32_t)r < N) {
+            if ((uint32_t)r < nout) {
                 const Rsrc rout = out_rsrc(r);
 #pragma unroll
                 for (int t = 0; t < U; ++t) {
@@ -1065,7 +1141,7 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
 #pragma unroll
         for (int j = 0; j < NMAX; ++j) {
             u32x4 x = {0, 0, 0, 0};
-            if ((uint32_t)j < N) {
+            if ((uint32_t)j < nsrc) {
                 const Rsrc rin = in_rsrc(j);
 #pragma unroll
                 for (int i = 0; i < (int)A; ++i) {
@@ -1077,12 +1153,15 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
             }
             v[j] = x;
         }
-        float acc[A];
-        chain(v, acc);
-        const u32x4 y = narrow(acc);
+        u32x4 y = v[0];
+        if (coll != AR_COLL_ALLGATHER) {
+            float acc[A];
+            chain(v, acc);
+            y = narrow(acc);
+        }
 #pragma unroll
         for (int r = 0; r < NMAX; ++r) {
-            if ((uint32_t)r < N) {
+            if ((uint32_t)r < nout) {
                 const Rsrc rout = out_rsrc(r);
 #pragma unroll
                 for (int i = 0; i < (int)A; ++i) {

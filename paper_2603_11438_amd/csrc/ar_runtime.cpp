@@ -56,29 +56,43 @@ int zero_workspace(ar_plan_t *p, void *stream)
     return launch_fill_u32((uint32_t *)p->ws, p->ws_bytes / 4, 0u, stream);
 }
 
-bool ranges_overlap(uintptr_t a, uintptr_t b, size_t n)
+bool overlap2(uintptr_t a, size_t na, uintptr_t b, size_t nb) { return a < b + nb && b < a + na; }
+
+// Bytes of each rank's send and recv buffer for the plan's collective.
+void buffer_bytes(const ar_plan_t *p, size_t *send_b, size_t *recv_b)
 {
-    return a < b + n && b < a + n;
+    const size_t blk = p->info.count * (p->info.dtype == AR_FLOAT32 ? 4 : 2);
+    const size_t full = p->info.coll == AR_COLL_ALLREDUCE ? blk : blk * (size_t)p->info.nranks;
+    *send_b = p->info.coll == AR_COLL_ALLGATHER ? blk : full;
+    *recv_b = p->info.coll == AR_COLL_REDUCESCATTER ? blk : full;
 }
 
 // Validate rank buffers: non-NULL, 16-byte aligned, and no recv buffer
-// overlapping another rank's send or recv buffer.
+// overlapping another rank's send or recv buffer.  A rank's own send and
+// recv buffers may coincide only in the collective's in-place layout.
 int check_buffers(const ar_plan_t *p, const void *const *send, void *const *recv)
 {
     if (!send || !recv) return AR_ERR_ARG;
     const int n = p->info.nranks;
-    const size_t bytes = p->info.count * (p->info.dtype == AR_FLOAT32 ? 4 : 2);
-    if (bytes == 0) return AR_OK;
+    size_t sb, rb;
+    buffer_bytes(p, &sb, &rb);
+    if (sb == 0) return AR_OK;
+    const size_t blk = p->info.count * (p->info.dtype == AR_FLOAT32 ? 4 : 2);
     for (int r = 0; r < n; ++r) {
         if (!send[r] || !recv[r]) return AR_ERR_ARG;
         if (((uintptr_t)send[r] | (uintptr_t)recv[r]) & 15u) return AR_ERR_ARG;
-        if (send[r] != recv[r] && ranges_overlap((uintptr_t)send[r], (uintptr_t)recv[r], bytes)) return AR_ERR_ARG;
+        const uintptr_t s = (uintptr_t)send[r], d = (uintptr_t)recv[r];
+        bool in_place = false;
+        if (p->info.coll == AR_COLL_ALLREDUCE) in_place = s == d;
+        else if (p->info.coll == AR_COLL_REDUCESCATTER) in_place = d == s + (size_t)r * blk;
+        else in_place = s == d + (size_t)r * blk;
+        if (!in_place && overlap2(s, sb, d, rb)) return AR_ERR_ARG;
     }
     for (int r = 0; r < n; ++r) {
         for (int q = 0; q < n; ++q) {
             if (q == r) continue;
-            if (ranges_overlap((uintptr_t)recv[r], (uintptr_t)recv[q], bytes)) return AR_ERR_ARG;
-            if (ranges_overlap((uintptr_t)recv[r], (uintptr_t)send[q], bytes)) return AR_ERR_ARG;
+            if (overlap2((uintptr_t)recv[r], rb, (uintptr_t)recv[q], rb)) return AR_ERR_ARG;
+            if (overlap2((uintptr_t)recv[r], rb, (uintptr_t)send[q], sb)) return AR_ERR_ARG;
         }
     }
     return AR_OK;
@@ -122,7 +136,7 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess || dev != p->device) return ret(AR_ERR_ARG);
     if (g.grid == 0) {
-        // One rank: the sum is the input itself.
+        // One rank: every collective is a copy of its one block.
         rc = launch_copy(send[0], recv[0], bytes, stream);
         return ret(rc);
     }
@@ -141,8 +155,9 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
     a.fifo = p->fifo;
     a.flags = p->flags;
     a.ctl = p->ctl;
-    a.count = g.count;
+    a.count = g.coll == AR_COLL_ALLREDUCE ? g.count : g.count * (uint64_t)g.nranks;
     a.seg = g.seg_elems;
+    a.coll = (uint32_t)g.coll;
     a.cs = g.chan_elems;
     a.chunk = g.chunk_elems;
     a.kw = g.wave_elems;
@@ -259,7 +274,25 @@ ar_plan_t *ar_plan(int nranks, size_t count, int dtype, int proto, int nchannels
 
 int ar_run(ar_plan_t *plan, void *const *bufs, void *stream)
 {
-    return run_impl(plan, (const void *const *)bufs, bufs, stream);
+    if (!plan || !bufs) return ret(AR_ERR_ARG);
+    if (plan->info.coll == AR_COLL_ALLREDUCE) return run_impl(plan, (const void *const *)bufs, bufs, stream);
+    // ReduceScatter / AllGather in place: the block of rank r sits at r*count.
+    const int n = plan->info.nranks;
+    const size_t blk = plan->info.count * (plan->info.dtype == AR_FLOAT32 ? 4 : 2);
+    const void *send[AR_MAX_RANKS];
+    void *recv[AR_MAX_RANKS];
+    for (int r = 0; r < n; ++r) {
+        if (!bufs[r]) return ret(AR_ERR_ARG);
+        char *b = (char *)bufs[r];
+        if (plan->info.coll == AR_COLL_REDUCESCATTER) {
+            send[r] = b;
+            recv[r] = b + (size_t)r * blk;
+        } else {
+            send[r] = b + (size_t)r * blk;
+            recv[r] = b;
+        }
+    }
+    return run_impl(plan, send, recv, stream);
 }
 
 int ar_run_oop(ar_plan_t *plan, const void *const *send, void *const *recv, void *stream)

@@ -202,6 +202,7 @@ int resolve_direct(const ar_plan_desc *d, const ar_tune_out *t, ar_plan_info *ou
     int nw = d->nwaves ? d->nwaves : (t && t->direct_nwaves ? t->direct_nwaves : 4);
     ar_plan_info g = {};
     g.algo = AR_ALGO_DIRECT;
+    g.coll = d->coll;
     g.proto = AR_PROTO_AUTO;
     g.nranks = d->nranks;
     g.dtype = d->dtype;
@@ -209,7 +210,7 @@ int resolve_direct(const ar_plan_desc *d, const ar_tune_out *t, ar_plan_info *ou
     g.placement = d->placement;
     g.count = d->count;
     g.block = 64 * nw;
-    g.seg_elems = round_up(ceil_div(d->count, N), A);
+    g.seg_elems = d->coll == AR_COLL_ALLREDUCE ? round_up(ceil_div(d->count, N), A) : d->count;
     if (N == 1 || d->count == 0) {
         g.grid = 0;
         *out = g;
@@ -244,13 +245,18 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     if (d->chunk_bytes > kMaxChunkBytes) return AR_ERR_ARG;
     if (d->flags & ~(uint32_t)AR_PLAN_PROFILE) return AR_ERR_ARG;
     if (!valid_algo(d->algo)) return AR_ERR_ARG;
+    if (d->coll != AR_COLL_ALLREDUCE && d->coll != AR_COLL_REDUCESCATTER && d->coll != AR_COLL_ALLGATHER)
+        return AR_ERR_ARG;
     if (max_channels < 1) max_channels = 1;
     if (max_channels > AR_MAX_CHANNELS) max_channels = AR_MAX_CHANNELS;
 
     const uint64_t e = d->dtype == AR_FLOAT32 ? 4 : 2;
     const uint64_t A = 16 / e;
     // Per-rank byte counts stay below 2^46 so every byte offset fits easily.
-    if (d->count > (1ull << 44)) return AR_ERR_ARG;
+    if (d->count > (1ull << 44) / (uint64_t)d->nranks) return AR_ERR_ARG;
+    if (d->coll != AR_COLL_ALLREDUCE && d->count % A != 0) return AR_ERR_UNSUPPORTED;
+    // Bytes of the full per-rank buffer (what the tuner sizes its decision by).
+    const uint64_t full_bytes = d->count * e * (d->coll == AR_COLL_ALLREDUCE ? 1 : (uint64_t)d->nranks);
 
     // A requested protocol implies the ring.
     int algo = d->algo;
@@ -265,8 +271,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     bool have_t = false;
     if (algo == AR_ALGO_AUTO || (algo == AR_ALGO_RING && ring_needs_tuner) ||
         (algo == AR_ALGO_DIRECT && direct_needs_tuner)) {
-        ar_tune_ctx ctx = {AR_COLL_ALLREDUCE, (size_t)(d->count * e), d->nranks, d->dtype,
-                           max_channels, d->comm_id};
+        ar_tune_ctx ctx = {d->coll, (size_t)full_bytes, d->nranks, d->dtype, max_channels, d->comm_id};
         int rc = ar_tune(&ctx, &t);
         if (rc != AR_OK) return rc;
         have_t = true;
@@ -293,6 +298,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
 
     ar_plan_info g = {};
     g.algo = AR_ALGO_RING;
+    g.coll = d->coll;
     g.nranks = d->nranks;
     g.dtype = d->dtype;
     g.proto = proto;
@@ -304,7 +310,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     g.block = 64 * nw;
 
     const uint64_t N = (uint64_t)d->nranks;
-    g.seg_elems = round_up(ceil_div(d->count, N), A);
+    g.seg_elems = d->coll == AR_COLL_ALLREDUCE ? round_up(ceil_div(d->count, N), A) : d->count;
     if (N == 1 || d->count == 0) {
         // Nothing moves between ranks: no FIFOs, no launch of the ring kernel.
         g.grid = 0;
@@ -332,14 +338,22 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     const uint64_t conns = (uint64_t)nch * N * (uint64_t)nw;
     g.fifo_bytes = conns * (uint64_t)depth * g.slot_bytes;
     g.flag_bytes = conns * kConnFlagU64 * 8 + kCtlU32 * 4;
-    g.msgs_per_run = g.nchunks * (2 * N - 2);
+    g.msgs_per_run = g.nchunks * (d->coll == AR_COLL_ALLREDUCE ? 2 * N - 2 : N - 1);
 
-    // Wire bytes actually written per run: each element crosses 2(N-1) links,
-    // N-1 of them as an fp32 partial and N-1 as a finished value.
-    const uint64_t elems = d->count;
+    // Wire bytes actually written per run.  AllReduce: each element crosses
+    // 2(N-1) links, N-1 as an fp32 partial and N-1 as a finished value;
+    // ReduceScatter: each of N blocks crosses N-1 links as fp32 partials;
+    // AllGather: each of N blocks crosses N-1 links as data.
     const double ag_e = (double)e;
-    double rs_bytes = (double)elems * 4.0 * (double)(N - 1);
-    double ag_bytes = (double)elems * ag_e * (double)(N - 1);
+    double rs_bytes = 0, ag_bytes = 0;
+    if (d->coll == AR_COLL_ALLREDUCE) {
+        rs_bytes = (double)d->count * 4.0 * (double)(N - 1);
+        ag_bytes = (double)d->count * ag_e * (double)(N - 1);
+    } else if (d->coll == AR_COLL_REDUCESCATTER) {
+        rs_bytes = (double)d->count * (double)N * 4.0 * (double)(N - 1);
+    } else {
+        ag_bytes = (double)d->count * (double)N * ag_e * (double)(N - 1);
+    }
     double w = proto == AR_PROTO_LL ? 2.0 : (proto == AR_PROTO_LL128 ? 128.0 / 120.0 : 1.0);
     g.wire_bytes_per_run = (uint64_t)((rs_bytes + ag_bytes) * w);
 

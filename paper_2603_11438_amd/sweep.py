@@ -259,29 +259,33 @@ def stability(args):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    n, size = args.nranks, args.size
-    count = size // 4
+    n, size, coll = args.nranks, args.size, args.coll
+    # size = bytes of each rank's full buffer; AllGather / ReduceScatter
+    # plans count one block of it.
+    count = size // 4 if coll == "allreduce" else size // 4 // n
     out = {}
     for name, tuner, algo in (("tuned", None, "auto"), ("tuned_ring", None, "ring"),
                               ("default", "fixed_default", "auto")):
         bws = []
         for run in range(args.runs):
             g = torch.Generator(device="cuda:0").manual_seed(11438 + 200 + run)
-            ts = [torch.rand(count, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
+            ts = [torch.rand(size // 4, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
             ar.ar_set_tuner(tuner)
-            plan = ar.Plan(n, count, "f32", proto="auto", algo=algo)
+            plan = ar.Plan(n, count, "f32", proto="auto", algo=algo, coll=coll)
             ar.ar_set_tuner(None)
             times = _timer(plan, ts, stream, reps=1)
-            bws.append(ar.bus_bandwidth(size, times[0], n))
+            # bus bandwidth: AllReduce S/t 2(N-1)/N; AllGather / ReduceScatter S/t (N-1)/N
+            factor = 2.0 if coll == "allreduce" else 1.0
+            bws.append(size / times[0] * factor * (n - 1) / n / 1e9)
             plan.destroy()
             del ts
         mean = statistics.mean(bws)
         sd = statistics.stdev(bws) if len(bws) > 1 else 0.0
         out[name] = {"mean_busbw": mean, "sd": sd, "cv": sd / mean, "min": min(bws), "max": max(bws),
                      "runs": len(bws)}
-        print(json.dumps({"size": size, "policy": name, **out[name]}), flush=True)
+        print(json.dumps({"coll": coll, "size": size, "policy": name, **out[name]}), flush=True)
     with open(args.out, "a") as fo:
-        fo.write(json.dumps({"size": size, **out}) + "\n")
+        fo.write(json.dumps({"coll": coll, "size": size, **out}) + "\n")
 
 
 def main(argv=None):
@@ -303,6 +307,7 @@ def main(argv=None):
     st.add_argument("--size", type=int, default=128 << 20)
     st.add_argument("--runs", type=int, default=20)
     st.add_argument("--nranks", type=int, default=8)
+    st.add_argument("--coll", default="allreduce", choices=("allreduce", "allgather", "reducescatter"))
     args = ap.parse_args(argv)
     {"measure": measure, "table": table_cmd, "validate": validate, "stability": stability}[args.cmd](args)
 

@@ -358,3 +358,55 @@ def test_bf16_rne_exhaustive_vs_torch():
         nan = np.isnan(f)
         assert np.array_equal(ours[~nan], ref[~nan]), hex(start)
         assert np.all(ours[nan] == 0x7FC0)
+
+
+# ------------------------------------------------ ReduceScatter / AllGather
+
+def test_reduce_scatter_golden_order():
+    vals = {}
+    with open(os.path.join(GOLDEN, "reduce_scatter_order_n4_f32.txt")) as f:
+        for line in f:
+            line = line.split("#", 1)[0].split()
+            if line:
+                vals[line[0]] = line[1:]
+    n, count = int(vals["nranks"][0]), int(vals["count"][0])
+    x = np.repeat(np.array([float(v) for v in vals["x"]], np.float32)[:, None], n * count, axis=1)
+    y = ro.reduce_scatter(x, "f32")
+    for r, want in enumerate(vals["y"]):
+        assert np.all(y[r] == np.float32(float(want))), (r, y[r])
+
+
+def test_reduce_scatter_invariants():
+    rng = np.random.default_rng(21)
+    for dtype in ("f32", "bf16"):
+        for n in (1, 2, 3, 8, 16):
+            for count in (1, 8, 100):
+                # all ones -> n
+                ones = np.ones((n, n * count), np.float32)
+                xo = ones if dtype == "f32" else ro.f32_to_bf16_rne(ones).reshape(n, n * count)
+                y = _as_f32(ro.reduce_scatter(xo, dtype).reshape(-1), dtype)
+                assert np.all(y == n)
+                # integers exact; block r of the sum lands on rank r
+                xi = rng.integers(-8, 9, size=(n, n * count))
+                xf = xi.astype(np.float32)
+                x = xf if dtype == "f32" else ro.f32_to_bf16_rne(xf).reshape(n, n * count)
+                y = _as_f32(ro.reduce_scatter(x, dtype).reshape(-1), dtype).reshape(n, count)
+                want = xi.sum(axis=0).reshape(n, count)
+                assert np.array_equal(y.astype(np.int64), want)
+
+
+def test_reduce_scatter_brute_force_chain():
+    rng = np.random.default_rng(22)
+    for n in (2, 3, 5, 8):
+        count = 7
+        x = rng.choice(ORDER_VALUES, size=(n, n * count)).astype(np.float32)
+        y = ro.reduce_scatter(x, "f32")
+        for r in range(n):
+            for i in range(count):
+                vals = [float(x[q, r * count + i]) for q in range(n)]
+                assert float(y[r, i]) == _scalar_chain(vals, (r + 1) % n)
+
+
+def test_all_gather_is_concatenation():
+    x = np.arange(24, dtype=np.float32).reshape(4, 6)
+    assert np.array_equal(ro.all_gather(x), np.arange(24, dtype=np.float32))
