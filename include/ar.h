@@ -240,8 +240,10 @@ int ar_plan_geometry(const ar_plan_desc *desc, ar_plan_info *out);
  * (collective type, message size, rank count) plus dtype and the channel
  * capacity the decision must respect. */
 typedef struct ar_tune_ctx {
-    int coll;              /* AR_COLL_ALLREDUCE */
-    size_t msg_bytes;      /* bytes per rank */
+    int coll;              /* AR_COLL_* */
+    size_t msg_bytes;      /* bytes of one rank's full buffer: AllReduce count *
+                              element size; ReduceScatter / AllGather nranks *
+                              count * element size */
     int nranks;
     int dtype;
     int max_channels;      /* the decision is clamped to [1, max_channels] */

@@ -37,7 +37,8 @@ struct TableRow {
 
 #include "tuner_table.inc"
 
-constexpr int kTableRows = (int)(sizeof(kTable) / sizeof(kTable[0]));
+template <size_t K>
+constexpr int rows_of(const TableRow (&)[K]) { return (int)K; }
 
 constexpr int kDefaultProto = AR_PROTO_SIMPLE;
 constexpr int kDefaultChannels = 16;
@@ -403,16 +404,20 @@ int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
 {
     (void)user;
     if (!ctx || !out) return -1;
-    if (ctx->coll != AR_COLL_ALLREDUCE) {
-        // Only AllReduce is tabulated: defer to the default.
-        return ar_tuner_noop(ctx, out, nullptr);
+    const TableRow *table;
+    int nrows;
+    switch (ctx->coll) {
+    case AR_COLL_ALLREDUCE: table = kTableAllReduce; nrows = rows_of(kTableAllReduce); break;
+    case AR_COLL_REDUCESCATTER: table = kTableReduceScatter; nrows = rows_of(kTableReduceScatter); break;
+    case AR_COLL_ALLGATHER: table = kTableAllGather; nrows = rows_of(kTableAllGather); break;
+    default: return ar_tuner_noop(ctx, out, nullptr);  // not tabulated: defer to the default
     }
     int lg = 0;
     while (lg < 63 && (1ull << lg) < (unsigned long long)ctx->msg_bytes) ++lg;
-    const TableRow *row = &kTable[0];
-    for (int i = 0; i < kTableRows; ++i) {
-        row = &kTable[i];
-        if (kTable[i].log2_bytes >= lg) break;
+    const TableRow *row = &table[0];
+    for (int i = 0; i < nrows; ++i) {
+        row = &table[i];
+        if (table[i].log2_bytes >= lg) break;
     }
     out->proto = row->proto;
     out->nchannels = row->nchannels;

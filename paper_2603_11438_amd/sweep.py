@@ -65,18 +65,32 @@ DIRECT_PARTS = (0, 16, 64, 256)
 DIRECT_WAVES = (2, 4, 8, 16)
 
 
-def grid(size, protos=("ll", "ll128", "simple"), channels=(1, 2, 4, 8, 16, 32, 64), waves=(2, 4, 8)):
+def grid(size, protos=("ll", "ll128", "simple"), channels=(1, 2, 4, 8, 16, 32, 64), waves=(2, 4, 8),
+         chunks=None):
     for parts in DIRECT_PARTS:
         for w in DIRECT_WAVES:
             yield dict(algo="direct", nchannels=parts, nwaves=w)
+    chunks = chunks or CHUNKS
     for p in protos:
         for c in channels:
             for w in waves:
-                for k in CHUNKS[p]:
+                for k in chunks[p]:
                     # chunks far beyond a channel's share repeat the same geometry
-                    if k > 4 * max(size // 8 // c, 16) and k != CHUNKS[p][0]:
+                    if k > 4 * max(size // 8 // c, 16) and k != chunks[p][0]:
                         continue
                     yield dict(proto=p, nchannels=c, nwaves=w, chunk_bytes=k)
+
+
+def bus_bw(coll, size, seconds, n):
+    """Bus bandwidth, GB/s: AllReduce S/t * 2(N-1)/N; ReduceScatter and
+    AllGather S/t * (N-1)/N, with S the bytes of each rank's full buffer."""
+    factor = 2.0 if coll == "allreduce" else 1.0
+    return size / seconds * factor * (n - 1) / n / 1e9
+
+
+# A reduced ring grid for ReduceScatter / AllGather sweeps.
+SMALL_GRID = dict(channels=(4, 16, 32, 64), waves=(4, 8),
+                  chunks={"ll": (4096, 16384), "ll128": (15360, 61440), "simple": (65536, 262144)})
 
 
 def measure(args):
@@ -85,26 +99,28 @@ def measure(args):
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     sizes = [int(s) for s in args.sizes.split(",")] if args.sizes else SIZES
-    n = args.nranks
+    n, coll = args.nranks, args.coll
     with open(args.out, "a") as fo:
         for size in sizes:
-            count = size // 4
+            count = size // 4 if coll == "allreduce" else size // 4 // n
+            if count == 0:
+                continue
             g = torch.Generator(device="cuda:0").manual_seed(11438)
-            ts = [torch.rand(count, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
-            for cfg in grid(size):
+            ts = [torch.rand(size // 4, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
+            for cfg in grid(size, **({} if coll == "allreduce" else SMALL_GRID)):
                 if args.algo and cfg.get("algo", "ring") != args.algo:
                     continue
                 try:
-                    plan = ar.Plan(n, count, "f32", **cfg)
+                    plan = ar.Plan(n, count, "f32", coll=coll, **cfg)
                 except ar.ARError as e:
                     continue
                 times = _timer(plan, ts, stream)
                 info = plan.info
                 med = statistics.median(times)
-                rec = {"size": size, "nranks": n, "proto": info["proto_name"], "chunk_bytes": 0, **cfg,
+                rec = {"coll": coll, "size": size, "nranks": n, "proto": info["proto_name"], "chunk_bytes": 0, **cfg,
                        "algo": info["algo_name"], "parts_eff": info["nchannels"], "chunk_eff": info["chunk_elems"] * 4,
                        "t_med_us": med * 1e6, "t_min_us": min(times) * 1e6, "t_max_us": max(times) * 1e6,
-                       "busbw": ar.bus_bandwidth(size, med, n)}
+                       "busbw": bus_bw(coll, size, med, n)}
                 fo.write(json.dumps(rec) + "\n")
                 plan.destroy()
             fo.flush()
@@ -113,11 +129,12 @@ def measure(args):
             torch.cuda.empty_cache()
 
 
-def default_row(size, rs, nranks=8):
+def default_row(size, rs, nranks=8, coll="allreduce"):
     """The measured row that has the fixed default's geometry (Simple, 16
     channels, default chunk and waves), if the sweep contains it."""
-    g = ar.ar_plan_geometry(ar.make_desc(nranks, size // 4, "f32", "simple", 16, DEFAULT_CHUNK,
-                                         nwaves=DEFAULT_WAVES))
+    count = size // 4 if coll == "allreduce" else size // 4 // nranks
+    g = ar.ar_plan_geometry(ar.make_desc(nranks, count, "f32", "simple", 16, DEFAULT_CHUNK,
+                                         nwaves=DEFAULT_WAVES, coll=coll))
     for r in rs:
         if (r["proto"], r["nchannels"], r["nwaves"]) == ("simple", 16, DEFAULT_WAVES) and \
                 r["chunk_eff"] == g["chunk_elems"] * 4:
@@ -125,9 +142,9 @@ def default_row(size, rs, nranks=8):
     return None
 
 
-def select(rows, tie=0.02):
+def select(rows, tie=0.02, coll="allreduce"):
     """Per size: {"ring": ring choice, "direct": direct choice or None, "algo": "ring" | "direct"}."""
-    ring = select_ring([r for r in rows if r.get("algo", "ring") == "ring"], tie)
+    ring = select_ring([r for r in rows if r.get("algo", "ring") == "ring"], tie, coll)
     out = {}
     for size, rr in ring.items():
         ds = [r for r in rows if r["size"] == size and r.get("algo") == "direct"]
@@ -142,7 +159,7 @@ def select(rows, tie=0.02):
     return out
 
 
-def select_ring(rows, tie=0.02):
+def select_ring(rows, tie=0.02, coll="allreduce"):
     """Per size: the highest median bus bandwidth; candidates within `tie` of
     the best are ties, broken by fewer channels, fewer wire bytes, smaller
     chunk, fewer waves.  When the fixed default is itself within `tie` of the
@@ -154,7 +171,7 @@ def select_ring(rows, tie=0.02):
     table = {}
     for size, rs in sorted(by.items()):
         best = max(r["busbw"] for r in rs)
-        dflt = default_row(size, rs)
+        dflt = default_row(size, rs, coll=coll)
         if dflt is not None and dflt["busbw"] >= (1 - tie) * best:
             table[size] = dict(dflt, proto="default")
             continue
@@ -164,13 +181,26 @@ def select_ring(rows, tie=0.02):
     return table
 
 
-def emit(table, path):
+TABLE_NAMES = {"allreduce": "kTableAllReduce", "reducescatter": "kTableReduceScatter",
+               "allgather": "kTableAllGather"}
+
+
+def emit(tables, path):
+    """tables: {coll: per-size selection}; writes one C array per collective."""
+    out = []
+    for coll in ("allreduce", "reducescatter", "allgather"):
+        out.append(emit_one(tables.get(coll, {}), coll))
+    with open(path, "w") as f:
+        f.write("\n".join(out))
+
+
+def emit_one(table, coll):
     names = {"ll": "AR_PROTO_LL", "ll128": "AR_PROTO_LL128", "simple": "AR_PROTO_SIMPLE",
              "default": "AR_PROTO_AUTO"}
     lines = [
-        "// MI355X size -> {algorithm; ring protocol, channels, chunk, waves; direct",
-        "// workgroups per segment, waves} table for 8-rank fp32",
-        "// AllReduce, one row per power-of-two message size (bytes per rank) from",
+        f"// {coll}: MI355X size -> {{algorithm; ring protocol, channels, chunk, waves;",
+        "// direct workgroups per segment, waves} table for 8-rank fp32",
+        "// collectives, one row per power-of-two size of each rank's full buffer from",
         "// 4 KiB to 128 MiB.  A message of S bytes uses the row of the smallest size",
         "// >= S (sizes below 4 KiB use the first row, above 128 MiB the last).",
         "//",
@@ -185,8 +215,10 @@ def emit(table, path):
         "//",
         "// columns: log2(size), ring proto, nchannels, chunk_bytes, nwaves, algorithm,",
         "//          direct parts, direct waves   [busBW GB/s: ring / direct]",
-        "static const TableRow kTable[] = {",
+        f"static const TableRow {TABLE_NAMES[coll]}[] = {{",
     ]
+    if not table:
+        lines.append("    {27, AR_PROTO_AUTO, 0, 0, 0, AR_ALGO_AUTO, 0, 0},  // not measured: defer to the default")
     for size, row in sorted(table.items()):
         lg = size.bit_length() - 1
         r, d = row["ring"], row["direct"]
@@ -197,22 +229,31 @@ def emit(table, path):
         dbw = f"{d['busbw']:.1f}" if d else "-"
         lines.append(f"    {{{lg}, {ring_cols}, {algo}, {dcols}}},  // {r['busbw']:.1f} / {dbw}")
     lines.append("};")
-    with open(path, "w") as f:
-        f.write("\n".join(lines) + "\n")
+    return "\n".join(lines) + "\n"
 
 
 def table_cmd(args):
     rows = []
     for f in args.jsonl:
         rows += [json.loads(l) for l in open(f) if l.strip()]
-    table = select(rows)
+    tables = {}
+    for coll in ("allreduce", "reducescatter", "allgather"):
+        rs = [r for r in rows if r.get("coll", "allreduce") == coll]
+        if rs:
+            tables[coll] = select(rs, coll=coll)
+    for coll, table in tables.items():
+        print(f"== {coll}")
+        print_table(table)
+    if args.emit:
+        emit(tables, args.emit)
+
+
+def print_table(table):
     for size, row in sorted(table.items()):
         r, d = row["ring"], row["direct"]
         ds = f"direct P={d['nchannels']:3} W={d['nwaves']:2} busBW={d['busbw']:7.1f}" if d else "direct -"
         print(f"{size:>10} {row['algo']:6} | ring {r['proto']:7} C={r['nchannels']:3} chunk={r['chunk_bytes']:8} "
               f"W={r['nwaves']} busBW={r['busbw']:6.1f} | {ds}")
-    if args.emit:
-        emit(table, args.emit)
 
 
 def validate(args):
@@ -221,28 +262,31 @@ def validate(args):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    n = args.nranks
+    n, coll = args.nranks, args.coll
+    sizes = [int(s) for s in args.sizes.split(",")] if args.sizes else SIZES
     with open(args.out, "a") as fo:
-        for size in SIZES:
-            count = size // 4
+        for size in sizes:
+            count = size // 4 if coll == "allreduce" else size // 4 // n
+            if count == 0:
+                continue
             g = torch.Generator(device="cuda:0").manual_seed(11438 + 100)
-            ts = [torch.rand(count, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
+            ts = [torch.rand(size // 4, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
             res = {}
             bad = lambda ctx: {"proto": ar.AR_PROTO_SIMPLE, "nchannels": 1, "algo": ar.AR_ALGO_RING}
             for name, tuner, algo in (("tuned", None, "auto"), ("tuned_ring", None, "ring"),
                                       ("default", "fixed_default", "auto"), ("bad_channels", bad, "auto")):
                 ar.ar_set_tuner(tuner)
-                plan = ar.Plan(n, count, "f32", proto="auto", algo=algo)
+                plan = ar.Plan(n, count, "f32", proto="auto", algo=algo, coll=coll)
                 ar.ar_set_tuner(None)
                 times = _timer(plan, ts, stream, reps=7)
                 med = statistics.median(times)
-                res[name] = {"t_med_us": med * 1e6, "busbw": ar.bus_bandwidth(size, med, n),
+                res[name] = {"t_med_us": med * 1e6, "busbw": bus_bw(coll, size, med, n),
                              "cv": statistics.pstdev(times) / statistics.mean(times),
                              "algo": plan.info["algo_name"],
                              "proto": plan.info["proto_name"], "nchannels": plan.info["nchannels"],
                              "chunk": plan.info["chunk_elems"] * 4, "nwaves": plan.info["nwaves"]}
                 plan.destroy()
-            rec = {"size": size, **{f"{k}_{kk}": vv for k, v in res.items() for kk, vv in v.items()},
+            rec = {"coll": coll, "size": size, **{f"{k}_{kk}": vv for k, v in res.items() for kk, vv in v.items()},
                    "ratio": res["tuned"]["busbw"] / res["default"]["busbw"],
                    "ratio_ring": res["tuned_ring"]["busbw"] / res["default"]["busbw"],
                    "bad_channels_loss": 1 - res["bad_channels"]["busbw"] / res["default"]["busbw"]}
@@ -296,12 +340,15 @@ def main(argv=None):
     m.add_argument("--sizes", default="")
     m.add_argument("--nranks", type=int, default=8)
     m.add_argument("--algo", default="", help="measure only this algorithm (ring or direct)")
+    m.add_argument("--coll", default="allreduce", choices=("allreduce", "allgather", "reducescatter"))
     t = sub.add_parser("table")
     t.add_argument("jsonl", nargs="+")
     t.add_argument("--emit", default="")
     v = sub.add_parser("validate")
     v.add_argument("--out", required=True)
     v.add_argument("--nranks", type=int, default=8)
+    v.add_argument("--sizes", default="")
+    v.add_argument("--coll", default="allreduce", choices=("allreduce", "allgather", "reducescatter"))
     st = sub.add_parser("stability")
     st.add_argument("--out", required=True)
     st.add_argument("--size", type=int, default=128 << 20)

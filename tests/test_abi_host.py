@@ -77,6 +77,33 @@ def test_builtin_table_form():
     assert prev is not None
 
 
+@pytest.mark.parametrize("coll", (ar.AR_COLL_REDUCESCATTER, ar.AR_COLL_ALLGATHER))
+def test_builtin_table_per_collective(coll):
+    # ReduceScatter and AllGather have tables of their own, keyed on the bytes
+    # of one rank's full buffer, with the same bucket rule as AllReduce.
+    for k in range(12, 28):
+        d = ar.ar_tune(1 << k, coll=coll)
+        assert d["algo"] in (ar.AR_ALGO_RING, ar.AR_ALGO_DIRECT)
+        assert 1 <= d["nchannels"] <= ar.AR_MAX_CHANNELS and 1 <= d["nwaves"] <= ar.AR_MAX_WAVES
+        if k > 12:
+            assert ar.ar_tune((1 << (k - 1)) + 1, coll=coll) == d
+    assert ar.ar_tune(1 << 30, coll=coll) == ar.ar_tune(1 << 27, coll=coll)
+    # a plan asks with msg_bytes = nranks * count * element size
+    n, count = 8, (1 << 20) // 4 // 8
+    g = ar.ar_plan_geometry(ar.make_desc(n, count, "f32", "auto", 0, coll=
+                                         {ar.AR_COLL_REDUCESCATTER: "reducescatter",
+                                          ar.AR_COLL_ALLGATHER: "allgather"}[coll], algo="auto"))
+    assert g["algo"] == ar.ar_tune(1 << 20, coll=coll)["algo"]
+
+
+def test_unknown_collective_defers_to_default():
+    assert ar.ar_tune(1 << 20, coll=7) == ar.ar_tune(1 << 20, coll=7)
+    ar.ar_set_tuner("fixed_default")
+    dflt = ar.ar_tune(1 << 20)
+    ar.ar_set_tuner(None)
+    assert ar.ar_tune(1 << 20, coll=7) == dflt
+
+
 def test_fixed_default_and_noop():
     ar.ar_set_tuner("fixed_default")
     d = ar.ar_tune(1 << 20)
