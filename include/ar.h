@@ -28,8 +28,9 @@
  * return int return AR_OK (0) or an AR_ERR_* code; functions that return a
  * pointer return NULL on error and leave the code in ar_last_error().
  * Nothing here is thread-safe for one plan: use a plan from one host thread
- * and keep at most one ar_run of a plan in flight (its FIFOs and flag epoch
- * are shared by all its runs).  Different plans are independent.
+ * and keep at most one ar_run of a plan in flight, graph replays included
+ * (its FIFOs and flag epochs are shared by all its runs).  Different plans
+ * are independent.
  */
 #ifndef AR_H
 #define AR_H
@@ -161,8 +162,10 @@ typedef struct ar_plan_info {
     size_t nchunks;        /* chunk steps per channel sub-range */
     size_t slot_bytes;     /* one FIFO slot of one (connection, wave) */
     size_t fifo_bytes;     /* all FIFO slots */
-    size_t flag_bytes;     /* head/tail counters and control words */
-    uint64_t msgs_per_run; /* messages per connection per run: nchunks*(2N-2) */
+    size_t flag_bytes;     /* head/tail counters, ring epochs, control words */
+    uint64_t msgs_per_run; /* messages per connection per run: nchunks*(2N-2)
+                              (AllReduce) or nchunks*(N-1) (ReduceScatter /
+                              AllGather) */
     uint64_t wire_bytes_per_run; /* FIFO payload+flag bytes written per run (all connections) */
     int algo;              /* AR_ALGO_RING or AR_ALGO_DIRECT */
     int coll;              /* AR_COLL_* */
@@ -193,7 +196,9 @@ ar_plan_t *ar_plan_ex(const ar_plan_desc *desc);
  * errors found on the host are returned (AR_ERR_ARG, AR_ERR_STATE,
  * AR_ERR_HIP); a watchdog timeout inside the kernel is reported later by
  * ar_plan_status.  Safe in place: a rank reads each element of its input
- * before it writes the result to that element. */
+ * before it writes the result to that element.  The launch carries no
+ * per-run state (flag epochs live in the plan's device memory), so it may
+ * be captured into a HIP graph and replayed; issues no memset. */
 int ar_run(ar_plan_t *plan, void *const *bufs, void *stream);
 
 /* Out-of-place collective: reads send[r], writes recv[r] (sizes per

@@ -14,8 +14,11 @@ namespace ar {
 // two counters written by different waves share a cache line.
 //   tail: messages the sender has published on the link (sender writes)
 //   head: messages the receiver has consumed on the link (receiver writes)
+// The sender's tail line also holds, at u64 offset kEpochU64, that wave's
+// message epoch: the absolute index of its next run's first message.
 constexpr int kFlagLineU64 = 16;                 // 128 bytes
 constexpr int kConnFlagU64 = 2 * kFlagLineU64;   // tail line + head line
+constexpr int kEpochU64 = 8;                     // epoch: byte 64 of the tail line
 constexpr int kCtlU32 = 64;                      // control block: 256 bytes
 constexpr int kCtlAbort = 0;                     // nonzero: every wave must leave
 constexpr int kCtlStatus = 32;                   // sticky AR_ERR_* bit set
@@ -38,7 +41,6 @@ struct RingArgs {
     uint64_t chunk;                  // per-(segment, channel) ring step
     uint64_t kw;                     // one wave's share of a chunk step
     uint64_t slot_bytes;             // bytes of one FIFO slot
-    uint64_t epoch;                  // absolute index of this run's first message
     uint64_t timeout_ticks;          // watchdog, in 100 MHz real-time ticks
     uint32_t nranks, nchannels, nwaves, depth, nchunks, placement, debug;
     uint32_t coll;                   // AR_COLL_*: which steps of the ring run

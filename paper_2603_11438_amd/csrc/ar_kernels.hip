@@ -457,13 +457,17 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
 
 // ========================================================================= LL
 //
-// 8-byte lines {u32 data, u32 flag}; flag = low 32 bits of (message index +
-// 1), never 0 (fresh memory) nor 0xFFFFFFFF (poison) because the host
-// restarts the epoch before it could wrap.  One 16-byte store carries two
+// 8-byte lines {u32 data, u32 flag}; flag = ll_tag(message index), never 0
+// (fresh memory) nor 0xFFFFFFFF (poison).  One 16-byte store carries two
 // lines, so a lane's 16-byte access is two complete lines.  Reduce-scatter
 // lines carry one fp32 partial each; all-gather lines carry one fp32 or two
 // bf16 values.  Lanes take "groups" of 8 data bytes (2 fp32 or 4 bf16):
 // input/output 8 bytes, RS wire G lines, AG wire 2 lines (16 bytes).
+
+// LL flag of message m: (m mod (2^32 - 2)) + 1.  Two messages share a flag
+// only when their indices differ by a multiple of 2^32 - 2; the plan limits
+// how old a stale line in a slot can be to far less than that.
+__device__ __forceinline__ uint32_t ll_tag(uint64_t m) { return (uint32_t)(m % 0xFFFFFFFEull) + 1u; }
 
 template <int DT, int KIND>
 struct LLStep {
@@ -618,8 +622,8 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
     // A skipped post writes the lines with the previous message's flag, which
     // the receiver never accepts for this message.
     const bool skip = send && skip_this_post(g);
-    const uint32_t tag_out = (uint32_t)(skip ? g.m_out : g.m_out + 1);
-    if (!LLStep<DT, KIND>::run(a, src, dst, rslot, wslot, len, (uint32_t)(g.m_in + 1), tag_out)) return false;
+    const uint32_t tag_out = ll_tag(skip ? g.m_out - 1 : g.m_out);
+    if (!LLStep<DT, KIND>::run(a, src, dst, rslot, wslot, len, ll_tag(g.m_in), tag_out)) return false;
     if (send) ++g.m_out;
     if (recv) {
         // Every line of the message has been loaded and checked: the slot is free.
@@ -929,48 +933,13 @@ __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, uin
     return ll128_step<DT, KIND>(g, src, dst, len, lds);
 }
 
+// All steps of one run for one wave; false if the wave had to give up.
 template <int PROTO, int DT>
-__global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
+__device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
 {
-    __shared__ uint32_t lds_all[(PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? AR_MAX_WAVES * kLdsWordsPerWave : 1];
     constexpr uint32_t E = Elem<DT>::E;
-    const uint32_t N = a.nranks, C = a.nchannels, W = a.nwaves;
-    const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint32_t b = blockIdx.x;
-    uint32_t c, r;
-    if (a.placement == AR_PLACE_CHANNEL_LOCAL) {
-        r = b / C;
-        c = b % C;
-    } else {
-        c = b / N;
-        r = b % N;
-    }
-    const uint32_t rprev = (r + N - 1) % N;
-    const uint64_t conn_out = ((uint64_t)c * W + w) * N + r;
-    const uint64_t conn_in = ((uint64_t)c * W + w) * N + rprev;
-
-    Ring g;
-    g.a = &a;
-    g.N = N;
-    g.r = r;
-    g.c = c;
-    g.w = w;
-    g.tail_out = a.flags + conn_out * kConnFlagU64;
-    g.head_out = g.tail_out + kFlagLineU64;
-    g.tail_in = a.flags + conn_in * kConnFlagU64;
-    g.head_in = g.tail_in + kFlagLineU64;
-    g.fifo_out = a.fifo + conn_out * a.depth * a.slot_bytes;
-    g.fifo_in = a.fifo + conn_in * a.depth * a.slot_bytes;
-    g.m_out = a.epoch;
-    g.m_in = a.epoch;
-    g.head_seen = 0;
-    g.tail_seen = 0;
-    uint32_t *lds = lds_all + ((PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? w * kLdsWordsPerWave : 0);
-
-    // A previous run that timed out leaves the abort word raised: do nothing.
-    if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED,
-                                                         __HIP_MEMORY_SCOPE_AGENT)) != 0)
-        return;
+    const RingArgs &a = *g.a;
+    const uint32_t N = g.N, r = g.r, c = g.c, w = g.w;
 
     // Step schedule per collective (segment handled at ring step k):
     //   AllReduce      k = 0 .. 2N-2, segment (r - k) mod N, owner of s is s-1
@@ -1013,9 +982,70 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
                 else if (k < N - 1) ok = do_step<PROTO, DT, kRecvCopySend>(g, s_ptr, d_ptr, len, lds);
                 else ok = do_step<PROTO, DT, kRecvCopy>(g, s_ptr, d_ptr, len, lds);
             }
-            if (!ok) return;
+            if (!ok) return false;
         }
     }
+    return true;
+}
+
+template <int PROTO, int DT>
+__global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
+{
+    __shared__ uint32_t lds_all[(PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? AR_MAX_WAVES * kLdsWordsPerWave : 1];
+    const uint32_t N = a.nranks, C = a.nchannels, W = a.nwaves;
+    const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t b = blockIdx.x;
+    uint32_t c, r;
+    if (a.placement == AR_PLACE_CHANNEL_LOCAL) {
+        r = b / C;
+        c = b % C;
+    } else {
+        c = b / N;
+        r = b % N;
+    }
+    const uint32_t rprev = (r + N - 1) % N;
+    const uint64_t conn_out = ((uint64_t)c * W + w) * N + r;
+    const uint64_t conn_in = ((uint64_t)c * W + w) * N + rprev;
+
+    Ring g;
+    g.a = &a;
+    g.N = N;
+    g.r = r;
+    g.c = c;
+    g.w = w;
+    g.tail_out = a.flags + conn_out * kConnFlagU64;
+    g.head_out = g.tail_out + kFlagLineU64;
+    g.tail_in = a.flags + conn_in * kConnFlagU64;
+    g.head_in = g.tail_in + kFlagLineU64;
+    g.fifo_out = a.fifo + conn_out * a.depth * a.slot_bytes;
+    g.fifo_in = a.fifo + conn_in * a.depth * a.slot_bytes;
+    // Each wave keeps its message epoch in device memory, so a launch
+    // captured in a graph and replayed continues the counters where the last
+    // run left them.  It is read here together with the head counter of the
+    // outgoing link (whose final value from the previous run frees the first
+    // slots), so both cost one round trip.  Only this wave reads or writes
+    // its epoch, and every member of a ring sends and receives the same
+    // number of messages per run, so the members' epochs stay equal without
+    // any exchange; the next run's value is stored at once, which keeps
+    // nothing alive across the loop.  (A wave that gives up leaves the plan
+    // in its timeout state, which only ar_plan_reset clears, zeroing every
+    // epoch.)
+    uint64_t *epoch_p = g.tail_out + kEpochU64;
+    const uint64_t epoch = uniform64(flag_load(epoch_p));
+    g.head_seen = uniform64(flag_load(g.head_out));
+    after_observe();
+    if (lane_id() == 0)
+        flag_store(epoch_p, epoch + (uint64_t)a.nchunks * (a.coll == AR_COLL_ALLREDUCE ? 2 * N - 2 : N - 1));
+    g.m_out = epoch;
+    g.m_in = epoch;
+    g.tail_seen = 0;
+    uint32_t *lds = lds_all + ((PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? w * kLdsWordsPerWave : 0);
+
+    // A previous run that timed out leaves the abort word raised: do nothing.
+    if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT)) != 0)
+        return;
+    ring_steps<PROTO, DT>(g, lds);
 }
 
 // ===================================================================== direct

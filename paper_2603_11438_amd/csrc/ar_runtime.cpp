@@ -20,7 +20,6 @@ struct ar_plan_s {
     uint32_t *ctl;
     uint64_t *flags;
     char *fifo;
-    uint64_t epoch;      // absolute index of the next run's first message
     uint64_t timeout_ticks;
     int sticky;          // host-side copy of a timeout seen by ar_plan_status
     // Profiler hook (AR_PLAN_PROFILE): one pair of events around the last
@@ -33,7 +32,6 @@ namespace {
 
 constexpr uint32_t kDefaultTimeoutUs = 2000000;  // 2 s per flag wait
 constexpr uint64_t kTicksPerUs = 100;            // 100 MHz real-time counter
-constexpr uint64_t kLLTagLimit = 0xFFFFFFF0ull;  // restart the epoch before 32-bit tags wrap
 
 template <typename T>
 T *fail(int code)
@@ -49,12 +47,6 @@ int ret(int code)
 }
 
 size_t round_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
-
-int zero_workspace(ar_plan_t *p, void *stream)
-{
-    if (!p->ws) return AR_OK;
-    return launch_fill_u32((uint32_t *)p->ws, p->ws_bytes / 4, 0u, stream);
-}
 
 bool overlap2(uintptr_t a, size_t na, uintptr_t b, size_t nb) { return a < b + nb && b < a + na; }
 
@@ -140,12 +132,6 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
         rc = launch_copy(send[0], recv[0], bytes, stream);
         return ret(rc);
     }
-    if (g.algo == AR_ALGO_RING && g.proto == AR_PROTO_LL && p->epoch + g.msgs_per_run + 2 >= kLLTagLimit) {
-        // 32-bit LL flags are about to wrap: start again from zeroed memory.
-        rc = zero_workspace(p, stream);
-        if (rc != AR_OK) return ret(rc);
-        p->epoch = 0;
-    }
     RingArgs a;
     memset(&a, 0, sizeof a);
     for (int r = 0; r < g.nranks; ++r) {
@@ -162,7 +148,6 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
     a.chunk = g.chunk_elems;
     a.kw = g.wave_elems;
     a.slot_bytes = g.slot_bytes;
-    a.epoch = p->epoch;
     a.timeout_ticks = p->timeout_ticks;
     a.nranks = (uint32_t)g.nranks;
     a.nchannels = (uint32_t)g.nchannels;
@@ -179,7 +164,6 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
     rc = launch_ring(g, a, stream);
     if (rc != AR_OK) return ret(rc);
     if (timed && hipEventRecord(p->ev_stop, (hipStream_t)stream) == hipSuccess) p->ev_pending = true;
-    p->epoch += g.msgs_per_run;
     return AR_OK;
 }
 
@@ -241,7 +225,7 @@ ar_plan_t *ar_plan_ex(const ar_plan_desc *desc)
         }
     }
     if (info.grid > 0 && info.algo == AR_ALGO_RING) {
-        const size_t ctl_bytes = 256;
+        const size_t ctl_bytes = kCtlU32 * 4;
         const size_t flag_bytes = round_up(info.flag_bytes - kCtlU32 * 4, 256);
         p->ws_bytes = ctl_bytes + flag_bytes + info.fifo_bytes;
         if (hipMalloc((void **)&p->ws, p->ws_bytes) != hipSuccess) {
@@ -323,7 +307,6 @@ int ar_plan_reset(ar_plan_t *p)
         if (hipMemset(p->ws, 0, p->ws_bytes) != hipSuccess) return ret(AR_ERR_HIP);
         if (hipDeviceSynchronize() != hipSuccess) return ret(AR_ERR_HIP);
     }
-    p->epoch = 0;
     p->sticky = 0;
     return AR_OK;
 }

@@ -361,6 +361,9 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     // Sanity limits: 32-bit byte offsets inside a slot, bounded FIFO memory.
     if (g.slot_bytes > (1ull << 31)) return AR_ERR_ARG;
     if (g.fifo_bytes > (16ull << 30)) return AR_ERR_ARG;
+    // LL flags repeat every 2^32 - 2 messages; a stale line in a slot is at
+    // most depth * msgs_per_run messages old, which must stay below that.
+    if (proto == AR_PROTO_LL && g.msgs_per_run * (uint64_t)depth >= (1ull << 31)) return AR_ERR_UNSUPPORTED;
     *out = g;
     return AR_OK;
 }

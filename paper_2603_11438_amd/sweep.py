@@ -8,6 +8,8 @@ on MI355X for the simulated ring.
     python -m paper_2603_11438_amd.sweep measure --out sweep.jsonl
     python -m paper_2603_11438_amd.sweep table sweep.jsonl --emit csrc/tuner_table.inc
     python -m paper_2603_11438_amd.sweep validate --out validate.jsonl
+    python -m paper_2603_11438_amd.sweep stability --coll allgather --out stability.jsonl
+    python -m paper_2603_11438_amd.sweep latency --out latency.jsonl
 
 Selection rule per size, for the ring's columns: the highest median bus
 bandwidth wins; candidates within 2 % of the best count as ties and are
@@ -332,6 +334,80 @@ def stability(args):
         fo.write(json.dumps({"coll": coll, "size": size, **out}) + "\n")
 
 
+def _pct(v, q):
+    v = sorted(v)
+    return v[min(len(v) - 1, max(0, int(round(q * (len(v) - 1)))))]
+
+
+def _stats(times_s):
+    us = [t * 1e6 for t in times_s]
+    mean = statistics.mean(us)
+    return {"p10_us": _pct(us, 0.1), "p50_us": statistics.median(us), "p90_us": _pct(us, 0.9),
+            "cv": statistics.pstdev(us) / mean if mean else 0.0}
+
+
+def latency(args):
+    """Small-message time per call, launched back to back from the host and
+    replayed from a HIP graph that holds `--graph-runs` calls (out of place,
+    so every call does the same work)."""
+    import torch
+
+    torch.cuda.set_device(0)
+    n = args.nranks
+    sizes = [int(s) for s in args.sizes.split(",")] if args.sizes else [1 << k for k in range(12, 23)]
+    k = args.graph_runs
+    with open(args.out, "a") as fo:
+        for size in sizes:
+            count = size // 4
+            g0 = torch.Generator(device="cuda:0").manual_seed(11438 + 200)
+            send = [torch.rand(count, device="cuda:0", generator=g0) * 2 - 1 for _ in range(n)]
+            recv = [torch.empty(count, device="cuda:0") for _ in range(n)]
+            for name, kw in (("tuned", dict(proto="auto", algo="auto")), ("ring", dict(proto="auto", algo="ring")),
+                             ("direct", dict(algo="direct"))):
+                plan = ar.Plan(n, count, "f32", **kw)
+                side = torch.cuda.Stream()
+                side.wait_stream(torch.cuda.current_stream())
+                with torch.cuda.stream(side):
+                    for _ in range(5):
+                        plan.run_oop(send, recv, side)
+                    side.synchronize()
+                    eager = []
+                    for _ in range(7):
+                        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                        e0.record(side)
+                        for _ in range(k):
+                            plan.run_oop(send, recv, side)
+                        e1.record(side)
+                        e1.synchronize()
+                        eager.append(e0.elapsed_time(e1) / k / 1e3)
+                torch.cuda.synchronize()
+                graph = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(graph, stream=side):
+                    for _ in range(k):
+                        plan.run_oop(send, recv, side)
+                torch.cuda.synchronize()
+                graph.replay()
+                torch.cuda.synchronize()
+                replay = []
+                for _ in range(7):
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                    graph.replay()
+                    e1.record()
+                    e1.synchronize()
+                    replay.append(e0.elapsed_time(e1) / k / 1e3)
+                if plan.status() != ar.AR_OK:
+                    raise RuntimeError(f"{name} {size}: plan status {plan.status()}")
+                info = plan.info
+                rec = {"size": size, "policy": name, "algo": info["algo_name"], "proto": info["proto_name"],
+                       "nchannels": info["nchannels"], "nwaves": info["nwaves"], "runs_per_graph": k,
+                       "eager": _stats(eager), "graph": _stats(replay)}
+                fo.write(json.dumps(rec) + "\n")
+                print(json.dumps(rec), flush=True)
+                del graph
+                plan.destroy()
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -355,8 +431,14 @@ def main(argv=None):
     st.add_argument("--runs", type=int, default=20)
     st.add_argument("--nranks", type=int, default=8)
     st.add_argument("--coll", default="allreduce", choices=("allreduce", "allgather", "reducescatter"))
+    la = sub.add_parser("latency")
+    la.add_argument("--out", required=True)
+    la.add_argument("--sizes", default="")
+    la.add_argument("--nranks", type=int, default=8)
+    la.add_argument("--graph-runs", type=int, default=100)
     args = ap.parse_args(argv)
-    {"measure": measure, "table": table_cmd, "validate": validate, "stability": stability}[args.cmd](args)
+    {"measure": measure, "table": table_cmd, "validate": validate, "stability": stability,
+     "latency": latency}[args.cmd](args)
 
 
 if __name__ == "__main__":
