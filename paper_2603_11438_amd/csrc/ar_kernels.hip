@@ -144,6 +144,16 @@ template <int POL> __device__ __forceinline__ void st16(Rsrc r, uint32_t off, ui
 
 __device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & 63u; }
 
+// The lane index as a value the compiler may not hoist out of the step loop:
+// a step's per-lane offsets are then recomputed each step (a few ALU ops)
+// instead of being held in registers across every step of the kernel.
+__device__ __forceinline__ uint32_t step_lane()
+{
+    uint32_t l = lane_id();
+    asm volatile("" : "+v"(l));
+    return l;
+}
+
 __device__ __forceinline__ uint64_t uniform64(uint64_t v)
 {
     uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
@@ -265,11 +275,34 @@ struct Ring {
     const char *fifo_in;
     uint64_t m_out, m_in;           // absolute index of the next message out / in
     uint64_t head_seen, tail_seen;  // last counter values observed
+    uint32_t slot_out, slot_in;     // FIFO slot of message m_out / m_in: m mod depth
 };
 
-__device__ __forceinline__ char *slot_ptr(char *base, uint64_t m, const RingArgs &a)
+// LL flag of message m: the low 32 bits of m + 1.  A line left in a slot by
+// an earlier message carries that message's flag, and a plan keeps every
+// stale line fewer than 2^31 messages old (the same per-run message pattern
+// repeats, so each line of a slot is rewritten within depth * msgs_per_run
+// messages), so a stale flag never equals the current one.  Fresh (zeroed)
+// memory is only ever read within the first such window, when flags are
+// small and nonzero.
+__device__ __forceinline__ uint32_t ll_tag(uint64_t m) { return (uint32_t)m + 1u; }
+
+__device__ __forceinline__ char *slot_ptr(char *base, uint32_t slot, const RingArgs &a)
 {
-    return base + (m % a.depth) * a.slot_bytes;
+    return base + (uint64_t)slot * a.slot_bytes;
+}
+
+// Step to the next message on the outgoing / incoming link (no divisions on
+// the per-message path).
+__device__ __forceinline__ void advance_out(Ring &g)
+{
+    ++g.m_out;
+    g.slot_out = g.slot_out + 1 == g.a->depth ? 0u : g.slot_out + 1;
+}
+__device__ __forceinline__ void advance_in(Ring &g)
+{
+    ++g.m_in;
+    g.slot_in = g.slot_in + 1 == g.a->depth ? 0u : g.slot_in + 1;
 }
 
 // Sender side: wait until the slot of message m_out is free, i.e. the
@@ -388,7 +421,7 @@ struct SimpleStep {
     __device__ static void run(const RingArgs &a, const char *src, char *dst, const char *rslot,
                                char *wslot, uint32_t len)
     {
-        const uint32_t lane = lane_id();
+        const uint32_t lane = step_lane();
         const uint32_t nfull = len / A, rem = len % A;
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
@@ -434,11 +467,11 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
     char *wslot = nullptr;
     if (recv) {
         if (!wait_geq(a, g.tail_in, g.m_in + 1, g.tail_seen)) return false;
-        rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.m_in, a);
+        rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.slot_in, a);
     }
     if (send) {
         if (!acquire_send_slot(g)) return false;
-        wslot = slot_ptr(g.fifo_out, g.m_out, a);
+        wslot = slot_ptr(g.fifo_out, g.slot_out, a);
     }
     SimpleStep<DT, KIND>::run(a, src, dst, rslot, wslot, len);
     // Slot writes (and slot reads) complete before either counter moves.
@@ -446,28 +479,23 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
     if (send) {
         debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
         if (!skip_this_post(g) && lane_id() == 0) flag_store(g.tail_out, g.m_out + 1);
-        ++g.m_out;
+        advance_out(g);
     }
     if (recv) {
         if (lane_id() == 0) flag_store(g.head_in, g.m_in + 1);
-        ++g.m_in;
+        advance_in(g);
     }
     return true;
 }
 
 // ========================================================================= LL
 //
-// 8-byte lines {u32 data, u32 flag}; flag = ll_tag(message index), never 0
-// (fresh memory) nor 0xFFFFFFFF (poison).  One 16-byte store carries two
+// 8-byte lines {u32 data, u32 flag}; flag = ll_tag(message index).  One
+// 16-byte store carries two
 // lines, so a lane's 16-byte access is two complete lines.  Reduce-scatter
 // lines carry one fp32 partial each; all-gather lines carry one fp32 or two
 // bf16 values.  Lanes take "groups" of 8 data bytes (2 fp32 or 4 bf16):
 // input/output 8 bytes, RS wire G lines, AG wire 2 lines (16 bytes).
-
-// LL flag of message m: (m mod (2^32 - 2)) + 1.  Two messages share a flag
-// only when their indices differ by a multiple of 2^32 - 2; the plan limits
-// how old a stale line in a slot can be to far less than that.
-__device__ __forceinline__ uint32_t ll_tag(uint64_t m) { return (uint32_t)(m % 0xFFFFFFFEull) + 1u; }
 
 template <int DT, int KIND>
 struct LLStep {
@@ -511,7 +539,7 @@ struct LLStep {
     __device__ static bool run(const RingArgs &a, const char *src, char *dst, const char *rslot,
                                char *wslot, uint32_t len, uint32_t tag_in, uint32_t tag_out)
     {
-        const uint32_t lane = lane_id();
+        const uint32_t lane = step_lane();
         const uint32_t ng = (len + G - 1) / G;
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
@@ -613,10 +641,10 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
     constexpr bool send = KindTraits<KIND>::kSendRS || KindTraits<KIND>::kSendAG;
     const char *rslot = nullptr;
     char *wslot = nullptr;
-    if (recv) rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.m_in, a);
+    if (recv) rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.slot_in, a);
     if (send) {
         if (!acquire_send_slot(g)) return false;
-        wslot = slot_ptr(g.fifo_out, g.m_out, a);
+        wslot = slot_ptr(g.fifo_out, g.slot_out, a);
     }
     if (send) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
     // A skipped post writes the lines with the previous message's flag, which
@@ -624,12 +652,14 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
     const bool skip = send && skip_this_post(g);
     const uint32_t tag_out = ll_tag(skip ? g.m_out - 1 : g.m_out);
     if (!LLStep<DT, KIND>::run(a, src, dst, rslot, wslot, len, ll_tag(g.m_in), tag_out)) return false;
-    if (send) ++g.m_out;
+    if (send) advance_out(g);
     if (recv) {
-        // Every line of the message has been loaded and checked: the slot is free.
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        // Every line of the message has been loaded and its flag checked, so
+        // no read of the slot is outstanding: free it at once, without
+        // waiting for this step's own stores (compiler ordering only).
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         if (lane_id() == 0) flag_store(g.head_in, g.m_in + 1);
-        ++g.m_in;
+        advance_in(g);
     }
     return true;
 }
@@ -743,7 +773,7 @@ struct LL128Step {
     __device__ static bool await_lines(const RingArgs &a, Rsrc wi, u32x4 *lines, const uint32_t *line_of,
                                        const bool *act, uint64_t tag)
     {
-        const uint32_t lane = lane_id();
+        const uint32_t lane = step_lane();
         const uint32_t p = lane & 7u;
         Watchdog wd;
         while (true) {
@@ -772,7 +802,7 @@ struct LL128Step {
     __device__ static bool run(const RingArgs &a, const char *src, char *dst, const char *rslot,
                                char *wslot, uint32_t len, uint64_t tag_in, uint64_t tag_out, uint32_t *lds)
     {
-        const uint32_t lane = lane_id();
+        const uint32_t lane = step_lane();
         const uint32_t p = lane & 7u, ls = lane >> 3;
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
@@ -904,21 +934,23 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
     constexpr bool send = KindTraits<KIND>::kSendRS || KindTraits<KIND>::kSendAG;
     const char *rslot = nullptr;
     char *wslot = nullptr;
-    if (recv) rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.m_in, a);
+    // LL128 runs out of vector registers first, so it derives the slot from
+    // the message index instead of carrying the slot counters.
+    if (recv) rslot = slot_ptr(const_cast<char *>(g.fifo_in), (uint32_t)(g.m_in % a.depth), a);
     if (send) {
         if (!acquire_send_slot(g)) return false;
-        wslot = slot_ptr(g.fifo_out, g.m_out, a);
+        wslot = slot_ptr(g.fifo_out, (uint32_t)(g.m_out % a.depth), a);
     }
     if (send) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
     const bool skip = send && skip_this_post(g);
     // A skipped post: write the data but a flag from the previous message.
     const uint64_t tag_out = skip ? g.m_out : g.m_out + 1;
     if (!LL128Step<DT, KIND>::run(a, src, dst, rslot, wslot, len, g.m_in + 1, tag_out, lds)) return false;
-    if (send) ++g.m_out;
+    if (send) advance_out(g);
     if (recv) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
         if (lane_id() == 0) flag_store(g.head_in, g.m_in + 1);
-        ++g.m_in;
+        advance_in(g);
     }
     return true;
 }
@@ -949,9 +981,10 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
     char *dst = a.dst[r];
     const uint32_t coll = a.coll;
     const uint32_t nsteps = coll == AR_COLL_ALLREDUCE ? 2 * N - 1 : N;
+    const uint32_t s0 = coll == AR_COLL_REDUCESCATTER ? (r + N - 1) % N : r;
     for (uint32_t j = 0; j < a.nchunks; ++j) {
-        for (uint32_t k = 0; k < nsteps; ++k) {
-            const uint32_t s = coll == AR_COLL_REDUCESCATTER ? (r + 2 * N - 1 - k) % N : (r + 2 * N - k) % N;
+        uint32_t s = s0;
+        for (uint32_t k = 0; k < nsteps; ++k, s = s == 0 ? N - 1 : s - 1) {
             const uint64_t seg_lo = (uint64_t)s * a.seg;
             const uint64_t seg_hi = seg_lo + a.seg < a.count ? seg_lo + a.seg : a.count;
             const uint64_t ch_lo = seg_lo + (uint64_t)c * a.cs;
@@ -1038,6 +1071,7 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
         flag_store(epoch_p, epoch + (uint64_t)a.nchunks * (a.coll == AR_COLL_ALLREDUCE ? 2 * N - 2 : N - 1));
     g.m_out = epoch;
     g.m_in = epoch;
+    g.slot_out = g.slot_in = (uint32_t)(epoch % a.depth);
     g.tail_seen = 0;
     uint32_t *lds = lds_all + ((PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? w * kLdsWordsPerWave : 0);
 
