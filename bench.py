@@ -43,9 +43,18 @@ def kernel_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def read_traffic(workload: str, kernel: str) -> dict | None:
+def geometry_key(info: dict) -> str:
+    """The launch geometry a counter summary was taken with."""
+    if info["algo_name"] == "direct":
+        return f"direct parts={info['nchannels']} W={info['nwaves']}"
+    return (f"ring proto={info['proto_name']} C={info['nchannels']} W={info['nwaves']} "
+            f"chunk_elems={info['chunk_elems']} depth={info['fifo_depth']}")
+
+
+def read_traffic(workload: str, kernel: str, geometry: str) -> dict | None:
     """HBM-side bytes per launch from a committed rocprofv3 counter summary,
-    or None when there is none or the kernel source has changed since."""
+    or None when there is none, it was taken with another launch geometry,
+    or the kernel source has changed since."""
     path = os.path.join(PROFILES, f"{kernel}_{workload}_pmc.txt")
     if not os.path.exists(path):
         return None
@@ -55,7 +64,7 @@ def read_traffic(workload: str, kernel: str) -> dict | None:
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("kernel_source_sha256") != kernel_source_hash():
+    if vals.get("kernel_source_sha256") != kernel_source_hash() or vals.get("geometry") != geometry:
         return None
     try:
         return {"bytes": float(vals["traffic_bytes_per_launch"]), "file": os.path.relpath(path, ROOT)}
@@ -187,13 +196,13 @@ def main(argv=None) -> int:
         b_comp = ar.compulsory_bytes(s_bytes, n)
         b_alg = ar.ring_bytes(s_bytes, n, dtype, info["proto_name"]) if algo == "ring" else b_comp
         achieved = b_alg / t / 1e9
-        traffic = read_traffic(wl.name, kernel)
+        traffic = read_traffic(wl.name, kernel, geometry_key(info))
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": round(traffic["bytes"]) if traffic else None,
                 "kernel": (f"ring_kernel<{info['proto_name']}, {dtype}>" if algo == "ring"
                            else f"direct_kernel<{dtype}>"),
-                "algorithmic_bytes_per_launch": b_alg,
+                "algorithmic_bytes_per_launch": b_alg, "geometry": geometry_key(info),
                 "achieved_compulsory": round(b_comp / t / 1e9, 1),
                 "frac_compulsory": round(b_comp / t / 1e9 / HBM_PEAK_GBS, 4)}
         if traffic:

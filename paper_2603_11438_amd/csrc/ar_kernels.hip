@@ -322,13 +322,27 @@ __device__ __forceinline__ bool skip_this_post(const Ring &g)
     return (g.a->debug & AR_DEBUG_SKIP_POST) && g.c == 0 && g.w == 0 && g.r == 0;
 }
 
+// Byte offset, in a slot, of 16-byte vector v (of `nv` per item) of item i
+// when a message holds n items and every item is wider than one vector (the
+// fp32 partials of bf16 data).  Items are taken in blocks of 64, one per
+// lane, and within a block vector v of every item comes before vector v + 1
+// of any: one store instruction of a wave then covers one contiguous stretch
+// instead of every other 16 bytes, which would make the device-coherent
+// write-through send each 64-byte sector twice.  With nv = 1 this is i * 16.
+__device__ __forceinline__ uint32_t wide_off(uint32_t i, uint32_t v, uint32_t nv, uint32_t n)
+{
+    const uint32_t blk = i & ~63u;
+    const uint32_t in_blk = n - blk < 64u ? n - blk : 64u;
+    return blk * nv * 16 + v * in_blk * 16 + (i & 63u) * 16;
+}
+
 // ===================================================================== Simple
 //
-// Slot layout: the message's elements back to back, as fp32 partials during
-// the reduce-scatter (A*4 bytes per unit of A elements) and in the data type
-// during the all-gather (16 bytes per unit).  A unit is A elements = 16 bytes
-// of the data type; lanes take consecutive units, U units per lane per batch,
-// all loads of a batch before its stores.
+// Slot layout: the message's elements as fp32 partials during the
+// reduce-scatter (A*4 bytes per unit of A elements, placed by wide_off) and
+// in the data type during the all-gather (16 bytes per unit, back to back).
+// A unit is A elements = 16 bytes of the data type; lanes take consecutive
+// units, U units per lane per batch, all loads of a batch before its stores.
 
 template <int DT, int KIND>
 struct SimpleStep {
@@ -385,7 +399,7 @@ struct SimpleStep {
         }
     }
 
-    __device__ static void unit(Rsrc rin, Rsrc rout, Rsrc wi, Rsrc wo, uint32_t u, uint32_t valid,
+    __device__ static void unit(Rsrc rin, Rsrc rout, Rsrc wi, Rsrc wo, uint32_t u, uint32_t valid, uint32_t nunits,
                                 const u32x4 &in, const u32x4 *rs, const u32x4 &ag)
     {
         (void)rin;
@@ -395,7 +409,7 @@ struct SimpleStep {
             for (uint32_t v = 0; v < RSV; ++v) {
                 u32x4 o = {as_u32(acc[4 * v]), as_u32(acc[4 * v + 1]), as_u32(acc[4 * v + 2]),
                            as_u32(acc[4 * v + 3])};
-                st128<kFifoSt>(wo, u * (A * 4) + 16 * v, o);
+                st128<kFifoSt>(wo, wide_off(u, v, RSV, nunits), o);
             }
         }
         u32x4 y;
@@ -423,6 +437,7 @@ struct SimpleStep {
     {
         const uint32_t lane = step_lane();
         const uint32_t nfull = len / A, rem = len % A;
+        const uint32_t nunits = nfull + (rem ? 1u : 0u);
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
         const Rsrc wi = make_rsrc(rslot, a.slot_bytes);
@@ -435,14 +450,14 @@ struct SimpleStep {
                 if (u < nfull) {
                     if (kLoadIn) in[t] = ld128<kInPol>(rin, u * 16);
                     if (kRecvRS)
-                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoLd>(wi, u * (A * 4) + 16 * v);
+                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoLd>(wi, wide_off(u, v, RSV, nunits));
                     if (kRecvAG) ag[t] = ld128<kFifoLd>(wi, u * 16);
                 }
             }
 #pragma unroll
             for (int t = 0; t < U; ++t) {
                 const uint32_t u = base + 64 * t + lane;
-                if (u < nfull) unit(rin, rout, wi, wo, u, A, in[t], rs[t], ag[t]);
+                if (u < nfull) unit(rin, rout, wi, wo, u, A, nunits, in[t], rs[t], ag[t]);
             }
         }
         if (rem && lane == (nfull & 63u)) {
@@ -450,9 +465,9 @@ struct SimpleStep {
             u32x4 in = {0, 0, 0, 0}, rs[RSV], ag = {0, 0, 0, 0};
             if (kLoadIn) in = load_in_partial(rin, u * 16, rem);
             if (kRecvRS)
-                for (uint32_t v = 0; v < RSV; ++v) rs[v] = ld128<kFifoLd>(wi, u * (A * 4) + 16 * v);
+                for (uint32_t v = 0; v < RSV; ++v) rs[v] = ld128<kFifoLd>(wi, wide_off(u, v, RSV, nunits));
             if (kRecvAG) ag = ld128<kFifoLd>(wi, u * 16);
-            unit(rin, rout, wi, wo, u, rem, in, rs, ag);
+            unit(rin, rout, wi, wo, u, rem, nunits, in, rs, ag);
         }
     }
 };
@@ -491,11 +506,11 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
 // ========================================================================= LL
 //
 // 8-byte lines {u32 data, u32 flag}; flag = ll_tag(message index).  One
-// 16-byte store carries two
-// lines, so a lane's 16-byte access is two complete lines.  Reduce-scatter
-// lines carry one fp32 partial each; all-gather lines carry one fp32 or two
-// bf16 values.  Lanes take "groups" of 8 data bytes (2 fp32 or 4 bf16):
-// input/output 8 bytes, RS wire G lines, AG wire 2 lines (16 bytes).
+// 16-byte store carries two lines, so a lane's 16-byte access is two complete
+// lines.  Reduce-scatter lines carry one fp32 partial each; all-gather lines
+// carry one fp32 or two bf16 values.  Lanes take "groups" of 8 data bytes (2
+// fp32 or 4 bf16): input/output 8 bytes, RS wire G lines (placed by
+// wide_off), AG wire 2 lines (16 bytes).
 
 template <int DT, int KIND>
 struct LLStep {
@@ -556,7 +571,7 @@ struct LLStep {
                 if (valid[t]) {
                     if (kLoadIn) in[t] = load_in(rin, q, valid[t]);
                     if (kRecvRS)
-                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoLd>(wi, q * (G * 8) + 16 * v);
+                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoLd>(wi, wide_off(q, v, RSV, ng));
                     if (kRecvAG) ag[t] = ld128<kFifoLd>(wi, q * 16);
                 }
             }
@@ -582,7 +597,7 @@ struct LLStep {
                         if (!valid[t]) continue;
                         if (kRecvRS)
                             for (uint32_t v = 0; v < RSV; ++v)
-                                if (!lines_ok(rs[t][v], tag_in)) rs[t][v] = ld128<kFifoLd>(wi, q * (G * 8) + 16 * v);
+                                if (!lines_ok(rs[t][v], tag_in)) rs[t][v] = ld128<kFifoLd>(wi, wide_off(q, v, RSV, ng));
                         if (kRecvAG)
                             if (!lines_ok(ag[t], tag_in)) ag[t] = ld128<kFifoLd>(wi, q * 16);
                     }
@@ -613,7 +628,7 @@ struct LLStep {
                 if (kSendRS) {
                     for (uint32_t v = 0; v < RSV; ++v) {
                         u32x4 o = {as_u32(acc[2 * v]), tag_out, as_u32(acc[2 * v + 1]), tag_out};
-                        st128<kFifoSt>(wo, q * (G * 8) + 16 * v, o);
+                        st128<kFifoSt>(wo, wide_off(q, v, RSV, ng), o);
                     }
                 }
                 u32x2 y;

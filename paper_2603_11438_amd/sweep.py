@@ -10,6 +10,7 @@ on MI355X for the simulated ring.
     python -m paper_2603_11438_amd.sweep validate --out validate.jsonl
     python -m paper_2603_11438_amd.sweep stability --coll allgather --out stability.jsonl
     python -m paper_2603_11438_amd.sweep latency --out latency.jsonl
+    python -m paper_2603_11438_amd.sweep configs --out configs.jsonl
 
 Selection rule per size, for the ring's columns: the highest median bus
 bandwidth wins; candidates within 2 % of the best count as ties and are
@@ -408,6 +409,94 @@ def latency(args):
                 plan.destroy()
 
 
+def _to_device(x, dtype):
+    """(N, count) numpy array (float32, or uint16 bf16 bits) -> one device tensor per rank."""
+    import numpy as np
+    import torch
+
+    if dtype == "f32":
+        return [torch.from_numpy(np.ascontiguousarray(x[r])).to("cuda:0") for r in range(x.shape[0])]
+    return [torch.from_numpy(np.ascontiguousarray(x[r]).view(np.int16)).view(torch.bfloat16).to("cuda:0")
+            for r in range(x.shape[0])]
+
+
+def _config_points(name):
+    """Plan settings of each measured point of the named workload."""
+    import workloads
+
+    wl = workloads.WORKLOADS[name]
+    if name == "D1":
+        return wl, [dict(proto="simple", nchannels=1, chunk_bytes=1024)]
+    if name == "D2":
+        return wl, [dict(proto=p, nchannels=c) for p in wl.protos for c in wl.channels]
+    if name == "D3":
+        return wl, [dict(proto="simple", nchannels=c, chunk_bytes=k) for k in wl.chunks for c in wl.channels]
+    if name == "D5":
+        return wl, [dict(proto=p, nchannels=c) for p in wl.protos for c in wl.channels]
+    raise ValueError(name)
+
+
+def configs(args):
+    """The named workloads at their stated settings: time per call (median,
+    p10, p90, CV over 7 repeats), algBW / busBW, the fraction of 8 TB/s on
+    the ring-byte and compulsory-byte bases, and ring bytes per element."""
+    import torch
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    peak = 8000.0  # GB/s
+    with open(args.out, "a") as fo:
+        for name in args.names.split(","):
+            wl, points = _config_points(name)
+            n, count, dtype = wl.nranks, wl.count, wl.dtype
+            size = wl.bytes_per_rank
+            ts = _to_device(wl.draw(), dtype)
+            for cfg in points:
+                plan = ar.Plan(n, count, dtype, **cfg)
+                times = _timer(plan, ts, stream, reps=7, warm=5)
+                info = plan.info
+                st = _stats(times)
+                t = st["p50_us"] * 1e-6
+                rb = ar.ring_bytes(size, n, dtype, info["proto_name"])
+                cb = ar.compulsory_bytes(size, n)
+                rec = {"workload": name, "size": size, "dtype": dtype, **cfg, "proto": info["proto_name"],
+                       "nchannels_eff": info["nchannels"], "chunk_eff": info["chunk_elems"] * (4 if dtype == "f32" else 2),
+                       "nwaves": info["nwaves"], "nchunks": info["nchunks"], **st,
+                       "algbw": ar.alg_bandwidth(size, t), "busbw": ar.bus_bandwidth(size, t, n),
+                       "hbm_frac_ring": rb / t / 1e9 / peak, "hbm_frac_comp": cb / t / 1e9 / peak,
+                       "ring_bytes_per_elem": rb / count}
+                if name == "D1":
+                    graph = torch.cuda.CUDAGraph()
+                    side = torch.cuda.Stream()
+                    side.wait_stream(torch.cuda.current_stream())
+                    with torch.cuda.stream(side):
+                        plan.run(ts, side)
+                    torch.cuda.synchronize()
+                    with torch.cuda.graph(graph, stream=side):
+                        for _ in range(100):
+                            plan.run(ts, side)
+                    graph.replay()
+                    torch.cuda.synchronize()
+                    rep = []
+                    for _ in range(7):
+                        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                        e0.record()
+                        graph.replay()
+                        e1.record()
+                        e1.synchronize()
+                        rep.append(e0.elapsed_time(e1) / 100 / 1e3)
+                    rec["graph"] = _stats(rep)
+                    del graph
+                if plan.status() != ar.AR_OK:
+                    raise RuntimeError(f"{name} {cfg}: plan status {plan.status()}")
+                plan.destroy()
+                fo.write(json.dumps(rec) + "\n")
+                fo.flush()
+                print(json.dumps(rec), flush=True)
+            del ts
+            torch.cuda.empty_cache()
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -431,6 +520,9 @@ def main(argv=None):
     st.add_argument("--runs", type=int, default=20)
     st.add_argument("--nranks", type=int, default=8)
     st.add_argument("--coll", default="allreduce", choices=("allreduce", "allgather", "reducescatter"))
+    co = sub.add_parser("configs")
+    co.add_argument("--out", required=True)
+    co.add_argument("--names", default="D1,D2,D3,D5")
     la = sub.add_parser("latency")
     la.add_argument("--out", required=True)
     la.add_argument("--sizes", default="")
@@ -438,7 +530,7 @@ def main(argv=None):
     la.add_argument("--graph-runs", type=int, default=100)
     args = ap.parse_args(argv)
     {"measure": measure, "table": table_cmd, "validate": validate, "stability": stability,
-     "latency": latency}[args.cmd](args)
+     "latency": latency, "configs": configs}[args.cmd](args)
 
 
 if __name__ == "__main__":
