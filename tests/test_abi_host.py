@@ -222,6 +222,9 @@ def test_geometry_trivial_cases():
     (dict(placement=3), ar.AR_ERR_ARG),
     (dict(chunk_bytes=1 << 30), ar.AR_ERR_ARG),
     (dict(nchannels=20, max_channels=10), ar.AR_ERR_OCCUPANCY),
+    # LL flags are 32-bit: a plan whose slots could hold a line 2^31 messages
+    # old is refused (here 2^28 one-unit chunks x 14 messages x depth 4).
+    (dict(count=1 << 33, proto="ll", nchannels=1, nwaves=1, chunk_bytes=16), ar.AR_ERR_UNSUPPORTED),
 ])
 def test_geometry_errors(kw, code):
     base = dict(nranks=8, count=1 << 20, dtype="f32", proto="simple", nchannels=4)
