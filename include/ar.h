@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define AR_VERSION 2
+#define AR_VERSION 3
 #define AR_MAX_RANKS 16
 #define AR_MAX_CHANNELS 256
 #define AR_MAX_WAVES 16
@@ -146,8 +146,16 @@ typedef struct ar_plan_desc {
  *                    launch) into the telemetry map under desc.comm_id.  A
  *                    run's sample is harvested without blocking by a later
  *                    ar_run, or by ar_plan_status; a run whose predecessor's
- *                    events are still pending is not timed. */
-enum { AR_PLAN_PROFILE = 1u };
+ *                    events are still pending is not timed.
+ *   AR_PLAN_FIFO_ALLGATHER  Simple ring only: carry the all-gather half
+ *                    through the FIFOs.  By default the Simple ring writes
+ *                    each finished chunk straight into the next rank's
+ *                    output buffer and forwards it from there: no FIFO copy,
+ *                    and nothing moves on the last hop.  The result bits are
+ *                    the same either way.  The other protocols always use
+ *                    their FIFOs, and the direct algorithm has none, so they
+ *                    ignore the flag. */
+enum { AR_PLAN_PROFILE = 1u, AR_PLAN_FIFO_ALLGATHER = 2u };
 
 /* Resolved plan geometry (after the tuner and defaults). */
 typedef struct ar_plan_info {
@@ -166,9 +174,14 @@ typedef struct ar_plan_info {
     uint64_t msgs_per_run; /* messages per connection per run: nchunks*(2N-2)
                               (AllReduce) or nchunks*(N-1) (ReduceScatter /
                               AllGather) */
-    uint64_t wire_bytes_per_run; /* FIFO payload+flag bytes written per run (all connections) */
+    uint64_t wire_bytes_per_run; /* bytes that cross ring links per run (all
+                              connections): written to a FIFO with flags, or
+                              with the direct all-gather into the next rank's
+                              output */
     int algo;              /* AR_ALGO_RING or AR_ALGO_DIRECT */
     int coll;              /* AR_COLL_* */
+    int ag_direct;         /* 1: the Simple ring's all-gather writes into the
+                              next rank's output (see AR_PLAN_FIFO_ALLGATHER) */
 } ar_plan_info;
 
 /* ---- plans -------------------------------------------------------------- */

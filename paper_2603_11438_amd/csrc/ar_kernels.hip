@@ -343,8 +343,17 @@ __device__ __forceinline__ uint32_t wide_off(uint32_t i, uint32_t v, uint32_t nv
 // in the data type during the all-gather (16 bytes per unit, back to back).
 // A unit is A elements = 16 bytes of the data type; lanes take consecutive
 // units, U units per lane per batch, all loads of a batch before its stores.
+//
+// DAG (direct all-gather): an all-gather message is not staged in the FIFO.
+// The sender writes the finished values straight into the next rank's output
+// buffer, at the place they belong, and announces them with the same tail
+// counter; the receiver forwards them from its own output buffer, and the
+// last hop of the ring moves no data at all.  The all-gather half then costs
+// two accesses per element and hop instead of three.  Every access to an
+// output buffer in this mode is device-coherent, because ranks on other
+// XCDs write into it.
 
-template <int DT, int KIND>
+template <int DT, int KIND, bool DAG>
 struct SimpleStep {
     static constexpr uint32_t A = Elem<DT>::A;
     static constexpr uint32_t E = Elem<DT>::E;
@@ -358,27 +367,33 @@ struct SimpleStep {
     static constexpr bool kReduceToY = KindTraits<KIND>::kReduceToY;
     static constexpr bool kCopyInToY = KindTraits<KIND>::kCopyInToY;
     static constexpr int U = AR_SIMPLE_U;
+    // With DAG a received all-gather message is already in the own output.
+    static constexpr bool kWriteOwn = kWriteOut && !(DAG && kRecvAG);
+    static constexpr int kOwnPol = DAG ? kFifoSt : kOutPol;  // own output stores
+    static constexpr int kAgLdPol = kFifoLd;                  // all-gather reads (FIFO or own output)
 
     // Partial last unit of the buffer: element-wise data accesses.
-    __device__ static u32x4 load_in_partial(Rsrc r, uint32_t off, uint32_t valid)
+    template <int POL>
+    __device__ static u32x4 load_partial(Rsrc r, uint32_t off, uint32_t valid)
     {
         u32x4 v = {0, 0, 0, 0};
         if (E == 4) {
-            for (uint32_t i = 0; i < valid; ++i) v[i] = ld32<kInPol>(r, off + 4 * i);
+            for (uint32_t i = 0; i < valid; ++i) v[i] = ld32<POL>(r, off + 4 * i);
         } else {
             for (uint32_t i = 0; i < valid; ++i) {
-                uint32_t h = ld16<kInPol>(r, off + 2 * i);
+                uint32_t h = ld16<POL>(r, off + 2 * i);
                 v[i >> 1] |= (i & 1) ? (h << 16) : h;
             }
         }
         return v;
     }
-    __device__ static void store_out_partial(Rsrc r, uint32_t off, u32x4 v, uint32_t valid)
+    template <int POL>
+    __device__ static void store_partial(Rsrc r, uint32_t off, u32x4 v, uint32_t valid)
     {
         if (E == 4) {
-            for (uint32_t i = 0; i < valid; ++i) st32<kOutPol>(r, off + 4 * i, v[i]);
+            for (uint32_t i = 0; i < valid; ++i) st32<POL>(r, off + 4 * i, v[i]);
         } else {
-            for (uint32_t i = 0; i < valid; ++i) st16<kOutPol>(r, off + 2 * i, (i & 1) ? (v[i >> 1] >> 16) : (v[i >> 1] & 0xFFFFu));
+            for (uint32_t i = 0; i < valid; ++i) st16<POL>(r, off + 2 * i, (i & 1) ? (v[i >> 1] >> 16) : (v[i >> 1] & 0xFFFFu));
         }
     }
 
@@ -424,24 +439,31 @@ struct SimpleStep {
         } else {
             y = ag;
         }
-        if (kWriteOut) {
-            if (valid == A) st128<kOutPol>(rout, u * 16, y);
-            else store_out_partial(rout, u * 16, y, valid);
+        if (kWriteOwn) {
+            if (valid == A) st128<kOwnPol>(rout, u * 16, y);
+            else store_partial<kOwnPol>(rout, u * 16, y, valid);
         }
-        if (kSendAG) st128<kFifoSt>(wo, u * 16, y);
+        if (kSendAG) {
+            // A FIFO slot is padded to whole units; the next rank's output is not.
+            if (valid == A || !DAG) st128<kFifoSt>(wo, u * 16, y);
+            else store_partial<kFifoSt>(wo, u * 16, y, valid);
+        }
         (void)wi;
     }
 
+    // rslot / wslot: FIFO slots, or with DAG for all-gather messages the own
+    // and the next rank's output at this message's elements.
     __device__ static void run(const RingArgs &a, const char *src, char *dst, const char *rslot,
                                char *wslot, uint32_t len)
     {
+        if (DAG && KIND == kRecvCopy) return;  // the data is already in place
         const uint32_t lane = step_lane();
         const uint32_t nfull = len / A, rem = len % A;
         const uint32_t nunits = nfull + (rem ? 1u : 0u);
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
-        const Rsrc wi = make_rsrc(rslot, a.slot_bytes);
-        const Rsrc wo = make_rsrc(wslot, a.slot_bytes);
+        const Rsrc wi = make_rsrc(rslot, DAG && kRecvAG ? (uint64_t)len * E : a.slot_bytes);
+        const Rsrc wo = make_rsrc(wslot, DAG && kSendAG ? (uint64_t)len * E : a.slot_bytes);
         for (uint32_t base = 0; base < nfull; base += 64 * U) {
             u32x4 in[U], rs[U][RSV], ag[U];
 #pragma unroll
@@ -451,7 +473,7 @@ struct SimpleStep {
                     if (kLoadIn) in[t] = ld128<kInPol>(rin, u * 16);
                     if (kRecvRS)
                         for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoLd>(wi, wide_off(u, v, RSV, nunits));
-                    if (kRecvAG) ag[t] = ld128<kFifoLd>(wi, u * 16);
+                    if (kRecvAG) ag[t] = ld128<kAgLdPol>(wi, u * 16);
                 }
             }
 #pragma unroll
@@ -463,32 +485,37 @@ struct SimpleStep {
         if (rem && lane == (nfull & 63u)) {
             const uint32_t u = nfull;
             u32x4 in = {0, 0, 0, 0}, rs[RSV], ag = {0, 0, 0, 0};
-            if (kLoadIn) in = load_in_partial(rin, u * 16, rem);
+            if (kLoadIn) in = load_partial<kInPol>(rin, u * 16, rem);
             if (kRecvRS)
                 for (uint32_t v = 0; v < RSV; ++v) rs[v] = ld128<kFifoLd>(wi, wide_off(u, v, RSV, nunits));
-            if (kRecvAG) ag = ld128<kFifoLd>(wi, u * 16);
+            if (kRecvAG) ag = DAG ? load_partial<kAgLdPol>(wi, u * 16, rem) : ld128<kAgLdPol>(wi, u * 16);
             unit(rin, rout, wi, wo, u, rem, nunits, in, rs, ag);
         }
     }
 };
 
-template <int DT, int KIND>
-__device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst, uint32_t len)
+// dst: this step's elements in the own output; peer_dst: the same elements
+// in the next rank's output (used by DAG all-gather sends only).
+template <int DT, int KIND, bool DAG>
+__device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst, char *peer_dst, uint32_t len)
 {
     const RingArgs &a = *g.a;
     constexpr bool recv = KindTraits<KIND>::kRecvRS || KindTraits<KIND>::kRecvAG;
     constexpr bool send = KindTraits<KIND>::kSendRS || KindTraits<KIND>::kSendAG;
+    // With DAG only reduce-scatter messages occupy FIFO slots.
+    constexpr bool fifo_in = KindTraits<KIND>::kRecvRS || (KindTraits<KIND>::kRecvAG && !DAG);
+    constexpr bool fifo_out = KindTraits<KIND>::kSendRS || (KindTraits<KIND>::kSendAG && !DAG);
     const char *rslot = nullptr;
     char *wslot = nullptr;
     if (recv) {
         if (!wait_geq(a, g.tail_in, g.m_in + 1, g.tail_seen)) return false;
-        rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.slot_in, a);
+        rslot = fifo_in ? slot_ptr(const_cast<char *>(g.fifo_in), g.slot_in, a) : dst;
     }
     if (send) {
-        if (!acquire_send_slot(g)) return false;
-        wslot = slot_ptr(g.fifo_out, g.slot_out, a);
+        if (fifo_out && !acquire_send_slot(g)) return false;
+        wslot = fifo_out ? slot_ptr(g.fifo_out, g.slot_out, a) : peer_dst;
     }
-    SimpleStep<DT, KIND>::run(a, src, dst, rslot, wslot, len);
+    SimpleStep<DT, KIND, DAG>::run(a, src, dst, rslot, wslot, len);
     // Slot writes (and slot reads) complete before either counter moves.
     drain_vmem();
     if (send) {
@@ -972,16 +999,17 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
 
 // ===================================================================== kernel
 
-template <int PROTO, int DT, int KIND>
-__device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, uint32_t len, uint32_t *lds)
+template <int PROTO, int DT, bool DAG, int KIND>
+__device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, char *peer_dst, uint32_t len,
+                                        uint32_t *lds)
 {
-    if (PROTO == AR_PROTO_SIMPLE) return simple_step<DT, KIND>(g, src, dst, len);
+    if (PROTO == AR_PROTO_SIMPLE) return simple_step<DT, KIND, DAG>(g, src, dst, peer_dst, len);
     if (PROTO == AR_PROTO_LL) return ll_step<DT, KIND>(g, src, dst, len);
     return ll128_step<DT, KIND>(g, src, dst, len, lds);
 }
 
 // All steps of one run for one wave; false if the wave had to give up.
-template <int PROTO, int DT>
+template <int PROTO, int DT, bool DAG>
 __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
 {
     constexpr uint32_t E = Elem<DT>::E;
@@ -994,6 +1022,7 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
     //   AllGather      k = 0 .. N-1,  segment (r - k) mod N, starting from the own block
     const char *src = a.src[r];
     char *dst = a.dst[r];
+    char *peer = DAG ? a.dst[r + 1 == N ? 0 : r + 1] : nullptr;  // the next rank's output
     const uint32_t coll = a.coll;
     const uint32_t nsteps = coll == AR_COLL_ALLREDUCE ? 2 * N - 1 : N;
     const uint32_t s0 = coll == AR_COLL_REDUCESCATTER ? (r + N - 1) % N : r;
@@ -1014,21 +1043,22 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
             const uint64_t out_e = hi > lo ? (coll == AR_COLL_REDUCESCATTER ? lo - seg_lo : lo) : 0;
             const char *s_ptr = src + in_e * E;
             char *d_ptr = dst + out_e * E;
+            char *p_ptr = DAG ? peer + out_e * E : nullptr;
             bool ok;
             if (coll == AR_COLL_ALLREDUCE) {
-                if (k == 0) ok = do_step<PROTO, DT, kSend>(g, s_ptr, d_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, kRecvReduceSend>(g, s_ptr, d_ptr, len, lds);
-                else if (k == N - 1) ok = do_step<PROTO, DT, kRecvReduceCopySend>(g, s_ptr, d_ptr, len, lds);
-                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, kRecvCopySend>(g, s_ptr, d_ptr, len, lds);
-                else ok = do_step<PROTO, DT, kRecvCopy>(g, s_ptr, d_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, kSend>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                else if (k == N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceCopySend>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, DAG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, len, lds);
             } else if (coll == AR_COLL_REDUCESCATTER) {
-                if (k == 0) ok = do_step<PROTO, DT, kSend>(g, s_ptr, d_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, kRecvReduceSend>(g, s_ptr, d_ptr, len, lds);
-                else ok = do_step<PROTO, DT, kRecvReduceCopy>(g, s_ptr, d_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, kSend>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, kRecvReduceCopy>(g, s_ptr, d_ptr, p_ptr, len, lds);
             } else {
-                if (k == 0) ok = do_step<PROTO, DT, kCopySend>(g, s_ptr, d_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, kRecvCopySend>(g, s_ptr, d_ptr, len, lds);
-                else ok = do_step<PROTO, DT, kRecvCopy>(g, s_ptr, d_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, kCopySend>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, len, lds);
             }
             if (!ok) return false;
         }
@@ -1036,7 +1066,7 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
     return true;
 }
 
-template <int PROTO, int DT>
+template <int PROTO, int DT, bool DAG>
 __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
 {
     __shared__ uint32_t lds_all[(PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? AR_MAX_WAVES * kLdsWordsPerWave : 1];
@@ -1094,7 +1124,7 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
     if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED,
                                                          __HIP_MEMORY_SCOPE_AGENT)) != 0)
         return;
-    ring_steps<PROTO, DT>(g, lds);
+    ring_steps<PROTO, DT, DAG>(g, lds);
 }
 
 // ===================================================================== direct
@@ -1279,16 +1309,18 @@ __global__ void bf16_round_kernel(const float *in, uint16_t *out, size_t n)
 
 typedef void (*RingFn)(RingArgs);
 
-__host__ RingFn ring_fn(int proto, int dtype)
+// dag: the Simple ring's direct all-gather (the other protocols always
+// carry the all-gather through their FIFOs).
+__host__ RingFn ring_fn(int proto, int dtype, bool dag)
 {
     if (dtype == AR_FLOAT32) {
-        if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, AR_FLOAT32>;
-        if (proto == AR_PROTO_LL128) return ring_kernel<AR_PROTO_LL128, AR_FLOAT32>;
-        return ring_kernel<AR_PROTO_SIMPLE, AR_FLOAT32>;
+        if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, AR_FLOAT32, false>;
+        if (proto == AR_PROTO_LL128) return ring_kernel<AR_PROTO_LL128, AR_FLOAT32, false>;
+        return dag ? ring_kernel<AR_PROTO_SIMPLE, AR_FLOAT32, true> : ring_kernel<AR_PROTO_SIMPLE, AR_FLOAT32, false>;
     }
-    if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, AR_BFLOAT16>;
-    if (proto == AR_PROTO_LL128) return ring_kernel<AR_PROTO_LL128, AR_BFLOAT16>;
-    return ring_kernel<AR_PROTO_SIMPLE, AR_BFLOAT16>;
+    if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, AR_BFLOAT16, false>;
+    if (proto == AR_PROTO_LL128) return ring_kernel<AR_PROTO_LL128, AR_BFLOAT16, false>;
+    return dag ? ring_kernel<AR_PROTO_SIMPLE, AR_BFLOAT16, true> : ring_kernel<AR_PROTO_SIMPLE, AR_BFLOAT16, false>;
 }
 
 __host__ RingFn direct_fn(int dtype, int nranks)
@@ -1306,7 +1338,7 @@ __host__ RingFn direct_fn(int dtype, int nranks)
 int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
 {
     dev::RingFn fn = info.algo == AR_ALGO_DIRECT ? dev::direct_fn(info.dtype, info.nranks)
-                                                 : dev::ring_fn(info.proto, info.dtype);
+                                                 : dev::ring_fn(info.proto, info.dtype, info.ag_direct != 0);
     RingArgs a = args;
     void *kargs[] = {&a};
     hipError_t e = hipLaunchKernel((const void *)fn, dim3((unsigned)info.grid), dim3((unsigned)info.block), kargs,
@@ -1314,13 +1346,18 @@ int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
     return e == hipSuccess ? AR_OK : AR_ERR_HIP;
 }
 
+// The smaller co-residency of the protocol's kernel variants.
 int ring_occupancy(int proto, int dtype, int block, int *blocks_per_cu)
 {
-    dev::RingFn fn = dev::ring_fn(proto, dtype);
-    int n = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, (const void *)fn, block, 0);
-    if (e != hipSuccess) return AR_ERR_HIP;
-    *blocks_per_cu = n;
+    int best = 1 << 30;
+    for (int dag = 0; dag < 2; ++dag) {
+        dev::RingFn fn = dev::ring_fn(proto, dtype, dag != 0);
+        int n = 0;
+        hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, (const void *)fn, block, 0);
+        if (e != hipSuccess) return AR_ERR_HIP;
+        if (n < best) best = n;
+    }
+    *blocks_per_cu = best;
     return AR_OK;
 }
 

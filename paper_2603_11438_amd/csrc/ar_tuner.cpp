@@ -244,7 +244,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     if (d->nwaves < 0 || d->nwaves > AR_MAX_WAVES) return AR_ERR_ARG;
     if (d->placement != AR_PLACE_RANK_SPREAD && d->placement != AR_PLACE_CHANNEL_LOCAL) return AR_ERR_ARG;
     if (d->chunk_bytes > kMaxChunkBytes) return AR_ERR_ARG;
-    if (d->flags & ~(uint32_t)AR_PLAN_PROFILE) return AR_ERR_ARG;
+    if (d->flags & ~(uint32_t)(AR_PLAN_PROFILE | AR_PLAN_FIFO_ALLGATHER)) return AR_ERR_ARG;
     if (!valid_algo(d->algo)) return AR_ERR_ARG;
     if (d->coll != AR_COLL_ALLREDUCE && d->coll != AR_COLL_REDUCESCATTER && d->coll != AR_COLL_ALLGATHER)
         return AR_ERR_ARG;
@@ -309,6 +309,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     g.placement = d->placement;
     g.count = d->count;
     g.block = 64 * nw;
+    g.ag_direct = proto == AR_PROTO_SIMPLE && d->coll != AR_COLL_REDUCESCATTER && !(d->flags & AR_PLAN_FIFO_ALLGATHER);
 
     const uint64_t N = (uint64_t)d->nranks;
     g.seg_elems = d->coll == AR_COLL_ALLREDUCE ? round_up(ceil_div(d->count, N), A) : d->count;

@@ -50,7 +50,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_version_and_strerror():
-    assert ar.ar_version() == 2
+    assert ar.ar_version() == 3
     for code in range(8):
         assert ar.ar_strerror(code)
     assert ar.ar_strerror(99) == "unknown error"
@@ -259,6 +259,26 @@ def test_ring_byte_counts():
     assert abs(ar.ring_bytes(S, 8, "f32", "ll128") - (16 + 28 * 128 / 120) * S) < 1
     assert ar.ring_bytes(S, 8, "bf16", "simple") == 58 * S
     assert ar.compulsory_bytes(S, 8) == 16 * S
+    # Simple with the direct all-gather: 8 ranks fp32 36 S, bf16 50 S; with
+    # 2 ranks only the chain start and the owner move data (fp32 6 S).
+    assert ar.ring_bytes(S, 8, "f32", "simple", ag_direct=True) == 36 * S
+    assert ar.ring_bytes(S, 8, "bf16", "simple", ag_direct=True) == 50 * S
+    assert ar.ring_bytes(S, 2, "f32", "simple", ag_direct=True) == 6 * S
+    assert ar.ring_bytes(S, 8, "f32", "ll", ag_direct=True) == 72 * S  # LL has no direct mode
+
+
+def test_direct_allgather_mode_in_geometry():
+    def geom(proto, coll="allreduce", flags=0):
+        return ar.ar_plan_geometry(ar.make_desc(8, 1 << 16, "f32", proto, 4, coll=coll, flags=flags, algo="ring"))
+    assert geom("simple")["ag_direct"] == 1
+    assert geom("simple", "allgather")["ag_direct"] == 1
+    assert geom("simple", "reducescatter")["ag_direct"] == 0
+    assert geom("simple", flags=ar.AR_PLAN_FIFO_ALLGATHER)["ag_direct"] == 0
+    assert geom("ll")["ag_direct"] == 0 and geom("ll128")["ag_direct"] == 0
+    # the same link bytes either way
+    assert geom("simple")["wire_bytes_per_run"] == geom("simple", flags=ar.AR_PLAN_FIFO_ALLGATHER)["wire_bytes_per_run"]
+    d = ar.make_desc(8, 1 << 16, "f32", "simple", 4, flags=8)
+    assert ar.lib().ar_plan_geometry(ctypes.byref(d), ctypes.byref(ar.ar_plan_info())) == ar.AR_ERR_ARG
 
 
 # ------------------------------------------------------------- algorithms

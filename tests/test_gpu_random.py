@@ -34,6 +34,7 @@ def _case(rng):
         cfg["chunk_bytes"] = int(rng.choice([16, 256, 1024, 4096, 65536]))
         cfg["fifo_depth"] = int(rng.choice([2, 3, 4, 8]))
         cfg["placement"] = int(rng.integers(0, 2))
+        cfg["flags"] = int(rng.choice([0, 2]))  # 2: all-gather through the FIFOs
     else:
         cfg["nchannels"] = int(rng.choice([0, 1, 3, 16]))
         cfg["nwaves"] = int(rng.choice([0, 1, 4, 16]))
