@@ -139,6 +139,8 @@ typedef struct ar_plan_desc {
     uint32_t flags;        /* AR_PLAN_* */
     int algo;              /* AR_ALGO_* */
     int coll;              /* AR_COLL_* (0 = AllReduce) */
+    int direct_unroll;     /* direct algorithm: 1 or 2 units per thread and
+                              iteration; 0 asks the tuner / default */
 } ar_plan_desc;
 
 /* Plan flags.
@@ -182,6 +184,7 @@ typedef struct ar_plan_info {
     int coll;              /* AR_COLL_* */
     int ag_direct;         /* 1: the Simple ring's all-gather writes into the
                               next rank's output (see AR_PLAN_FIFO_ALLGATHER) */
+    int direct_unroll;     /* direct algorithm: units per thread and iteration */
 } ar_plan_info;
 
 /* ---- plans -------------------------------------------------------------- */
@@ -280,6 +283,9 @@ typedef struct ar_tune_out {
     int direct_parts;      /* direct algorithm: workgroups per segment
                               (0 = sized to the message) */
     int direct_nwaves;     /* direct algorithm: waves per workgroup (0 = 4) */
+    int direct_unroll;     /* direct algorithm: 16-byte units per thread and
+                              iteration, 1 or 2 (0 = by size: 2 up to 8 MiB
+                              per rank, 1 above) */
 } ar_tune_out;
 
 /* A tuner: fill *out from *ctx; return 0 on success.  A non-zero return, or

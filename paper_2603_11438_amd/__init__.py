@@ -45,7 +45,7 @@ class ar_plan_desc(ctypes.Structure):
                 ("fifo_depth", ctypes.c_int), ("nwaves", ctypes.c_int), ("placement", ctypes.c_int),
                 ("timeout_us", ctypes.c_uint32), ("debug_flags", ctypes.c_uint32),
                 ("max_channels", ctypes.c_int), ("comm_id", ctypes.c_uint64), ("flags", ctypes.c_uint32),
-                ("algo", ctypes.c_int), ("coll", ctypes.c_int)]
+                ("algo", ctypes.c_int), ("coll", ctypes.c_int), ("direct_unroll", ctypes.c_int)]
 
 
 class ar_plan_info(ctypes.Structure):
@@ -56,7 +56,7 @@ class ar_plan_info(ctypes.Structure):
                 ("chunk_elems", ctypes.c_size_t), ("wave_elems", ctypes.c_size_t), ("nchunks", ctypes.c_size_t),
                 ("slot_bytes", ctypes.c_size_t), ("fifo_bytes", ctypes.c_size_t), ("flag_bytes", ctypes.c_size_t),
                 ("msgs_per_run", ctypes.c_uint64), ("wire_bytes_per_run", ctypes.c_uint64), ("algo", ctypes.c_int),
-                ("coll", ctypes.c_int), ("ag_direct", ctypes.c_int)]
+                ("coll", ctypes.c_int), ("ag_direct", ctypes.c_int), ("direct_unroll", ctypes.c_int)]
 
     def as_dict(self) -> dict:
         d = {name: getattr(self, name) for name, _ in self._fields_}
@@ -74,7 +74,7 @@ class ar_tune_ctx(ctypes.Structure):
 class ar_tune_out(ctypes.Structure):
     _fields_ = [("proto", ctypes.c_int), ("nchannels", ctypes.c_int), ("chunk_bytes", ctypes.c_size_t),
                 ("nwaves", ctypes.c_int), ("algo", ctypes.c_int), ("direct_parts", ctypes.c_int),
-                ("direct_nwaves", ctypes.c_int)]
+                ("direct_nwaves", ctypes.c_int), ("direct_unroll", ctypes.c_int)]
 
 
 class ar_latency_state(ctypes.Structure):
@@ -173,7 +173,7 @@ def _check(rc: int, what: str):
 def make_desc(nranks: int, count: int, dtype="f32", proto="auto", nchannels: int = 0, chunk_bytes: int = 0,
               fifo_depth: int = 0, nwaves: int = 0, placement: int = 0, timeout_us: int = 0,
               debug_flags: int = 0, max_channels: int = 0, comm_id: int = 0, flags: int = 0,
-              algo="auto", coll="allreduce") -> ar_plan_desc:
+              algo="auto", coll="allreduce", direct_unroll: int = 0) -> ar_plan_desc:
     d = ar_plan_desc()
     d.nranks = nranks
     d.dtype = DTYPES[dtype] if isinstance(dtype, str) else dtype
@@ -191,6 +191,7 @@ def make_desc(nranks: int, count: int, dtype="f32", proto="auto", nchannels: int
     d.flags = flags
     d.algo = ALGOS[algo] if isinstance(algo, str) else algo
     d.coll = COLLS[coll] if isinstance(coll, str) else coll
+    d.direct_unroll = direct_unroll
     return d
 
 
@@ -210,7 +211,7 @@ def ar_tune(msg_bytes: int, nranks: int = 8, dtype="f32", max_channels: int = AR
     return {"proto": out.proto, "proto_name": PROTO_NAMES[out.proto], "nchannels": out.nchannels,
             "chunk_bytes": out.chunk_bytes, "nwaves": out.nwaves, "algo": out.algo,
             "algo_name": ALGO_NAMES[out.algo], "direct_parts": out.direct_parts,
-            "direct_nwaves": out.direct_nwaves}
+            "direct_nwaves": out.direct_nwaves, "direct_unroll": out.direct_unroll}
 
 
 _tuner_refs = []  # keep ctypes callbacks alive while installed
@@ -245,6 +246,7 @@ def _tuner_callback(fn):
             o.algo = int(res.get("algo", AR_ALGO_AUTO))
             o.direct_parts = int(res.get("direct_parts", 0))
             o.direct_nwaves = int(res.get("direct_nwaves", 0))
+            o.direct_unroll = int(res.get("direct_unroll", 0))
             return int(res.get("rc", 0))
 
         cb = ar_tuner_fn(_trampoline)
@@ -328,9 +330,9 @@ class Plan:
     def __init__(self, nranks: int, count: int, dtype="f32", proto="auto", nchannels: int = 0,
                  chunk_bytes: int = 0, fifo_depth: int = 0, nwaves: int = 0, placement: int = 0,
                  timeout_us: int = 0, debug_flags: int = 0, comm_id: int = 0, flags: int = 0, algo="auto",
-                 coll="allreduce"):
+                 coll="allreduce", direct_unroll: int = 0):
         self.desc = make_desc(nranks, count, dtype, proto, nchannels, chunk_bytes, fifo_depth, nwaves,
-                              placement, timeout_us, debug_flags, 0, comm_id, flags, algo, coll)
+                              placement, timeout_us, debug_flags, 0, comm_id, flags, algo, coll, direct_unroll)
         L = lib()
         h = L.ar_plan_ex(ctypes.byref(self.desc))
         if not h:

@@ -134,6 +134,7 @@ int ar_tuner_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->algo = AR_ALGO_RING;
     out->direct_parts = 0;
     out->direct_nwaves = 0;
+    out->direct_unroll = 0;
     Entry *e = find(ctx->comm_id, false);
     if (!e || e->samples.load(std::memory_order_acquire) == 0) {
         out->nchannels = cfg.min_channels;
@@ -190,6 +191,7 @@ int ar_tuner_size_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->nwaves = 0;
     out->direct_parts = 0;
     out->direct_nwaves = 0;
+    out->direct_unroll = 0;
     out->algo = ctx->msg_bytes <= 32u * 1024u ? AR_ALGO_DIRECT : AR_ALGO_RING;
     Entry *e = find(ctx->comm_id, false);
     if (!e || e->samples.load(std::memory_order_acquire) == 0) {

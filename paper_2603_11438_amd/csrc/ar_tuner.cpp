@@ -33,6 +33,7 @@ struct TableRow {
     int algo;          // ... and the algorithm to run (AUTO = the ring)
     int direct_parts;  // direct algorithm's workgroups per segment (0 = auto)
     int direct_nwaves; // direct algorithm's waves per workgroup (0 = default)
+    int direct_unroll; // direct algorithm's units per thread and iteration (0 = by size)
 };
 
 #include "tuner_table.inc"
@@ -94,6 +95,7 @@ bool out_valid(int rc, const ar_tune_out &o)
     if (o.proto != AR_PROTO_AUTO && !valid_proto(o.proto)) return false;
     if (o.nchannels < 0 || o.nwaves < 0 || o.nwaves > AR_MAX_WAVES) return false;
     if (o.direct_parts < 0 || o.direct_nwaves < 0 || o.direct_nwaves > AR_MAX_WAVES) return false;
+    if (o.direct_unroll < 0 || o.direct_unroll > 2) return false;
     return o.chunk_bytes <= kMaxChunkBytes;
 }
 
@@ -181,7 +183,10 @@ int default_depth(int proto) { return proto == AR_PROTO_SIMPLE ? 2 : 4; }
 
 // Direct algorithm: units (16 bytes of data) per thread per iteration, and
 // the largest grid it is sized to (8 workgroups per CU on 256 CUs).
-constexpr uint64_t kDirectUnroll = 2;
+// Direct algorithm: two units per thread and iteration up to this many bytes
+// per rank, one above (measured on MI355X: two keep more loads in flight
+// while the data is cache-resident, one streams faster from HBM).
+constexpr uint64_t kDirectUnrollBytes = 8ull << 20;
 constexpr uint64_t kDirectMaxGrid = 2048;
 
 size_t default_chunk_bytes(int proto)
@@ -201,8 +206,13 @@ int resolve_direct(const ar_plan_desc *d, const ar_tune_out *t, ar_plan_info *ou
     const uint64_t A = 16 / e;
     const uint64_t N = (uint64_t)d->nranks;
     int nw = d->nwaves ? d->nwaves : (t && t->direct_nwaves ? t->direct_nwaves : 4);
+    const uint64_t full_bytes = d->count * e * (d->coll == AR_COLL_ALLREDUCE ? 1 : N);
+    int unroll = d->direct_unroll ? d->direct_unroll : (t && t->direct_unroll ? t->direct_unroll : 0);
+    if (unroll == 0) unroll = full_bytes <= kDirectUnrollBytes ? 2 : 1;
+    if (d->nranks > 8) unroll = 1;  // the 9..16-rank kernel keeps one unit per thread
     ar_plan_info g = {};
     g.algo = AR_ALGO_DIRECT;
+    g.direct_unroll = unroll;
     g.coll = d->coll;
     g.proto = AR_PROTO_AUTO;
     g.nranks = d->nranks;
@@ -220,7 +230,7 @@ int resolve_direct(const ar_plan_desc *d, const ar_tune_out *t, ar_plan_info *ou
     const uint64_t seg_units = ceil_div(g.seg_elems, A);
     uint64_t parts = (uint64_t)(d->nchannels ? d->nchannels : (t ? t->direct_parts : 0));
     if (parts == 0) {
-        parts = ceil_div(seg_units, 64 * (uint64_t)nw * kDirectUnroll);
+        parts = ceil_div(seg_units, 64 * (uint64_t)nw * (uint64_t)unroll);
         uint64_t cap = kDirectMaxGrid / N;
         if (cap < 1) cap = 1;
         if (parts > cap) parts = cap;
@@ -242,6 +252,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     if (d->nchannels < 0 || d->nchannels > AR_MAX_CHANNELS) return AR_ERR_ARG;
     if (d->fifo_depth != 0 && (d->fifo_depth < 2 || d->fifo_depth > 16)) return AR_ERR_ARG;
     if (d->nwaves < 0 || d->nwaves > AR_MAX_WAVES) return AR_ERR_ARG;
+    if (d->direct_unroll < 0 || d->direct_unroll > 2) return AR_ERR_ARG;
     if (d->placement != AR_PLACE_RANK_SPREAD && d->placement != AR_PLACE_CHANNEL_LOCAL) return AR_ERR_ARG;
     if (d->chunk_bytes > kMaxChunkBytes) return AR_ERR_ARG;
     if (d->flags & ~(uint32_t)(AR_PLAN_PROFILE | AR_PLAN_FIFO_ALLGATHER)) return AR_ERR_ARG;
@@ -386,6 +397,7 @@ int ar_tuner_fixed_default(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->algo = AR_ALGO_RING;
     out->direct_parts = 0;
     out->direct_nwaves = 0;
+    out->direct_unroll = 0;
     return 0;
 }
 
@@ -401,6 +413,7 @@ int ar_tuner_noop(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->algo = AR_ALGO_AUTO;
     out->direct_parts = 0;
     out->direct_nwaves = 0;
+    out->direct_unroll = 0;
     return 0;
 }
 
@@ -430,6 +443,7 @@ int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->algo = row->algo;
     out->direct_parts = row->direct_parts;
     out->direct_nwaves = row->direct_nwaves;
+    out->direct_unroll = row->direct_unroll;
     return 0;
 }
 
@@ -458,7 +472,7 @@ int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out)
         t.nchannels = t.nchannels > 0 ? t.nchannels : kDefaultChannels;
     }
     bool fallback = rc != 0 || !valid_proto(t.proto) || !valid_algo(t.algo) || t.nchannels < 0 || t.nwaves < 0 ||
-                    t.direct_parts < 0 || t.direct_nwaves < 0;
+                    t.direct_parts < 0 || t.direct_nwaves < 0 || t.direct_unroll < 0 || t.direct_unroll > 2;
     if (fallback) {
         t.proto = kDefaultProto;
         t.nchannels = kDefaultChannels;
@@ -467,6 +481,7 @@ int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out)
         t.algo = AR_ALGO_RING;
         t.direct_parts = 0;
         t.direct_nwaves = 0;
+        t.direct_unroll = 0;
     }
     if (t.direct_nwaves > AR_MAX_WAVES) t.direct_nwaves = AR_MAX_WAVES;
     if (t.algo == AR_ALGO_AUTO) t.algo = AR_ALGO_RING;

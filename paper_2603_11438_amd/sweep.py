@@ -64,15 +64,17 @@ def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3):
     return out
 
 
-DIRECT_PARTS = (0, 16, 64, 256)
-DIRECT_WAVES = (2, 4, 8, 16)
+DIRECT_PARTS = (0, 16, 32, 64, 96, 128, 256)
+DIRECT_WAVES = (1, 2, 4, 8, 16)
+DIRECT_UNROLL = (1, 2)
 
 
 def grid(size, protos=("ll", "ll128", "simple"), channels=(1, 2, 4, 8, 16, 32, 64), waves=(2, 4, 8),
          chunks=None):
     for parts in DIRECT_PARTS:
         for w in DIRECT_WAVES:
-            yield dict(algo="direct", nchannels=parts, nwaves=w)
+            for u in DIRECT_UNROLL:
+                yield dict(algo="direct", nchannels=parts, nwaves=w, direct_unroll=u)
     chunks = chunks or CHUNKS
     for p in protos:
         for c in channels:
@@ -202,7 +204,7 @@ def emit_one(table, coll):
              "default": "AR_PROTO_AUTO"}
     lines = [
         f"// {coll}: MI355X size -> {{algorithm; ring protocol, channels, chunk, waves;",
-        "// direct workgroups per segment, waves} table for 8-rank fp32",
+        "// direct workgroups per segment, waves, units per thread} table for 8-rank fp32",
         "// collectives, one row per power-of-two size of each rank's full buffer from",
         "// 4 KiB to 128 MiB.  A message of S bytes uses the row of the smallest size",
         "// >= S (sizes below 4 KiB use the first row, above 128 MiB the last).",
@@ -217,18 +219,18 @@ def emit_one(table, coll):
         "// choice (direct on a tie, as it moves fewer bytes).",
         "//",
         "// columns: log2(size), ring proto, nchannels, chunk_bytes, nwaves, algorithm,",
-        "//          direct parts, direct waves   [busBW GB/s: ring / direct]",
+        "//          direct parts, direct waves, direct unroll   [busBW GB/s: ring / direct]",
         f"static const TableRow {TABLE_NAMES[coll]}[] = {{",
     ]
     if not table:
-        lines.append("    {27, AR_PROTO_AUTO, 0, 0, 0, AR_ALGO_AUTO, 0, 0},  // not measured: defer to the default")
+        lines.append("    {27, AR_PROTO_AUTO, 0, 0, 0, AR_ALGO_AUTO, 0, 0, 0},  // not measured: defer to the default")
     for size, row in sorted(table.items()):
         lg = size.bit_length() - 1
         r, d = row["ring"], row["direct"]
         ring_cols = ("AR_PROTO_AUTO, 0, 0, 0" if r["proto"] == "default" else
                      f"{names[r['proto']]}, {r['nchannels']}, {r['chunk_bytes']}, {r['nwaves']}")
         algo = "AR_ALGO_DIRECT" if row["algo"] == "direct" else "AR_ALGO_RING"
-        dcols = f"{d['nchannels']}, {d['nwaves']}" if d else "0, 0"
+        dcols = f"{d['nchannels']}, {d['nwaves']}, {d.get('direct_unroll', 0)}" if d else "0, 0, 0"
         dbw = f"{d['busbw']:.1f}" if d else "-"
         lines.append(f"    {{{lg}, {ring_cols}, {algo}, {dcols}}},  // {r['busbw']:.1f} / {dbw}")
     lines.append("};")
@@ -254,7 +256,8 @@ def table_cmd(args):
 def print_table(table):
     for size, row in sorted(table.items()):
         r, d = row["ring"], row["direct"]
-        ds = f"direct P={d['nchannels']:3} W={d['nwaves']:2} busBW={d['busbw']:7.1f}" if d else "direct -"
+        ds = (f"direct P={d['nchannels']:3} W={d['nwaves']:2} U={d.get('direct_unroll', 0)} busBW={d['busbw']:7.1f}"
+              if d else "direct -")
         print(f"{size:>10} {row['algo']:6} | ring {r['proto']:7} C={r['nchannels']:3} chunk={r['chunk_bytes']:8} "
               f"W={r['nwaves']} busBW={r['busbw']:6.1f} | {ds}")
 

@@ -147,7 +147,7 @@ def test_tuner_sees_context():
                     "max_channels": 40, "comm_id": 77}
     assert d == {"proto": ar.AR_PROTO_LL128, "proto_name": "ll128", "nchannels": 3,
                  "chunk_bytes": 992, "nwaves": ar.AR_MAX_WAVES, "algo": ar.AR_ALGO_RING, "algo_name": "ring",
-                 "direct_parts": 0, "direct_nwaves": 0}
+                 "direct_parts": 0, "direct_nwaves": 0, "direct_unroll": 0}
 
 
 def test_tune_rejects_bad_context():
@@ -265,6 +265,31 @@ def test_ring_byte_counts():
     assert ar.ring_bytes(S, 8, "bf16", "simple", ag_direct=True) == 50 * S
     assert ar.ring_bytes(S, 2, "f32", "simple", ag_direct=True) == 6 * S
     assert ar.ring_bytes(S, 8, "f32", "ll", ag_direct=True) == 72 * S  # LL has no direct mode
+
+
+def test_direct_unroll_resolution():
+    def geom(count, **kw):
+        return ar.ar_plan_geometry(ar.make_desc(8, count, "f32", algo="direct", **kw))
+    # by size: two units per thread up to 8 MiB per rank, one above
+    assert geom((8 << 20) // 4)["direct_unroll"] == 2
+    assert geom((8 << 20) // 4 + 4)["direct_unroll"] == 1
+    assert geom(1 << 20, direct_unroll=1)["direct_unroll"] == 1
+    assert geom(1 << 28, direct_unroll=2)["direct_unroll"] == 2
+    # more than 8 ranks: one unit
+    g = ar.ar_plan_geometry(ar.make_desc(9, 1 << 10, "f32", algo="direct", direct_unroll=2))
+    assert g["direct_unroll"] == 1
+    d = ar.make_desc(8, 1 << 10, "f32", algo="direct", direct_unroll=3)
+    assert ar.lib().ar_plan_geometry(ctypes.byref(d), ctypes.byref(ar.ar_plan_info())) == ar.AR_ERR_ARG
+    # a tuner's choice is used, and an out-of-range one falls back
+    ar.ar_set_tuner(lambda ctx: {"proto": ar.AR_PROTO_SIMPLE, "nchannels": 4, "algo": ar.AR_ALGO_DIRECT,
+                                 "direct_unroll": 1})
+    try:
+        assert geom(1 << 10)["direct_unroll"] == 1
+        ar.ar_set_tuner(lambda ctx: {"proto": ar.AR_PROTO_SIMPLE, "nchannels": 4, "algo": ar.AR_ALGO_DIRECT,
+                                     "direct_unroll": 5})
+        assert ar.ar_tune(1 << 10)["algo"] == ar.AR_ALGO_RING  # invalid output -> fixed default
+    finally:
+        ar.ar_set_tuner(None)
 
 
 def test_direct_allgather_mode_in_geometry():

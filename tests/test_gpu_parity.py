@@ -418,7 +418,9 @@ def test_direct_small_grid(ar, dtype, n):
     for count in SMALL_COUNTS:
         x = draw(n, count, dtype, "normal", seed=2000 + n * 31 + count)
         for parts in (0, 1, 3):
-            run_case(ar, x, dtype, f"direct-{dtype}-{n}-{count}-{parts}", algo="direct", nchannels=parts)
+            for unroll in (1, 2):
+                run_case(ar, x, dtype, f"direct-{dtype}-{n}-{count}-{parts}-u{unroll}", algo="direct",
+                         nchannels=parts, direct_unroll=unroll)
 
 
 def test_direct_order_revealing(ar):
@@ -439,7 +441,8 @@ def test_direct_equals_ring_bits(ar, dtype):
     want = oracle_bits(x, dtype)
     base = to_device(x, dtype)
     for cfg in (dict(algo="direct"), dict(algo="direct", nchannels=1, nwaves=1),
-                dict(algo="direct", nchannels=200, nwaves=16), dict(proto="simple", nchannels=7)):
+                dict(algo="direct", nchannels=200, nwaves=16), dict(proto="simple", nchannels=7),
+                dict(algo="direct", direct_unroll=1), dict(algo="direct", direct_unroll=2, nchannels=5)):
         ts = [t.clone() for t in base]
         plan = ar.Plan(n, count, dtype, **cfg)
         plan.run(ts)

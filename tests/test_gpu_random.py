@@ -38,6 +38,7 @@ def _case(rng):
     else:
         cfg["nchannels"] = int(rng.choice([0, 1, 3, 16]))
         cfg["nwaves"] = int(rng.choice([0, 1, 4, 16]))
+        cfg["direct_unroll"] = int(rng.choice([0, 1, 2]))
     return str(coll), str(dtype), n, count, cfg, bool(rng.integers(0, 2))
 
 
