@@ -12,12 +12,17 @@ on MI355X for the simulated ring.
     python -m paper_2603_11438_amd.sweep latency --out latency.jsonl
     python -m paper_2603_11438_amd.sweep configs --out configs.jsonl
 
+`measure` times each candidate as the device runs it (calls captured in a
+HIP graph and replayed), so small messages are ranked by kernel time rather
+than by the host's launch rate; `validate` times end-to-end calls launched
+from the host, as an application sees them (`--timing` switches either).
+
 Selection rule per size, for the ring's columns: the highest median bus
 bandwidth wins; candidates within 2 % of the best count as ties and are
 broken by fewer channels, then fewer wire bytes (Simple < LL128 < LL), then
 smaller chunk, then fewer waves; when the fixed default is within 2 % the
 row defers to it.  The direct algorithm's columns take its fastest
-{workgroups per segment, waves}.  The algorithm column picks the faster of
+{workgroups per segment, waves, units per thread}.  The algorithm column picks the faster of
 the two (the direct algorithm on a tie: it moves fewer bytes).
 """
 from __future__ import annotations
@@ -39,7 +44,11 @@ CHUNKS = {"ll": (4096, 16384, 65536), "ll128": (15360, 61440, 245760),
           "simple": (16384, 65536, 262144, 1048576)}
 
 
-def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3):
+def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3, graph=False):
+    """Seconds per call, `reps` samples.  Eager: k calls launched back to back
+    from the host (small messages then measure the host's launch rate).
+    Graph: k calls captured in one HIP graph and replayed, which measures the
+    device's time per call."""
     import torch
 
     for _ in range(warm):
@@ -50,6 +59,27 @@ def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3):
     torch.cuda.synchronize()
     one = max(time.perf_counter() - t0, 1e-6)
     k = max(10, min(2000, int(min_total_s / one)))
+    if graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            for _ in range(k):
+                plan.run(ts, side)
+        g.replay()
+        torch.cuda.synchronize()
+        out = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            e1.synchronize()
+            out.append(e0.elapsed_time(e1) / k / 1e3)
+        del g
+        if plan.status() != ar.AR_OK:
+            raise RuntimeError("timeout during sweep")
+        return out
     out = []
     for _ in range(reps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -119,10 +149,10 @@ def measure(args):
                     plan = ar.Plan(n, count, "f32", coll=coll, **cfg)
                 except ar.ARError as e:
                     continue
-                times = _timer(plan, ts, stream)
+                times = _timer(plan, ts, stream, graph=args.timing == "graph")
                 info = plan.info
                 med = statistics.median(times)
-                rec = {"coll": coll, "size": size, "nranks": n, "proto": info["proto_name"], "chunk_bytes": 0, **cfg,
+                rec = {"coll": coll, "timing": args.timing, "size": size, "nranks": n, "proto": info["proto_name"], "chunk_bytes": 0, **cfg,
                        "algo": info["algo_name"], "parts_eff": info["nchannels"], "chunk_eff": info["chunk_elems"] * 4,
                        "t_med_us": med * 1e6, "t_min_us": min(times) * 1e6, "t_max_us": max(times) * 1e6,
                        "busbw": bus_bw(coll, size, med, n)}
@@ -284,7 +314,7 @@ def validate(args):
                 ar.ar_set_tuner(tuner)
                 plan = ar.Plan(n, count, "f32", proto="auto", algo=algo, coll=coll)
                 ar.ar_set_tuner(None)
-                times = _timer(plan, ts, stream, reps=7)
+                times = _timer(plan, ts, stream, reps=7, graph=args.timing == "graph")
                 med = statistics.median(times)
                 res[name] = {"t_med_us": med * 1e6, "busbw": bus_bw(coll, size, med, n),
                              "cv": statistics.pstdev(times) / statistics.mean(times),
@@ -292,7 +322,7 @@ def validate(args):
                              "proto": plan.info["proto_name"], "nchannels": plan.info["nchannels"],
                              "chunk": plan.info["chunk_elems"] * 4, "nwaves": plan.info["nwaves"]}
                 plan.destroy()
-            rec = {"coll": coll, "size": size, **{f"{k}_{kk}": vv for k, v in res.items() for kk, vv in v.items()},
+            rec = {"coll": coll, "timing": args.timing, "size": size, **{f"{k}_{kk}": vv for k, v in res.items() for kk, vv in v.items()},
                    "ratio": res["tuned"]["busbw"] / res["default"]["busbw"],
                    "ratio_ring": res["tuned_ring"]["busbw"] / res["default"]["busbw"],
                    "bad_channels_loss": 1 - res["bad_channels"]["busbw"] / res["default"]["busbw"]}
@@ -511,6 +541,7 @@ def main(argv=None):
     m.add_argument("--nranks", type=int, default=8)
     m.add_argument("--algo", default="", help="measure only this algorithm (ring or direct)")
     m.add_argument("--coll", default="allreduce", choices=("allreduce", "allgather", "reducescatter"))
+    m.add_argument("--timing", default="graph", choices=("graph", "eager"))
     t = sub.add_parser("table")
     t.add_argument("jsonl", nargs="+")
     t.add_argument("--emit", default="")
@@ -519,6 +550,7 @@ def main(argv=None):
     v.add_argument("--nranks", type=int, default=8)
     v.add_argument("--sizes", default="")
     v.add_argument("--coll", default="allreduce", choices=("allreduce", "allgather", "reducescatter"))
+    v.add_argument("--timing", default="eager", choices=("graph", "eager"))
     st = sub.add_parser("stability")
     st.add_argument("--out", required=True)
     st.add_argument("--size", type=int, default=128 << 20)
