@@ -49,7 +49,7 @@ def geometry_key(info: dict) -> str:
         return f"direct parts={info['nchannels']} W={info['nwaves']}"
     return (f"ring proto={info['proto_name']} C={info['nchannels']} W={info['nwaves']} "
             f"chunk_elems={info['chunk_elems']} depth={info['fifo_depth']} "
-            f"allgather={'direct' if info['ag_direct'] else 'fifo'}")
+            f"peer={'direct' if info['peer_direct'] else 'fifo'}")
 
 
 def read_traffic(workload: str, kernel: str, geometry: str) -> dict | None:
@@ -112,7 +112,7 @@ def main(argv=None) -> int:
     ap.add_argument("--nwaves", type=int, default=0)
     ap.add_argument("--fifo-depth", type=int, default=0)
     ap.add_argument("--placement", type=int, default=0)
-    ap.add_argument("--fifo-allgather", type=int, default=0,
+    ap.add_argument("--fifo-only", type=int, default=0,
                     help="Simple ring: all-gather through the FIFOs instead of direct writes")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU-baseline budget (0 = skip)")
     ap.add_argument("--calibrate-copy", type=int, default=0,
@@ -197,7 +197,7 @@ def main(argv=None) -> int:
         algo = info["algo_name"]
         kernel = f"ring_{info['proto_name']}" if algo == "ring" else "direct"
         b_comp = ar.compulsory_bytes(s_bytes, n)
-        b_alg = (ar.ring_bytes(s_bytes, n, dtype, info["proto_name"], ag_direct=bool(info["ag_direct"]))
+        b_alg = (ar.ring_bytes(s_bytes, n, dtype, info["proto_name"], peer_direct=bool(info["peer_direct"]))
                  if algo == "ring" else b_comp)
         achieved = b_alg / t / 1e9
         traffic = read_traffic(wl.name, kernel, geometry_key(info))
@@ -215,7 +215,7 @@ def main(argv=None) -> int:
 
     plan = ar.Plan(n, count, dtype, proto=args.proto, nchannels=args.nchannels, chunk_bytes=args.chunk_bytes,
                    nwaves=args.nwaves, fifo_depth=args.fifo_depth, placement=args.placement, algo=args.algo,
-                   flags=ar.AR_PLAN_FIFO_ALLGATHER if args.fifo_allgather else 0)
+                   flags=ar.AR_PLAN_FIFO_ONLY if args.fifo_only else 0)
     info = plan.info
     ms, wall_ms = measure(plan)
     plan.destroy()
@@ -267,7 +267,7 @@ def main(argv=None) -> int:
                    "algo": info["algo_name"], "proto": info["proto_name"], "nchannels": info["nchannels"],
                    "chunk_bytes": info["chunk_elems"] * (4 if dtype == "f32" else 2),
                    "nwaves": info["nwaves"], "fifo_depth": info["fifo_depth"], "placement": info["placement"],
-                   "allgather": ("direct" if info["ag_direct"] else "fifo") if info["algo_name"] == "ring" else None,
+                   "peer_access": ("direct" if info["peer_direct"] else "fifo") if info["algo_name"] == "ring" else None,
                    "parallelism": "simulated ring, 1 GPU"},
         "algbw_gbs": round(algbw, 2),
         "wall_ms_per_step": round(wall_ms, 4),

@@ -149,15 +149,18 @@ typedef struct ar_plan_desc {
  *                    run's sample is harvested without blocking by a later
  *                    ar_run, or by ar_plan_status; a run whose predecessor's
  *                    events are still pending is not timed.
- *   AR_PLAN_FIFO_ALLGATHER  Simple ring only: carry the all-gather half
- *                    through the FIFOs.  By default the Simple ring writes
- *                    each finished chunk straight into the next rank's
- *                    output buffer and forwards it from there: no FIFO copy,
- *                    and nothing moves on the last hop.  The result bits are
- *                    the same either way.  The other protocols always use
- *                    their FIFOs, and the direct algorithm has none, so they
- *                    ignore the flag. */
-enum { AR_PLAN_PROFILE = 1u, AR_PLAN_FIFO_ALLGATHER = 2u };
+ *   AR_PLAN_FIFO_ONLY  Simple ring only: carry every hop through the FIFOs.
+ *                    By default the Simple ring accesses its neighbours'
+ *                    buffers directly where that saves a copy: the second
+ *                    rank of each reduce-scatter chain reads the chain
+ *                    start's input from that rank's buffer (one hop and its
+ *                    flag fewer), and each finished all-gather chunk is
+ *                    written straight into the next rank's output buffer and
+ *                    forwarded from there (nothing moves on the last hop).
+ *                    The result bits are the same either way.  The other
+ *                    protocols always use their FIFOs, and the direct
+ *                    algorithm has none, so they ignore the flag. */
+enum { AR_PLAN_PROFILE = 1u, AR_PLAN_FIFO_ONLY = 2u };
 
 /* Resolved plan geometry (after the tuner and defaults). */
 typedef struct ar_plan_info {
@@ -182,8 +185,9 @@ typedef struct ar_plan_info {
                               output */
     int algo;              /* AR_ALGO_RING or AR_ALGO_DIRECT */
     int coll;              /* AR_COLL_* */
-    int ag_direct;         /* 1: the Simple ring's all-gather writes into the
-                              next rank's output (see AR_PLAN_FIFO_ALLGATHER) */
+    int peer_direct;       /* 1: the Simple ring reads the chain start's input
+                              and writes all-gather chunks into the next
+                              rank's output directly (see AR_PLAN_FIFO_ONLY) */
     int direct_unroll;     /* direct algorithm: units per thread and iteration */
 } ar_plan_info;
 

@@ -26,7 +26,7 @@ AR_PLACE_RANK_SPREAD, AR_PLACE_CHANNEL_LOCAL = 0, 1
 (AR_OK, AR_ERR_ARG, AR_ERR_UNSUPPORTED, AR_ERR_NOMEM, AR_ERR_HIP, AR_ERR_OCCUPANCY,
  AR_ERR_TIMEOUT, AR_ERR_STATE) = range(8)
 AR_DEBUG_SKIP_POST, AR_DEBUG_JITTER = 1, 2
-AR_PLAN_PROFILE, AR_PLAN_FIFO_ALLGATHER = 1, 2
+AR_PLAN_PROFILE, AR_PLAN_FIFO_ONLY = 1, 2
 AR_ALGO_AUTO, AR_ALGO_RING, AR_ALGO_DIRECT = 0, 1, 2
 ALGOS = {"auto": AR_ALGO_AUTO, "ring": AR_ALGO_RING, "direct": AR_ALGO_DIRECT}
 ALGO_NAMES = {v: k for k, v in ALGOS.items()}
@@ -56,7 +56,7 @@ class ar_plan_info(ctypes.Structure):
                 ("chunk_elems", ctypes.c_size_t), ("wave_elems", ctypes.c_size_t), ("nchunks", ctypes.c_size_t),
                 ("slot_bytes", ctypes.c_size_t), ("fifo_bytes", ctypes.c_size_t), ("flag_bytes", ctypes.c_size_t),
                 ("msgs_per_run", ctypes.c_uint64), ("wire_bytes_per_run", ctypes.c_uint64), ("algo", ctypes.c_int),
-                ("coll", ctypes.c_int), ("ag_direct", ctypes.c_int), ("direct_unroll", ctypes.c_int)]
+                ("coll", ctypes.c_int), ("peer_direct", ctypes.c_int), ("direct_unroll", ctypes.c_int)]
 
     def as_dict(self) -> dict:
         d = {name: getattr(self, name) for name, _ in self._fields_}
@@ -442,7 +442,7 @@ def alg_bandwidth(msg_bytes: int, seconds: float) -> float:
     return msg_bytes / seconds / 1e9
 
 
-def ring_bytes(msg_bytes: int, nranks: int, dtype="f32", proto="simple", ag_direct: bool = False) -> float:
+def ring_bytes(msg_bytes: int, nranks: int, dtype="f32", proto="simple", peer_direct: bool = False) -> float:
     """Bytes the ring formulation moves through global memory per AllReduce.
 
     Through FIFOs: every rank reads its input and writes its output (2 N S),
@@ -450,17 +450,21 @@ def ring_bytes(msg_bytes: int, nranks: int, dtype="f32", proto="simple", ag_dire
     read once: N-1 crossings carry an fp32 partial, N-1 the finished value,
     scaled by the protocol's wire factor (LL 2, LL128 128/120, Simple 1).
 
-    With the Simple ring's direct all-gather (ag_direct), per element of a
-    segment: the chain start reads its input and writes an fp32 partial
-    (e + 4); each of the N-2 middle ranks reads a partial and its input and
-    writes a partial (8 + e); the owner reads a partial and its input and
-    writes its own and the next rank's output (4 + 3e); each of the N-2
-    forwarding ranks reads its output and writes the next rank's (2e); the
-    last rank moves nothing: (N-2)(8 + 3e) + 4e + 8 bytes in all."""
+    The peer-direct Simple ring (peer_direct), per element of a segment: the
+    second rank reads the chain start's input and its own and writes an fp32
+    partial (2e + 4); each of the N-3 further middle ranks reads a partial
+    and its input and writes a partial (8 + e); the owner reads a partial
+    and its input and writes its own and the next rank's output (4 + 3e);
+    each of the N-2 forwarding ranks reads its output and writes the next
+    rank's (2e); the last rank moves nothing.  With two ranks the owner is
+    the second rank: it reads both inputs and writes both outputs (4e)."""
     e = 4 if dtype == "f32" else 2
     count = msg_bytes // e
-    if ag_direct and proto == "simple" and nranks >= 2:
-        return float(count * ((nranks - 2) * (8 + 3 * e) + 4 * e + 8))
+    if peer_direct and proto == "simple" and nranks >= 2:
+        if nranks == 2:
+            return float(count * 4 * e)
+        per_elem = (2 * e + 4) + (nranks - 3) * (8 + e) + (4 + 3 * e) + (nranks - 2) * 2 * e
+        return float(count * per_elem)
     wf = {"simple": 1.0, "ll": 2.0, "ll128": 128.0 / 120.0}[proto]
     wire = count * (nranks - 1) * (4 + e) * wf
     return 2.0 * nranks * msg_bytes + 2.0 * wire

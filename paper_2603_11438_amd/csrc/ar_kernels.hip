@@ -82,7 +82,12 @@ enum Kind : int {
     kRecvCopySend,        // wire -> output and wire
     kRecvCopy,            // wire -> output
     kRecvReduceCopy,      // wire + own input -> output (ReduceScatter owner)
-    kCopySend             // own input -> output and wire (AllGather start)
+    kCopySend,            // own input -> output and wire (AllGather start)
+    // Simple peer-direct mode: the chain's second rank reads the chain start's
+    // input straight from that rank's buffer instead of a first FIFO hop.
+    kPeerReduceSend,      // peer input + own input -> wire
+    kPeerReduceCopySend,  // peer input + own input -> output and wire (2-rank AllReduce owner)
+    kPeerReduceCopy       // peer input + own input -> output (2-rank ReduceScatter owner)
 };
 
 // What a step kind does, shared by the three protocols.
@@ -90,11 +95,15 @@ template <int KIND>
 struct KindTraits {
     static constexpr bool kRecvRS = KIND == kRecvReduceSend || KIND == kRecvReduceCopySend || KIND == kRecvReduceCopy;
     static constexpr bool kRecvAG = KIND == kRecvCopySend || KIND == kRecvCopy;
-    static constexpr bool kLoadIn = KIND == kSend || kRecvRS || KIND == kCopySend;
-    static constexpr bool kSendRS = KIND == kSend || KIND == kRecvReduceSend;
-    static constexpr bool kSendAG = KIND == kRecvReduceCopySend || KIND == kRecvCopySend || KIND == kCopySend;
-    static constexpr bool kWriteOut = KIND == kRecvReduceCopySend || kRecvAG || KIND == kRecvReduceCopy || KIND == kCopySend;
-    static constexpr bool kReduceToY = KIND == kRecvReduceCopySend || KIND == kRecvReduceCopy;  // y = rounded sum
+    // the partial to add is the chain start's input, read from its buffer
+    static constexpr bool kRecvPeer = KIND == kPeerReduceSend || KIND == kPeerReduceCopySend || KIND == kPeerReduceCopy;
+    static constexpr bool kLoadIn = KIND == kSend || kRecvRS || KIND == kCopySend || kRecvPeer;
+    static constexpr bool kSendRS = KIND == kSend || KIND == kRecvReduceSend || KIND == kPeerReduceSend;
+    static constexpr bool kSendAG = KIND == kRecvReduceCopySend || KIND == kRecvCopySend || KIND == kCopySend ||
+                                    KIND == kPeerReduceCopySend;
+    static constexpr bool kReduceToY = KIND == kRecvReduceCopySend || KIND == kRecvReduceCopy ||
+                                       KIND == kPeerReduceCopySend || KIND == kPeerReduceCopy;  // y = rounded sum
+    static constexpr bool kWriteOut = kReduceToY || kRecvAG || KIND == kCopySend;
     static constexpr bool kCopyInToY = KIND == kCopySend;                                      // y = own input
 };
 
@@ -366,6 +375,7 @@ struct SimpleStep {
     static constexpr bool kWriteOut = KindTraits<KIND>::kWriteOut;
     static constexpr bool kReduceToY = KindTraits<KIND>::kReduceToY;
     static constexpr bool kCopyInToY = KindTraits<KIND>::kCopyInToY;
+    static constexpr bool kRecvPeer = KindTraits<KIND>::kRecvPeer;
     static constexpr int U = AR_SIMPLE_U;
     // With DAG a received all-gather message is already in the own output.
     static constexpr bool kWriteOwn = kWriteOut && !(DAG && kRecvAG);
@@ -397,7 +407,8 @@ struct SimpleStep {
         }
     }
 
-    // acc[A] = RS wire partials + widened input (or just the input at k = 0).
+    // acc[A] = RS wire partials (or the widened peer input) + widened input
+    // (or just the input at k = 0).
     __device__ static void reduce(const u32x4 *rs, u32x4 in, float *acc)
     {
         if (E == 4) {
@@ -412,12 +423,23 @@ struct SimpleStep {
             for (uint32_t v = 0; v < RSV; ++v)
                 for (int i = 0; i < 4; ++i) acc[4 * v + i] = as_f32(rs[v][i]) + acc[4 * v + i];
         }
+        if (kRecvPeer) {  // rs[0]: the chain start's unit, in the data type
+            if (E == 4) {
+                for (int i = 0; i < 4; ++i) acc[i] = as_f32(rs[0][i]) + acc[i];
+            } else {
+                for (int i = 0; i < 4; ++i) {
+                    acc[2 * i] = bf16_lo(rs[0][i]) + acc[2 * i];
+                    acc[2 * i + 1] = bf16_hi(rs[0][i]) + acc[2 * i + 1];
+                }
+            }
+        }
     }
 
     __device__ static void unit(Rsrc rin, Rsrc rout, Rsrc wi, Rsrc wo, uint32_t u, uint32_t valid, uint32_t nunits,
                                 const u32x4 &in, const u32x4 *rs, const u32x4 &ag)
     {
         (void)rin;
+        static_assert(!kRecvPeer || DAG, "peer reads belong to the peer-direct mode");
         float acc[A];
         if (kSendRS || kReduceToY) reduce(rs, in, acc);
         if (kSendRS) {
@@ -462,7 +484,7 @@ struct SimpleStep {
         const uint32_t nunits = nfull + (rem ? 1u : 0u);
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
-        const Rsrc wi = make_rsrc(rslot, DAG && kRecvAG ? (uint64_t)len * E : a.slot_bytes);
+        const Rsrc wi = make_rsrc(rslot, (DAG && kRecvAG) || kRecvPeer ? (uint64_t)len * E : a.slot_bytes);
         const Rsrc wo = make_rsrc(wslot, DAG && kSendAG ? (uint64_t)len * E : a.slot_bytes);
         for (uint32_t base = 0; base < nfull; base += 64 * U) {
             u32x4 in[U], rs[U][RSV], ag[U];
@@ -473,6 +495,7 @@ struct SimpleStep {
                     if (kLoadIn) in[t] = ld128<kInPol>(rin, u * 16);
                     if (kRecvRS)
                         for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoLd>(wi, wide_off(u, v, RSV, nunits));
+                    if (kRecvPeer) rs[t][0] = ld128<kInPol>(wi, u * 16);
                     if (kRecvAG) ag[t] = ld128<kAgLdPol>(wi, u * 16);
                 }
             }
@@ -488,6 +511,7 @@ struct SimpleStep {
             if (kLoadIn) in = load_partial<kInPol>(rin, u * 16, rem);
             if (kRecvRS)
                 for (uint32_t v = 0; v < RSV; ++v) rs[v] = ld128<kFifoLd>(wi, wide_off(u, v, RSV, nunits));
+            if (kRecvPeer) rs[0] = load_partial<kInPol>(wi, u * 16, rem);
             if (kRecvAG) ag = DAG ? load_partial<kAgLdPol>(wi, u * 16, rem) : ld128<kAgLdPol>(wi, u * 16);
             unit(rin, rout, wi, wo, u, rem, nunits, in, rs, ag);
         }
@@ -495,11 +519,15 @@ struct SimpleStep {
 };
 
 // dst: this step's elements in the own output; peer_dst: the same elements
-// in the next rank's output (used by DAG all-gather sends only).
+// in the next rank's output (DAG all-gather sends); peer_src: the same
+// elements of the previous rank's input (peer-direct chain starts).
 template <int DT, int KIND, bool DAG>
-__device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst, char *peer_dst, uint32_t len)
+__device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst, char *peer_dst,
+                                            const char *peer_src, uint32_t len)
 {
     const RingArgs &a = *g.a;
+    // A peer read needs no message: the chain start's input is in place
+    // before the kernel starts and stays there until the chain is done.
     constexpr bool recv = KindTraits<KIND>::kRecvRS || KindTraits<KIND>::kRecvAG;
     constexpr bool send = KindTraits<KIND>::kSendRS || KindTraits<KIND>::kSendAG;
     // With DAG only reduce-scatter messages occupy FIFO slots.
@@ -511,6 +539,7 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
         if (!wait_geq(a, g.tail_in, g.m_in + 1, g.tail_seen)) return false;
         rslot = fifo_in ? slot_ptr(const_cast<char *>(g.fifo_in), g.slot_in, a) : dst;
     }
+    if (KindTraits<KIND>::kRecvPeer) rslot = peer_src;
     if (send) {
         if (fifo_out && !acquire_send_slot(g)) return false;
         wslot = fifo_out ? slot_ptr(g.fifo_out, g.slot_out, a) : peer_dst;
@@ -1000,10 +1029,10 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
 // ===================================================================== kernel
 
 template <int PROTO, int DT, bool DAG, int KIND>
-__device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, char *peer_dst, uint32_t len,
-                                        uint32_t *lds)
+__device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, char *peer_dst, const char *peer_src,
+                                        uint32_t len, uint32_t *lds)
 {
-    if (PROTO == AR_PROTO_SIMPLE) return simple_step<DT, KIND, DAG>(g, src, dst, peer_dst, len);
+    if (PROTO == AR_PROTO_SIMPLE) return simple_step<DT, KIND, DAG>(g, src, dst, peer_dst, peer_src, len);
     if (PROTO == AR_PROTO_LL) return ll_step<DT, KIND>(g, src, dst, len);
     return ll128_step<DT, KIND>(g, src, dst, len, lds);
 }
@@ -1020,15 +1049,21 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
     //   AllReduce      k = 0 .. 2N-2, segment (r - k) mod N, owner of s is s-1
     //   ReduceScatter  k = 0 .. N-1,  segment (r - 1 - k) mod N, owner of s is s
     //   AllGather      k = 0 .. N-1,  segment (r - k) mod N, starting from the own block
+    // In the peer-direct mode (DAG) a reduction chain has no step 0: at step
+    // 1 the second rank reads the chain start's input from that rank's buffer.
     const char *src = a.src[r];
     char *dst = a.dst[r];
-    char *peer = DAG ? a.dst[r + 1 == N ? 0 : r + 1] : nullptr;  // the next rank's output
+    char *peer = DAG ? a.dst[r + 1 == N ? 0 : r + 1] : nullptr;             // the next rank's output
+    const char *prev_src = DAG ? a.src[r == 0 ? N - 1 : r - 1] : nullptr;  // the previous rank's input
     const uint32_t coll = a.coll;
+    const bool peer_start = DAG && coll != AR_COLL_ALLGATHER;
     const uint32_t nsteps = coll == AR_COLL_ALLREDUCE ? 2 * N - 1 : N;
-    const uint32_t s0 = coll == AR_COLL_REDUCESCATTER ? (r + N - 1) % N : r;
+    const uint32_t k0 = peer_start ? 1u : 0u;
+    uint32_t s0 = coll == AR_COLL_REDUCESCATTER ? (r + N - 1) % N : r;
+    if (peer_start) s0 = s0 == 0 ? N - 1 : s0 - 1;
     for (uint32_t j = 0; j < a.nchunks; ++j) {
         uint32_t s = s0;
-        for (uint32_t k = 0; k < nsteps; ++k, s = s == 0 ? N - 1 : s - 1) {
+        for (uint32_t k = k0; k < nsteps; ++k, s = s == 0 ? N - 1 : s - 1) {
             const uint64_t seg_lo = (uint64_t)s * a.seg;
             const uint64_t seg_hi = seg_lo + a.seg < a.count ? seg_lo + a.seg : a.count;
             const uint64_t ch_lo = seg_lo + (uint64_t)c * a.cs;
@@ -1044,21 +1079,34 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
             const char *s_ptr = src + in_e * E;
             char *d_ptr = dst + out_e * E;
             char *p_ptr = DAG ? peer + out_e * E : nullptr;
+            const char *q_ptr = DAG ? prev_src + in_e * E : nullptr;
             bool ok;
+            if constexpr (DAG) {
+                if (peer_start && k == 1) {
+                    if (coll == AR_COLL_ALLREDUCE && N == 2)
+                        ok = do_step<PROTO, DT, DAG, kPeerReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                    else if (N == 2)
+                        ok = do_step<PROTO, DT, DAG, kPeerReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                    else
+                        ok = do_step<PROTO, DT, DAG, kPeerReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                    if (!ok) return false;
+                    continue;
+                }
+            }
             if (coll == AR_COLL_ALLREDUCE) {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, kSend>(g, s_ptr, d_ptr, p_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, len, lds);
-                else if (k == N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceCopySend>(g, s_ptr, d_ptr, p_ptr, len, lds);
-                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, DAG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k == N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, DAG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             } else if (coll == AR_COLL_REDUCESCATTER) {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, kSend>(g, s_ptr, d_ptr, p_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, kRecvReduceCopy>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, kRecvReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             } else {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, kCopySend>(g, s_ptr, d_ptr, p_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, kCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             }
             if (!ok) return false;
         }
@@ -1112,8 +1160,13 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
     const uint64_t epoch = uniform64(flag_load(epoch_p));
     g.head_seen = uniform64(flag_load(g.head_out));
     after_observe();
-    if (lane_id() == 0)
-        flag_store(epoch_p, epoch + (uint64_t)a.nchunks * (a.coll == AR_COLL_ALLREDUCE ? 2 * N - 2 : N - 1));
+    if (lane_id() == 0) {
+        // messages per chunk: 2N-2 (AllReduce) or N-1, one fewer when a
+        // reduction chain starts with a peer read
+        const uint64_t per_chunk = (a.coll == AR_COLL_ALLREDUCE ? 2 * N - 2 : N - 1) -
+                                   (DAG && a.coll != AR_COLL_ALLGATHER ? 1 : 0);
+        flag_store(epoch_p, epoch + (uint64_t)a.nchunks * per_chunk);
+    }
     g.m_out = epoch;
     g.m_in = epoch;
     g.slot_out = g.slot_in = (uint32_t)(epoch % a.depth);
@@ -1342,7 +1395,7 @@ __host__ RingFn direct_fn(int dtype, int nranks, int unroll)
 int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
 {
     dev::RingFn fn = info.algo == AR_ALGO_DIRECT ? dev::direct_fn(info.dtype, info.nranks, info.direct_unroll)
-                                                 : dev::ring_fn(info.proto, info.dtype, info.ag_direct != 0);
+                                                 : dev::ring_fn(info.proto, info.dtype, info.peer_direct != 0);
     RingArgs a = args;
     void *kargs[] = {&a};
     hipError_t e = hipLaunchKernel((const void *)fn, dim3((unsigned)info.grid), dim3((unsigned)info.block), kargs,

@@ -255,7 +255,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     if (d->direct_unroll < 0 || d->direct_unroll > 2) return AR_ERR_ARG;
     if (d->placement != AR_PLACE_RANK_SPREAD && d->placement != AR_PLACE_CHANNEL_LOCAL) return AR_ERR_ARG;
     if (d->chunk_bytes > kMaxChunkBytes) return AR_ERR_ARG;
-    if (d->flags & ~(uint32_t)(AR_PLAN_PROFILE | AR_PLAN_FIFO_ALLGATHER)) return AR_ERR_ARG;
+    if (d->flags & ~(uint32_t)(AR_PLAN_PROFILE | AR_PLAN_FIFO_ONLY)) return AR_ERR_ARG;
     if (!valid_algo(d->algo)) return AR_ERR_ARG;
     if (d->coll != AR_COLL_ALLREDUCE && d->coll != AR_COLL_REDUCESCATTER && d->coll != AR_COLL_ALLGATHER)
         return AR_ERR_ARG;
@@ -320,7 +320,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     g.placement = d->placement;
     g.count = d->count;
     g.block = 64 * nw;
-    g.ag_direct = proto == AR_PROTO_SIMPLE && d->coll != AR_COLL_REDUCESCATTER && !(d->flags & AR_PLAN_FIFO_ALLGATHER);
+    g.peer_direct = proto == AR_PROTO_SIMPLE && !(d->flags & AR_PLAN_FIFO_ONLY);
 
     const uint64_t N = (uint64_t)d->nranks;
     g.seg_elems = d->coll == AR_COLL_ALLREDUCE ? round_up(ceil_div(d->count, N), A) : d->count;
@@ -351,7 +351,11 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     const uint64_t conns = (uint64_t)nch * N * (uint64_t)nw;
     g.fifo_bytes = conns * (uint64_t)depth * g.slot_bytes;
     g.flag_bytes = conns * kConnFlagU64 * 8 + kCtlU32 * 4;
-    g.msgs_per_run = g.nchunks * (d->coll == AR_COLL_ALLREDUCE ? 2 * N - 2 : N - 1);
+    // Messages per connection: 2N-2 per chunk (AllReduce) or N-1; with the
+    // peer-direct Simple ring a reduction chain starts with a peer read, one
+    // message fewer.
+    g.msgs_per_run = g.nchunks * ((d->coll == AR_COLL_ALLREDUCE ? 2 * N - 2 : N - 1) -
+                                  (g.peer_direct && d->coll != AR_COLL_ALLGATHER ? 1 : 0));
 
     // Wire bytes actually written per run.  AllReduce: each element crosses
     // 2(N-1) links, N-1 as an fp32 partial and N-1 as a finished value;
@@ -359,11 +363,14 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     // AllGather: each of N blocks crosses N-1 links as data.
     const double ag_e = (double)e;
     double rs_bytes = 0, ag_bytes = 0;
+    // With the peer-direct Simple ring the first link of a chain carries the
+    // chain start's input in the data type (a peer read), not a partial.
+    const double rs_link = g.peer_direct ? 4.0 * (double)(N - 2) + (double)e : 4.0 * (double)(N - 1);
     if (d->coll == AR_COLL_ALLREDUCE) {
-        rs_bytes = (double)d->count * 4.0 * (double)(N - 1);
+        rs_bytes = (double)d->count * rs_link;
         ag_bytes = (double)d->count * ag_e * (double)(N - 1);
     } else if (d->coll == AR_COLL_REDUCESCATTER) {
-        rs_bytes = (double)d->count * (double)N * 4.0 * (double)(N - 1);
+        rs_bytes = (double)d->count * (double)N * rs_link;
     } else {
         ag_bytes = (double)d->count * (double)N * ag_e * (double)(N - 1);
     }

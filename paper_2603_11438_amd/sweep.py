@@ -466,7 +466,7 @@ def _config_points(name):
         return wl, [dict(proto="simple", nchannels=c, chunk_bytes=k) for k in wl.chunks for c in wl.channels]
     if name == "D5":
         return wl, ([dict(proto=p, nchannels=c) for p in wl.protos for c in wl.channels] +
-                    [dict(proto="simple", nchannels=c, flags=ar.AR_PLAN_FIFO_ALLGATHER) for c in wl.channels])
+                    [dict(proto="simple", nchannels=c, flags=ar.AR_PLAN_FIFO_ONLY) for c in wl.channels])
     raise ValueError(name)
 
 
@@ -491,10 +491,10 @@ def configs(args):
                 info = plan.info
                 st = _stats(times)
                 t = st["p50_us"] * 1e-6
-                rb = ar.ring_bytes(size, n, dtype, info["proto_name"], ag_direct=bool(info["ag_direct"]))
+                rb = ar.ring_bytes(size, n, dtype, info["proto_name"], peer_direct=bool(info["peer_direct"]))
                 cb = ar.compulsory_bytes(size, n)
                 rec = {"workload": name, "size": size, "dtype": dtype, **cfg, "proto": info["proto_name"],
-                       "ag_direct": info["ag_direct"],
+                       "peer_direct": info["peer_direct"],
                        "nchannels_eff": info["nchannels"], "chunk_eff": info["chunk_elems"] * (4 if dtype == "f32" else 2),
                        "nwaves": info["nwaves"], "nchunks": info["nchunks"], **st,
                        "algbw": ar.alg_bandwidth(size, t), "busbw": ar.bus_bandwidth(size, t, n),

@@ -195,7 +195,8 @@ def test_geometry_segment_rule_matches_oracle(dtype):
                     assert g["nchunks"] * g["chunk_elems"] >= g["chan_elems"]
                     assert (g["nchunks"] - 1) * g["chunk_elems"] < g["chan_elems"]
                     assert g["wave_elems"] * g["nwaves"] >= g["chunk_elems"]
-                    assert g["msgs_per_run"] == g["nchunks"] * (2 * n - 2)
+                    # the peer-direct Simple ring starts each chain with a peer read
+                    assert g["msgs_per_run"] == g["nchunks"] * (2 * n - 2 - g["peer_direct"])
                     wire = {"ll": 8 * g["wave_elems"], "simple": 4 * g["wave_elems"],
                             "ll128": -(-4 * g["wave_elems"] // 120) * 128}[proto]
                     assert g["slot_bytes"] >= wire and g["slot_bytes"] % 256 == 0
@@ -259,12 +260,14 @@ def test_ring_byte_counts():
     assert abs(ar.ring_bytes(S, 8, "f32", "ll128") - (16 + 28 * 128 / 120) * S) < 1
     assert ar.ring_bytes(S, 8, "bf16", "simple") == 58 * S
     assert ar.compulsory_bytes(S, 8) == 16 * S
-    # Simple with the direct all-gather: 8 ranks fp32 36 S, bf16 50 S; with
-    # 2 ranks only the chain start and the owner move data (fp32 6 S).
-    assert ar.ring_bytes(S, 8, "f32", "simple", ag_direct=True) == 36 * S
-    assert ar.ring_bytes(S, 8, "bf16", "simple", ag_direct=True) == 50 * S
-    assert ar.ring_bytes(S, 2, "f32", "simple", ag_direct=True) == 6 * S
-    assert ar.ring_bytes(S, 8, "f32", "ll", ag_direct=True) == 72 * S  # LL has no direct mode
+    # The peer-direct Simple ring: 8 ranks fp32 34 S, bf16 46 S; with 2 ranks
+    # the owner reads both inputs and writes both outputs (4 S).
+    assert ar.ring_bytes(S, 8, "f32", "simple", peer_direct=True) == 34 * S
+    assert ar.ring_bytes(S, 8, "bf16", "simple", peer_direct=True) == 46 * S
+    assert ar.ring_bytes(S, 2, "f32", "simple", peer_direct=True) == 4 * S
+    # 3 ranks fp32: second rank 12 B, owner 16 B, forwarder 8 B per element
+    assert ar.ring_bytes(S, 3, "f32", "simple", peer_direct=True) == 9 * S
+    assert ar.ring_bytes(S, 8, "f32", "ll", peer_direct=True) == 72 * S  # LL has no direct mode
 
 
 def test_direct_unroll_resolution():
@@ -295,13 +298,18 @@ def test_direct_unroll_resolution():
 def test_direct_allgather_mode_in_geometry():
     def geom(proto, coll="allreduce", flags=0):
         return ar.ar_plan_geometry(ar.make_desc(8, 1 << 16, "f32", proto, 4, coll=coll, flags=flags, algo="ring"))
-    assert geom("simple")["ag_direct"] == 1
-    assert geom("simple", "allgather")["ag_direct"] == 1
-    assert geom("simple", "reducescatter")["ag_direct"] == 0
-    assert geom("simple", flags=ar.AR_PLAN_FIFO_ALLGATHER)["ag_direct"] == 0
-    assert geom("ll")["ag_direct"] == 0 and geom("ll128")["ag_direct"] == 0
-    # the same link bytes either way
-    assert geom("simple")["wire_bytes_per_run"] == geom("simple", flags=ar.AR_PLAN_FIFO_ALLGATHER)["wire_bytes_per_run"]
+    assert geom("simple")["peer_direct"] == 1
+    assert geom("simple", "allgather")["peer_direct"] == 1
+    assert geom("simple", "reducescatter")["peer_direct"] == 1
+    assert geom("simple", flags=ar.AR_PLAN_FIFO_ONLY)["peer_direct"] == 0
+    assert geom("ll")["peer_direct"] == 0 and geom("ll128")["peer_direct"] == 0
+    # one message fewer per chunk when a chain starts with a peer read
+    for coll, per_chunk in (("allreduce", 2 * 8 - 2), ("reducescatter", 8 - 1), ("allgather", 8 - 1)):
+        d, f = geom("simple", coll), geom("simple", coll, flags=ar.AR_PLAN_FIFO_ONLY)
+        assert f["msgs_per_run"] == f["nchunks"] * per_chunk
+        assert d["msgs_per_run"] == d["nchunks"] * (per_chunk - (coll != "allgather"))
+    # fp32: the same link bytes either way (the first link carries 4 bytes either way)
+    assert geom("simple")["wire_bytes_per_run"] == geom("simple", flags=ar.AR_PLAN_FIFO_ONLY)["wire_bytes_per_run"]
     d = ar.make_desc(8, 1 << 16, "f32", "simple", 4, flags=8)
     assert ar.lib().ar_plan_geometry(ctypes.byref(d), ctypes.byref(ar.ar_plan_info())) == ar.AR_ERR_ARG
 
