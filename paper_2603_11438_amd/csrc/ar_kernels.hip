@@ -353,14 +353,15 @@ __device__ __forceinline__ uint32_t wide_off(uint32_t i, uint32_t v, uint32_t nv
 // A unit is A elements = 16 bytes of the data type; lanes take consecutive
 // units, U units per lane per batch, all loads of a batch before its stores.
 //
-// DAG (direct all-gather): an all-gather message is not staged in the FIFO.
-// The sender writes the finished values straight into the next rank's output
-// buffer, at the place they belong, and announces them with the same tail
-// counter; the receiver forwards them from its own output buffer, and the
-// last hop of the ring moves no data at all.  The all-gather half then costs
-// two accesses per element and hop instead of three.  Every access to an
-// output buffer in this mode is device-coherent, because ranks on other
-// XCDs write into it.
+// DAG (peer-direct mode) uses the neighbours' buffers where that saves a
+// copy.  (1) An all-gather message is not staged in the FIFO: the sender
+// writes the finished values straight into the next rank's output buffer, at
+// the place they belong, and announces them with the same tail counter; the
+// receiver forwards them from its own output buffer, and the last hop of the
+// ring moves no data at all.  (2) A reduction chain has no first FIFO hop:
+// its second rank reads the chain start's input from that rank's buffer.
+// Every access to an output buffer in this mode is device-coherent, because
+// ranks on other XCDs write into it.
 
 template <int DT, int KIND, bool DAG>
 struct SimpleStep {
