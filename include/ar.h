@@ -178,11 +178,12 @@ typedef struct ar_plan_info {
     size_t flag_bytes;     /* head/tail counters, ring epochs, control words */
     uint64_t msgs_per_run; /* messages per connection per run: nchunks*(2N-2)
                               (AllReduce) or nchunks*(N-1) (ReduceScatter /
-                              AllGather) */
+                              AllGather); with peer_direct, nchunks fewer for
+                              AllReduce and ReduceScatter */
     uint64_t wire_bytes_per_run; /* bytes that cross ring links per run (all
-                              connections): written to a FIFO with flags, or
-                              with the direct all-gather into the next rank's
-                              output */
+                              connections): written to a FIFO with flags, or,
+                              with peer_direct, all-gather chunks written into
+                              the next rank's output */
     int algo;              /* AR_ALGO_RING or AR_ALGO_DIRECT */
     int coll;              /* AR_COLL_* */
     int peer_direct;       /* 1: the Simple ring reads the chain start's input
