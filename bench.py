@@ -100,7 +100,14 @@ def cpu_baseline(wl, target_s: float) -> dict:
 
     v, reps, el = timed(threads, target_s)
     v1, reps1, el1 = timed(1, target_s / 3)
-    return {"value": v, "unit": "GB/s", "cores": threads, "kind": "oracle",
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
+    return {"value": v, "unit": "GB/s", "cores": threads, "kind": "oracle", "cpu_model": model,
+            "host_cpus": os.cpu_count(),
             "sample": f"{reps} full passes of the plain-C oracle over the {wl.name} input "
                       f"({wl.nranks} x {s} B {wl.dtype}), {threads} OpenMP threads, {el:.1f} s",
             "single_thread": {"value": v1, "unit": "GB/s",

@@ -18,6 +18,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "_lib", "libar.so")
 
 # ---- constants (include/ar.h) -------------------------------------------
+AR_VERSION = 3  # the interface revision include/ar.h declares
 AR_FLOAT32, AR_BFLOAT16 = 0, 1
 AR_PROTO_AUTO, AR_PROTO_LL, AR_PROTO_LL128, AR_PROTO_SIMPLE = -1, 0, 1, 2
 AR_COLL_ALLREDUCE, AR_COLL_REDUCESCATTER, AR_COLL_ALLGATHER = 0, 1, 2
