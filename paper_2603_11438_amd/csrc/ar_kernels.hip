@@ -151,7 +151,31 @@ template <int POL> __device__ __forceinline__ void st16(Rsrc r, uint32_t off, ui
     __builtin_amdgcn_raw_buffer_store_b16((unsigned short)v, r, (int)off, 0, POL);
 }
 
+// A buffer offset outside every resource built by the ring steps (each covers
+// at most one step's data or one FIFO slot, far below 2^31 bytes): a load
+// there returns zeros and a store there is dropped, by the hardware's range
+// check.  Lanes past the end of a message use it instead of a branch, which
+// keeps a batch of accesses straight-line code; the compiler can then wait
+// for exactly the loads an instruction needs instead of for every
+// outstanding access (a branch around each access makes it wait for all of
+// them, earlier stores included, before each store).
+constexpr uint32_t kOobOff = 0x80000000u;
+__device__ __forceinline__ uint32_t in_range(bool ok, uint32_t off) { return ok ? off : kOobOff; }
+
 __device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & 63u; }
+
+// True on every lane when p holds on any active lane; the result is a
+// wave-uniform value the compiler knows to be uniform.
+//
+// Uniformity matters throughout the ring steps: a branch on the lane (such as
+// "lane 0 stores the flag") whose join merges any value makes the compiler
+// treat everything that depends on it as per-lane.  The step loop then runs
+// under an execution mask, loop-carried counters and pointers move into
+// vector registers, and every buffer access is wrapped in a loop that reads
+// its descriptor lane by lane.  So flags are stored by every lane (the same
+// value to the same address: one write), and partial units and groups use
+// out-of-range offsets instead of lane branches.
+__device__ __forceinline__ bool any_lane(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0; }
 
 // The lane index as a value the compiler may not hoist out of the step loop:
 // a step's per-lane offsets are then recomputed each step (a few ALU ops)
@@ -229,13 +253,13 @@ __device__ __forceinline__ bool watchdog_expired(const RingArgs &a, Watchdog &wd
     if ((++wd.iter & 31u) != 0) return false;
     uint32_t ab = __hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (__builtin_amdgcn_readfirstlane(ab) != 0) return true;
-    uint64_t now = wall_clock64();
+    uint64_t now = uniform64(wall_clock64());
     if (wd.start == 0) {
         wd.start = now;
         return false;
     }
     if (now - wd.start > a.timeout_ticks) {
-        if (lane_id() == 0) {
+        {  // every lane (see any_lane): the same bit, the same word
             __hip_atomic_fetch_or(a.ctl + kCtlStatus, kStatusTimeout, __ATOMIC_RELAXED,
                                   __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(a.ctl + kCtlAbort, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -257,6 +281,29 @@ __device__ __forceinline__ bool wait_geq(const RingArgs &a, const uint64_t *flag
             cache = v;
             break;
         }
+        __builtin_amdgcn_s_sleep(1);
+        if (watchdog_expired(a, wd)) return false;
+    }
+    after_observe();
+    return true;
+}
+
+// Wait until *f1 >= t1 and, when f2 is given, *f2 >= t2, reading both
+// counters in each round trip (a receiver's incoming tail and its outgoing
+// head: the send credit then costs no round trip of its own).
+__device__ __forceinline__ bool wait_geq2(const RingArgs &a, const uint64_t *f1, uint64_t t1, uint64_t &c1,
+                                          const uint64_t *f2, uint64_t t2, uint64_t &c2)
+{
+    const bool two = f2 != nullptr;
+    if (c1 >= t1 && (!two || c2 >= t2)) return true;
+    const uint64_t *g2 = two ? f2 : f1;
+    Watchdog wd;
+    while (true) {
+        const uint64_t v1 = uniform64(flag_load(f1));
+        const uint64_t v2 = uniform64(flag_load(g2));
+        if (v1 > c1) c1 = v1;
+        if (two && v2 > c2) c2 = v2;
+        if (c1 >= t1 && (!two || c2 >= t2)) break;
         __builtin_amdgcn_s_sleep(1);
         if (watchdog_expired(a, wd)) return false;
     }
@@ -312,6 +359,14 @@ __device__ __forceinline__ void advance_in(Ring &g)
 {
     ++g.m_in;
     g.slot_in = g.slot_in + 1 == g.a->depth ? 0u : g.slot_in + 1;
+}
+
+// True when the last head value seen already frees the slot of message
+// m_out (the receiver has consumed message m_out - depth).
+__device__ __forceinline__ bool slot_free_cached(const Ring &g)
+{
+    const uint64_t d = g.a->depth;
+    return g.m_out + 1 <= d || g.head_seen >= g.m_out + 1 - d;
 }
 
 // Sender side: wait until the slot of message m_out is free, i.e. the
@@ -436,10 +491,11 @@ struct SimpleStep {
         }
     }
 
-    __device__ static void unit(Rsrc rin, Rsrc rout, Rsrc wi, Rsrc wo, uint32_t u, uint32_t valid, uint32_t nunits,
+    // ok = false: a lane past the end of the message, whose full-unit
+    // accesses are sent out of range.
+    __device__ static void unit(Rsrc rout, Rsrc wo, uint32_t u, bool ok, uint32_t valid, uint32_t nunits,
                                 const u32x4 &in, const u32x4 *rs, const u32x4 &ag)
     {
-        (void)rin;
         static_assert(!kRecvPeer || DAG, "peer reads belong to the peer-direct mode");
         float acc[A];
         if (kSendRS || kReduceToY) reduce(rs, in, acc);
@@ -447,7 +503,7 @@ struct SimpleStep {
             for (uint32_t v = 0; v < RSV; ++v) {
                 u32x4 o = {as_u32(acc[4 * v]), as_u32(acc[4 * v + 1]), as_u32(acc[4 * v + 2]),
                            as_u32(acc[4 * v + 3])};
-                st128<kFifoSt>(wo, wide_off(u, v, RSV, nunits), o);
+                st128<kFifoSt>(wo, in_range(ok, wide_off(u, v, RSV, nunits)), o);
             }
         }
         u32x4 y;
@@ -463,15 +519,14 @@ struct SimpleStep {
             y = ag;
         }
         if (kWriteOwn) {
-            if (valid == A) st128<kOwnPol>(rout, u * 16, y);
+            if (valid == A) st128<kOwnPol>(rout, in_range(ok, u * 16), y);
             else store_partial<kOwnPol>(rout, u * 16, y, valid);
         }
         if (kSendAG) {
             // A FIFO slot is padded to whole units; the next rank's output is not.
-            if (valid == A || !DAG) st128<kFifoSt>(wo, u * 16, y);
+            if (valid == A || !DAG) st128<kFifoSt>(wo, in_range(ok, u * 16), y);
             else store_partial<kFifoSt>(wo, u * 16, y, valid);
         }
-        (void)wi;
     }
 
     // rslot / wslot: FIFO slots, or with DAG for all-gather messages the own
@@ -492,18 +547,18 @@ struct SimpleStep {
 #pragma unroll
             for (int t = 0; t < U; ++t) {
                 const uint32_t u = base + 64 * t + lane;
-                if (u < nfull) {
-                    if (kLoadIn) in[t] = ld128<kInPol>(rin, u * 16);
-                    if (kRecvRS)
-                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoLd>(wi, wide_off(u, v, RSV, nunits));
-                    if (kRecvPeer) rs[t][0] = ld128<kInPol>(wi, u * 16);
-                    if (kRecvAG) ag[t] = ld128<kAgLdPol>(wi, u * 16);
-                }
+                const bool ok = u < nfull;
+                if (kLoadIn) in[t] = ld128<kInPol>(rin, in_range(ok, u * 16));
+                if (kRecvRS)
+                    for (uint32_t v = 0; v < RSV; ++v)
+                        rs[t][v] = ld128<kFifoLd>(wi, in_range(ok, wide_off(u, v, RSV, nunits)));
+                if (kRecvPeer) rs[t][0] = ld128<kInPol>(wi, in_range(ok, u * 16));
+                if (kRecvAG) ag[t] = ld128<kAgLdPol>(wi, in_range(ok, u * 16));
             }
 #pragma unroll
             for (int t = 0; t < U; ++t) {
                 const uint32_t u = base + 64 * t + lane;
-                if (u < nfull) unit(rin, rout, wi, wo, u, A, nunits, in[t], rs[t], ag[t]);
+                unit(rout, wo, u, u < nfull, A, nunits, in[t], rs[t], ag[t]);
             }
         }
         if (rem && lane == (nfull & 63u)) {
@@ -514,7 +569,7 @@ struct SimpleStep {
                 for (uint32_t v = 0; v < RSV; ++v) rs[v] = ld128<kFifoLd>(wi, wide_off(u, v, RSV, nunits));
             if (kRecvPeer) rs[0] = load_partial<kInPol>(wi, u * 16, rem);
             if (kRecvAG) ag = DAG ? load_partial<kAgLdPol>(wi, u * 16, rem) : ld128<kAgLdPol>(wi, u * 16);
-            unit(rin, rout, wi, wo, u, rem, nunits, in, rs, ag);
+            unit(rout, wo, u, true, rem, nunits, in, rs, ag);
         }
     }
 };
@@ -537,7 +592,12 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
     const char *rslot = nullptr;
     char *wslot = nullptr;
     if (recv) {
-        if (!wait_geq(a, g.tail_in, g.m_in + 1, g.tail_seen)) return false;
+        // The incoming tail and, if the cached credit does not cover this
+        // message, the outgoing head are polled together.
+        const bool credit = fifo_out && !slot_free_cached(g);
+        if (!wait_geq2(a, g.tail_in, g.m_in + 1, g.tail_seen, credit ? g.head_out : nullptr,
+                       g.m_out + 1 - a.depth, g.head_seen))
+            return false;
         rslot = fifo_in ? slot_ptr(const_cast<char *>(g.fifo_in), g.slot_in, a) : dst;
     }
     if (KindTraits<KIND>::kRecvPeer) rslot = peer_src;
@@ -550,11 +610,11 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
     drain_vmem();
     if (send) {
         debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
-        if (!skip_this_post(g) && lane_id() == 0) flag_store(g.tail_out, g.m_out + 1);
+        if (!skip_this_post(g)) flag_store(g.tail_out, g.m_out + 1);
         advance_out(g);
     }
     if (recv) {
-        if (lane_id() == 0) flag_store(g.head_in, g.m_in + 1);
+        flag_store(g.head_in, g.m_in + 1);
         advance_in(g);
     }
     return true;
@@ -584,122 +644,159 @@ struct LLStep {
     static constexpr bool kCopyInToY = KindTraits<KIND>::kCopyInToY;
     static constexpr int U = 4;
 
-    __device__ static u32x2 load_in(Rsrc r, uint32_t q, uint32_t valid)
+    // A partial group (valid < G elements) moves element by element; ok =
+    // false sends every access out of range.
+    __device__ static u32x2 load_part(Rsrc r, uint32_t q, uint32_t valid, bool ok)
     {
-        if (valid == G) return ld64<kInPol>(r, q * 8);
         u32x2 v = {0, 0};
         for (uint32_t i = 0; i < valid; ++i) {
-            if (E == 4) v[i] = ld32<kInPol>(r, q * 8 + 4 * i);
-            else v[i >> 1] |= ld16<kInPol>(r, q * 8 + 2 * i) << ((i & 1) * 16);
+            if (E == 4) v[i] = ld32<kInPol>(r, in_range(ok, q * 8 + 4 * i));
+            else v[i >> 1] |= ld16<kInPol>(r, in_range(ok, q * 8 + 2 * i)) << ((i & 1) * 16);
         }
         return v;
     }
-    __device__ static void store_out(Rsrc r, uint32_t q, u32x2 v, uint32_t valid)
+    __device__ static void store_part(Rsrc r, uint32_t q, u32x2 v, uint32_t valid, bool ok)
     {
-        if (valid == G) {
-            st64<kOutPol>(r, q * 8, v);
-            return;
-        }
         for (uint32_t i = 0; i < valid; ++i) {
-            if (E == 4) st32<kOutPol>(r, q * 8 + 4 * i, v[i]);
-            else st16<kOutPol>(r, q * 8 + 2 * i, (v[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu);
+            if (E == 4) st32<kOutPol>(r, in_range(ok, q * 8 + 4 * i), v[i]);
+            else st16<kOutPol>(r, in_range(ok, q * 8 + 2 * i), (v[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu);
         }
     }
 
     __device__ static bool lines_ok(const u32x4 &l, uint32_t tag) { return l[1] == tag && l[3] == tag; }
 
+    // One group's arithmetic and stores; ok = false sends every access out
+    // of range (a lane past the end of the message).
+    __device__ static void group(Rsrc rout, Rsrc wo, uint32_t q, bool ok, uint32_t valid, uint32_t ng,
+                                 u32x2 in, const u32x4 *rs, const u32x4 &ag, uint32_t tag_out)
+    {
+        float acc[G];
+        if (kSendRS || kReduceToY) {
+            if (E == 4) {
+                acc[0] = as_f32(in[0]);
+                acc[1] = as_f32(in[1]);
+            } else {
+                acc[0] = bf16_lo(in[0]);
+                acc[1] = bf16_hi(in[0]);
+                acc[2] = bf16_lo(in[1]);
+                acc[3] = bf16_hi(in[1]);
+            }
+            if (kRecvRS) {
+                for (uint32_t v = 0; v < RSV; ++v) {
+                    acc[2 * v] = as_f32(rs[v][0]) + acc[2 * v];
+                    acc[2 * v + 1] = as_f32(rs[v][2]) + acc[2 * v + 1];
+                }
+            }
+        }
+        if (kSendRS) {
+            for (uint32_t v = 0; v < RSV; ++v) {
+                u32x4 o = {as_u32(acc[2 * v]), tag_out, as_u32(acc[2 * v + 1]), tag_out};
+                st128<kFifoSt>(wo, in_range(ok, wide_off(q, v, RSV, ng)), o);
+            }
+        }
+        u32x2 y;
+        if (kReduceToY) {
+            if (E == 4) y = u32x2{as_u32(acc[0]), as_u32(acc[1])};
+            else y = u32x2{pack_bf16(acc[0], acc[1]), pack_bf16(acc[2], acc[3])};
+        } else if (kCopyInToY) {
+            y = in;
+        } else {
+            y = u32x2{ag[0], ag[2]};
+        }
+        if (kWriteOut) {
+            if (valid == G) st64<kOutPol>(rout, in_range(ok, q * 8), y);
+            else store_part(rout, q, y, valid, ok);
+        }
+        if (kSendAG) st128<kFifoSt>(wo, in_range(ok, q * 16), u32x4{y[0], tag_out, y[1], tag_out});
+    }
+
+    // Full groups go in batches of U per lane as straight-line code (lanes
+    // past the end use out-of-range offsets); a partial last group is done
+    // afterwards by one lane, with its own poll.
     __device__ static bool run(const RingArgs &a, const char *src, char *dst, const char *rslot,
                                char *wslot, uint32_t len, uint32_t tag_in, uint32_t tag_out)
     {
         const uint32_t lane = step_lane();
-        const uint32_t ng = (len + G - 1) / G;
+        const uint32_t nfg = len / G, rem = len % G;
+        const uint32_t ng = nfg + (rem ? 1u : 0u);
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
         const Rsrc wi = make_rsrc(rslot, a.slot_bytes);
         const Rsrc wo = make_rsrc(wslot, a.slot_bytes);
-        for (uint32_t base = 0; base < ng; base += 64 * U) {
+        for (uint32_t base = 0; base < nfg; base += 64 * U) {
             u32x2 in[U];
             u32x4 rs[U][RSV], ag[U];
-            uint32_t valid[U];
 #pragma unroll
             for (int t = 0; t < U; ++t) {
                 const uint32_t q = base + 64 * t + lane;
-                valid[t] = q < ng ? (len - q * G < G ? len - q * G : G) : 0;
-                if (valid[t]) {
-                    if (kLoadIn) in[t] = load_in(rin, q, valid[t]);
-                    if (kRecvRS)
-                        for (uint32_t v = 0; v < RSV; ++v) rs[t][v] = ld128<kFifoLd>(wi, wide_off(q, v, RSV, ng));
-                    if (kRecvAG) ag[t] = ld128<kFifoLd>(wi, q * 16);
-                }
+                const bool ok = q < nfg;
+                if (kLoadIn) in[t] = ld64<kInPol>(rin, in_range(ok, q * 8));
+                if (kRecvRS)
+                    for (uint32_t v = 0; v < RSV; ++v)
+                        rs[t][v] = ld128<kFifoLd>(wi, in_range(ok, wide_off(q, v, RSV, ng)));
+                if (kRecvAG) ag[t] = ld128<kFifoLd>(wi, in_range(ok, q * 16));
             }
             if (kRecvRS || kRecvAG) {
-                // Spin until every line this wave needs carries the expected flag;
-                // only lanes with stale lines reload.
+                // Spin until every line this wave needs carries the expected
+                // flag, reloading all of them each time (a line that is
+                // already valid cannot change before this wave frees the slot).
                 Watchdog wd;
                 while (true) {
                     bool bad = false;
 #pragma unroll
                     for (int t = 0; t < U; ++t) {
-                        if (!valid[t]) continue;
+                        const bool ok = base + 64 * t + lane < nfg;
                         if (kRecvRS)
-                            for (uint32_t v = 0; v < RSV; ++v) bad |= !lines_ok(rs[t][v], tag_in);
-                        if (kRecvAG) bad |= !lines_ok(ag[t], tag_in);
+                            for (uint32_t v = 0; v < RSV; ++v) bad |= ok && !lines_ok(rs[t][v], tag_in);
+                        if (kRecvAG) bad |= ok && !lines_ok(ag[t], tag_in);
                     }
-                    if (!__any(bad)) break;
+                    if (!any_lane(bad)) break;
                     __builtin_amdgcn_s_sleep(1);
                     if (watchdog_expired(a, wd)) return false;
 #pragma unroll
                     for (int t = 0; t < U; ++t) {
                         const uint32_t q = base + 64 * t + lane;
-                        if (!valid[t]) continue;
+                        const bool ok = q < nfg;
                         if (kRecvRS)
                             for (uint32_t v = 0; v < RSV; ++v)
-                                if (!lines_ok(rs[t][v], tag_in)) rs[t][v] = ld128<kFifoLd>(wi, wide_off(q, v, RSV, ng));
-                        if (kRecvAG)
-                            if (!lines_ok(ag[t], tag_in)) ag[t] = ld128<kFifoLd>(wi, q * 16);
+                                rs[t][v] = ld128<kFifoLd>(wi, in_range(ok, wide_off(q, v, RSV, ng)));
+                        if (kRecvAG) ag[t] = ld128<kFifoLd>(wi, in_range(ok, q * 16));
                     }
                 }
             }
 #pragma unroll
             for (int t = 0; t < U; ++t) {
                 const uint32_t q = base + 64 * t + lane;
-                if (!valid[t]) continue;
-                float acc[G];
-                if (kSendRS || kReduceToY) {
-                    if (E == 4) {
-                        acc[0] = as_f32(in[t][0]);
-                        acc[1] = as_f32(in[t][1]);
-                    } else {
-                        acc[0] = bf16_lo(in[t][0]);
-                        acc[1] = bf16_hi(in[t][0]);
-                        acc[2] = bf16_lo(in[t][1]);
-                        acc[3] = bf16_hi(in[t][1]);
-                    }
-                    if (kRecvRS) {
-                        for (uint32_t v = 0; v < RSV; ++v) {
-                            acc[2 * v] = as_f32(rs[t][v][0]) + acc[2 * v];
-                            acc[2 * v + 1] = as_f32(rs[t][v][2]) + acc[2 * v + 1];
-                        }
-                    }
-                }
-                if (kSendRS) {
-                    for (uint32_t v = 0; v < RSV; ++v) {
-                        u32x4 o = {as_u32(acc[2 * v]), tag_out, as_u32(acc[2 * v + 1]), tag_out};
-                        st128<kFifoSt>(wo, wide_off(q, v, RSV, ng), o);
-                    }
-                }
-                u32x2 y;
-                if (kReduceToY) {
-                    if (E == 4) y = u32x2{as_u32(acc[0]), as_u32(acc[1])};
-                    else y = u32x2{pack_bf16(acc[0], acc[1]), pack_bf16(acc[2], acc[3])};
-                } else if (kCopyInToY) {
-                    y = in[t];
-                } else {
-                    y = u32x2{ag[t][0], ag[t][2]};
-                }
-                if (kWriteOut) store_out(rout, q, y, valid[t]);
-                if (kSendAG) st128<kFifoSt>(wo, q * 16, u32x4{y[0], tag_out, y[1], tag_out});
+                group(rout, wo, q, q < nfg, G, ng, in[t], rs[t], ag[t], tag_out);
             }
+        }
+        if (rem) {
+            // The whole wave runs this (no branch on the lane); only the lane
+            // of the partial group has its accesses in range.
+            const uint32_t q = nfg;
+            const bool me = lane == (nfg & 63u);
+            u32x2 in = {0, 0};
+            u32x4 rs[RSV], ag = {0, 0, 0, 0};
+            if (kLoadIn) in = load_part(rin, q, rem, me);
+            if (kRecvRS || kRecvAG) {
+                Watchdog wd;
+                while (true) {
+                    bool bad = false;
+                    if (kRecvRS)
+                        for (uint32_t v = 0; v < RSV; ++v) {
+                            rs[v] = ld128<kFifoLd>(wi, in_range(me, wide_off(q, v, RSV, ng)));
+                            bad |= me && !lines_ok(rs[v], tag_in);
+                        }
+                    if (kRecvAG) {
+                        ag = ld128<kFifoLd>(wi, in_range(me, q * 16));
+                        bad |= me && !lines_ok(ag, tag_in);
+                    }
+                    if (!any_lane(bad)) break;
+                    __builtin_amdgcn_s_sleep(1);
+                    if (watchdog_expired(a, wd)) return false;
+                }
+            }
+            group(rout, wo, q, me, rem, ng, in, rs, ag, tag_out);
         }
         return true;
     }
@@ -730,7 +827,7 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
         // no read of the slot is outstanding: free it at once, without
         // waiting for this step's own stores (compiler ordering only).
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        if (lane_id() == 0) flag_store(g.head_in, g.m_in + 1);
+        flag_store(g.head_in, g.m_in + 1);
         advance_in(g);
     }
     return true;
@@ -1021,7 +1118,7 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
     if (send) advance_out(g);
     if (recv) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        if (lane_id() == 0) flag_store(g.head_in, g.m_in + 1);
+        flag_store(g.head_in, g.m_in + 1);
         advance_in(g);
     }
     return true;
@@ -1161,9 +1258,9 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
     const uint64_t epoch = uniform64(flag_load(epoch_p));
     g.head_seen = uniform64(flag_load(g.head_out));
     after_observe();
-    if (lane_id() == 0) {
+    {
         // messages per chunk: 2N-2 (AllReduce) or N-1, one fewer when a
-        // reduction chain starts with a peer read
+        // reduction chain starts with a peer read (stored by every lane)
         const uint64_t per_chunk = (a.coll == AR_COLL_ALLREDUCE ? 2 * N - 2 : N - 1) -
                                    (DAG && a.coll != AR_COLL_ALLGATHER ? 1 : 0);
         flag_store(epoch_p, epoch + (uint64_t)a.nchunks * per_chunk);
