@@ -40,10 +40,13 @@ struct RingArgs {
     uint64_t cs;                     // per-channel sub-range of a segment
     uint64_t chunk;                  // per-(segment, channel) ring step
     uint64_t kw;                     // one wave's share of a chunk step
+    uint64_t part;                   // elements of segment full_segs (0 .. seg-1)
     uint64_t slot_bytes;             // bytes of one FIFO slot
     uint64_t timeout_ticks;          // watchdog, in 100 MHz real-time ticks
     uint32_t nranks, nchannels, nwaves, depth, nchunks, placement, debug;
     uint32_t coll;                   // AR_COLL_*: which steps of the ring run
+    uint32_t full_segs;              // segments 0 .. full_segs-1 hold seg elements; segment
+                                     // full_segs holds part, any later one none
 };
 
 // Resolved plan geometry.  Computed on the host only.

@@ -1159,21 +1159,37 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
     const uint32_t k0 = peer_start ? 1u : 0u;
     uint32_t s0 = coll == AR_COLL_REDUCESCATTER ? (r + N - 1) % N : r;
     if (peer_start) s0 = s0 == 0 ? N - 1 : s0 - 1;
+    // A wave's elements of chunk j sit at the same offset (rel) inside every
+    // segment; only the segment base and, for the one partial segment and
+    // the empty ones after it, the length change from step to step.  So the
+    // clamps are done once per chunk and a step costs a few scalar ops.
+    const uint64_t last_lo = (uint64_t)(N - 1) * a.seg;
+    const uint64_t c_lo = (uint64_t)c * a.cs;
     for (uint32_t j = 0; j < a.nchunks; ++j) {
+        const uint64_t ck_lo = c_lo + (uint64_t)j * a.chunk;
+        const uint64_t rel = ck_lo + (uint64_t)w * a.kw;
+        uint64_t hi = c_lo + a.cs;
+        if (ck_lo + a.chunk < hi) hi = ck_lo + a.chunk;
+        if (rel + a.kw < hi) hi = rel + a.kw;
+        const uint64_t hi_full = hi < a.seg ? hi : a.seg;
+        const uint64_t hi_part = hi < a.part ? hi : a.part;
+        const uint32_t len_full = hi_full > rel ? (uint32_t)(hi_full - rel) : 0u;
+        const uint32_t len_part = hi_part > rel ? (uint32_t)(hi_part - rel) : 0u;
         uint32_t s = s0;
-        for (uint32_t k = k0; k < nsteps; ++k, s = s == 0 ? N - 1 : s - 1) {
-            const uint64_t seg_lo = (uint64_t)s * a.seg;
-            const uint64_t seg_hi = seg_lo + a.seg < a.count ? seg_lo + a.seg : a.count;
-            const uint64_t ch_lo = seg_lo + (uint64_t)c * a.cs;
-            uint64_t hi = ch_lo + a.cs < seg_hi ? ch_lo + a.cs : seg_hi;
-            const uint64_t ck_lo = ch_lo + (uint64_t)j * a.chunk;
-            if (ck_lo + a.chunk < hi) hi = ck_lo + a.chunk;
-            const uint64_t lo = ck_lo + (uint64_t)w * a.kw;
-            if (lo + a.kw < hi) hi = lo + a.kw;
-            const uint32_t len = hi > lo ? (uint32_t)(hi - lo) : 0u;
+        uint64_t seg_lo = (uint64_t)s0 * a.seg;
+        for (uint32_t k = k0; k < nsteps; ++k) {
+            const uint32_t len = s < a.full_segs ? len_full : (s == a.full_segs ? len_part : 0u);
+            const uint64_t lo = seg_lo + rel;
             // ReduceScatter writes, and AllGather reads, one block-sized buffer.
-            const uint64_t in_e = hi > lo ? (coll == AR_COLL_ALLGATHER ? lo - seg_lo : lo) : 0;
-            const uint64_t out_e = hi > lo ? (coll == AR_COLL_REDUCESCATTER ? lo - seg_lo : lo) : 0;
+            const uint64_t in_e = len ? (coll == AR_COLL_ALLGATHER ? rel : lo) : 0;
+            const uint64_t out_e = len ? (coll == AR_COLL_REDUCESCATTER ? rel : lo) : 0;
+            if (s == 0) {
+                s = N - 1;
+                seg_lo = last_lo;
+            } else {
+                --s;
+                seg_lo -= a.seg;
+            }
             const char *s_ptr = src + in_e * E;
             char *d_ptr = dst + out_e * E;
             char *p_ptr = DAG ? peer + out_e * E : nullptr;

@@ -143,6 +143,12 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
     a.ctl = p->ctl;
     a.count = g.coll == AR_COLL_ALLREDUCE ? g.count : g.count * (uint64_t)g.nranks;
     a.seg = g.seg_elems;
+    {
+        uint64_t full = a.seg ? a.count / a.seg : 0;
+        if (full > (uint64_t)g.nranks) full = (uint64_t)g.nranks;
+        a.full_segs = (uint32_t)full;
+        a.part = full < (uint64_t)g.nranks ? a.count - full * a.seg : 0;
+    }
     a.coll = (uint32_t)g.coll;
     a.cs = g.chan_elems;
     a.chunk = g.chunk_elems;
