@@ -127,7 +127,10 @@ typedef struct ar_plan_desc {
     int nchannels;         /* 1 .. AR_MAX_CHANNELS; 0 asks the tuner */
     size_t chunk_bytes;    /* data bytes per ring step per (segment, channel);
                               0 asks the tuner / default */
-    int fifo_depth;        /* FIFO slots per connection (2..16); 0 = default */
+    int fifo_depth;        /* FIFO slots per connection (2..16); 0 = default:
+                              2 (Simple) or 4 (LL, LL128), doubled up to 16
+                              while a run has more messages than slots and
+                              the FIFO stays within 4 MiB */
     int nwaves;            /* wavefronts per workgroup (1..AR_MAX_WAVES); 0 = default */
     int placement;         /* AR_PLACE_* */
     uint32_t timeout_us;   /* watchdog per flag wait; 0 = default (2 s) */

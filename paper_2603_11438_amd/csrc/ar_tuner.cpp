@@ -180,6 +180,8 @@ int default_nwaves(int proto)
 }
 
 int default_depth(int proto) { return proto == AR_PROTO_SIMPLE ? 2 : 4; }
+constexpr int kMaxDepth = 16;
+constexpr uint64_t kSmallFifoBytes = 4ull << 20;
 
 // Direct algorithm: units (16 bytes of data) per thread per iteration, and
 // the largest grid it is sized to (8 workgroups per CU on 256 CUs).
@@ -250,7 +252,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     if (d->dtype != AR_FLOAT32 && d->dtype != AR_BFLOAT16) return AR_ERR_ARG;
     if (d->proto != AR_PROTO_AUTO && !valid_proto(d->proto)) return AR_ERR_ARG;
     if (d->nchannels < 0 || d->nchannels > AR_MAX_CHANNELS) return AR_ERR_ARG;
-    if (d->fifo_depth != 0 && (d->fifo_depth < 2 || d->fifo_depth > 16)) return AR_ERR_ARG;
+    if (d->fifo_depth != 0 && (d->fifo_depth < 2 || d->fifo_depth > kMaxDepth)) return AR_ERR_ARG;
     if (d->nwaves < 0 || d->nwaves > AR_MAX_WAVES) return AR_ERR_ARG;
     if (d->direct_unroll < 0 || d->direct_unroll > 2) return AR_ERR_ARG;
     if (d->placement != AR_PLACE_RANK_SPREAD && d->placement != AR_PLACE_CHANNEL_LOCAL) return AR_ERR_ARG;
@@ -306,7 +308,6 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     // Ring workgroups wait on each other, so they must all be resident.
     if (d->nchannels > max_channels) return AR_ERR_OCCUPANCY;
     chunk = clamp_chunk(chunk);
-    const int depth = d->fifo_depth ? d->fifo_depth : default_depth(proto);
 
     ar_plan_info g = {};
     g.algo = AR_ALGO_RING;
@@ -316,7 +317,6 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     g.proto = proto;
     g.nchannels = nch;
     g.nwaves = nw;
-    g.fifo_depth = depth;
     g.placement = d->placement;
     g.count = d->count;
     g.block = 64 * nw;
@@ -349,13 +349,26 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     }
     g.slot_bytes = round_up(slot, 256);
     const uint64_t conns = (uint64_t)nch * N * (uint64_t)nw;
-    g.fifo_bytes = conns * (uint64_t)depth * g.slot_bytes;
-    g.flag_bytes = conns * kConnFlagU64 * 8 + kCtlU32 * 4;
     // Messages per connection: 2N-2 per chunk (AllReduce) or N-1; with the
     // peer-direct Simple ring a reduction chain starts with a peer read, one
     // message fewer.
     g.msgs_per_run = g.nchunks * ((d->coll == AR_COLL_ALLREDUCE ? 2 * N - 2 : N - 1) -
                                   (g.peer_direct && d->coll != AR_COLL_ALLGATHER ? 1 : 0));
+    // Default depth: the protocol's, doubled (up to kMaxDepth) while a run
+    // has more messages than slots and the FIFO stays within
+    // kSmallFifoBytes.  A latency-bound run then finds its slots free from
+    // the head value read at kernel start instead of reading the receiver's
+    // head counter again, a round trip, every few messages.
+    int depth = d->fifo_depth;
+    if (depth == 0) {
+        depth = default_depth(proto);
+        while (depth < kMaxDepth && (uint64_t)depth < g.msgs_per_run &&
+               conns * (uint64_t)(2 * depth) * g.slot_bytes <= kSmallFifoBytes)
+            depth *= 2;
+    }
+    g.fifo_depth = depth;
+    g.fifo_bytes = conns * (uint64_t)depth * g.slot_bytes;
+    g.flag_bytes = conns * kConnFlagU64 * 8 + kCtlU32 * 4;
 
     // Wire bytes actually written per run.  AllReduce: each element crosses
     // 2(N-1) links, N-1 as an fp32 partial and N-1 as a finished value;

@@ -316,6 +316,31 @@ def test_direct_allgather_mode_in_geometry():
     assert ar.lib().ar_plan_geometry(ctypes.byref(d), ctypes.byref(ar.ar_plan_info())) == ar.AR_ERR_ARG
 
 
+def test_default_fifo_depth_deepens_small_runs():
+    """Without an explicit depth a run with more messages than slots gets a
+    deeper FIFO (up to 16) while the FIFO stays within 4 MiB; large runs keep
+    the protocol's depth; an explicit depth is kept as given."""
+    def geom(count, proto, nch, depth=0):
+        return ar.ar_plan_geometry(ar.make_desc(8, count, "f32", proto, nch, 0, fifo_depth=depth, algo="ring"))
+    for proto, base in (("simple", 2), ("ll", 4), ("ll128", 4)):
+        small = geom(1024, proto, 1)
+        assert small["fifo_depth"] == 16 and small["msgs_per_run"] <= 16
+        big = geom(1 << 25, proto, 64)
+        assert big["fifo_depth"] == base
+        assert geom(1024, proto, 1, depth=3)["fifo_depth"] == 3
+        for g in (small, big):
+            conns = g["nchannels"] * 8 * g["nwaves"]
+            assert g["fifo_bytes"] == conns * g["fifo_depth"] * g["slot_bytes"]
+            # deepened only while the doubled FIFO fits the budget
+            if g["fifo_depth"] > base:
+                assert g["fifo_bytes"] <= 4 << 20
+    # a run whose messages already fit keeps the protocol's depth (2 ranks:
+    # 2 LL messages, 1 peer-direct Simple message per run)
+    for proto, base in (("simple", 2), ("ll", 4)):
+        g = ar.ar_plan_geometry(ar.make_desc(2, 1024, "f32", proto, 1, 0, algo="ring"))
+        assert g["msgs_per_run"] <= base and g["fifo_depth"] == base
+
+
 # ------------------------------------------------------------- algorithms
 
 def test_direct_geometry_and_algorithm_choice():
