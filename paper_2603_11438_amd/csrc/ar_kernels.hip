@@ -1327,19 +1327,24 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
     if (seg_lo >= a.count) return;
     const uint64_t seg_hi = seg_lo + a.seg < a.count ? seg_lo + a.seg : a.count;
     const uint64_t len = seg_hi - seg_lo;
-    const uint32_t nfull = (uint32_t)(len / A), rem = (uint32_t)(len % A);
+    const uint64_t nfull_all = len / A;
+    const uint32_t rem = (uint32_t)(len % A);
     const uint32_t tid = threadIdx.x, nth = blockDim.x;
 
     // Rank j of the chain is rank (first + j) mod N.  AllGather reads a
     // block-sized source, ReduceScatter writes a block-sized destination.
-    auto in_rsrc = [&](uint32_t j) {
+    // A descriptor covers `bytes` from byte `off` of the segment: buffer
+    // offsets are 32-bit, so a segment is walked in windows of kWinUnits
+    // units (one window up to 1 GiB per segment).
+    auto in_rsrc = [&](uint32_t j, uint64_t off, uint64_t bytes) {
         const uint32_t r = (first + j) % N;
-        return make_rsrc(a.src[r] + (coll == AR_COLL_ALLGATHER ? 0 : seg_lo * E), len * E);
+        return make_rsrc(a.src[r] + (coll == AR_COLL_ALLGATHER ? 0 : seg_lo * E) + off, bytes);
     };
-    auto out_rsrc = [&](uint32_t i) {
+    auto out_rsrc = [&](uint32_t i, uint64_t off, uint64_t bytes) {
         const uint32_t r = coll == AR_COLL_REDUCESCATTER ? s : i;
-        return make_rsrc(a.dst[r] + (coll == AR_COLL_REDUCESCATTER ? 0 : seg_lo * E), len * E);
+        return make_rsrc(a.dst[r] + (coll == AR_COLL_REDUCESCATTER ? 0 : seg_lo * E) + off, bytes);
     };
+    constexpr uint64_t kWinUnits = 1ull << 26;
 
     auto chain = [&](const u32x4 *v, float *acc) {
         if (E == 4) {
@@ -1374,38 +1379,42 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
         return y;
     };
 
-    for (uint32_t base = part * nth * U; base < nfull; base += parts * nth * U) {
-        u32x4 v[U][NMAX];
+    for (uint64_t w0 = 0; w0 < nfull_all; w0 += kWinUnits) {
+        const uint32_t nfull = (uint32_t)(nfull_all - w0 < kWinUnits ? nfull_all - w0 : kWinUnits);
+        const uint64_t woff = w0 * 16, wbytes = (uint64_t)nfull * 16;
+        for (uint32_t base = part * nth * U; base < nfull; base += parts * nth * U) {
+            u32x4 v[U][NMAX];
 #pragma unroll
-        for (int j = 0; j < NMAX; ++j) {
-            if ((uint32_t)j < nsrc) {
-                const Rsrc rin = in_rsrc(j);
+            for (int j = 0; j < NMAX; ++j) {
+                if ((uint32_t)j < nsrc) {
+                    const Rsrc rin = in_rsrc(j, woff, wbytes);
 #pragma unroll
-                for (int t = 0; t < U; ++t) {
-                    const uint32_t u = base + t * nth + tid;
-                    if (u < nfull) v[t][j] = ld128<kInPol>(rin, u * 16);
+                    for (int t = 0; t < U; ++t) {
+                        const uint32_t u = base + t * nth + tid;
+                        v[t][j] = ld128<kInPol>(rin, in_range(u < nfull, u * 16));
+                    }
                 }
             }
-        }
-        u32x4 y[U];
+            u32x4 y[U];
 #pragma unroll
-        for (int t = 0; t < U; ++t) {
-            if (coll == AR_COLL_ALLGATHER) {
-                y[t] = v[t][0];  // a copy keeps every bit, NaN payloads included
-            } else {
-                float acc[A];
-                chain(v[t], acc);
-                y[t] = narrow(acc);
+            for (int t = 0; t < U; ++t) {
+                if (coll == AR_COLL_ALLGATHER) {
+                    y[t] = v[t][0];  // a copy keeps every bit, NaN payloads included
+                } else {
+                    float acc[A];
+                    chain(v[t], acc);
+                    y[t] = narrow(acc);
+                }
             }
-        }
 #pragma unroll
-        for (int r = 0; r < NMAX; ++r) {
-            if ((uint32_t)r < nout) {
-                const Rsrc rout = out_rsrc(r);
+            for (int r = 0; r < NMAX; ++r) {
+                if ((uint32_t)r < nout) {
+                    const Rsrc rout = out_rsrc(r, woff, wbytes);
 #pragma unroll
-                for (int t = 0; t < U; ++t) {
-                    const uint32_t u = base + t * nth + tid;
-                    if (u < nfull) st128<kOutPol>(rout, u * 16, y[t]);
+                    for (int t = 0; t < U; ++t) {
+                        const uint32_t u = base + t * nth + tid;
+                        st128<kOutPol>(rout, in_range(u < nfull, u * 16), y[t]);
+                    }
                 }
             }
         }
@@ -1418,12 +1427,12 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
         for (int j = 0; j < NMAX; ++j) {
             u32x4 x = {0, 0, 0, 0};
             if ((uint32_t)j < nsrc) {
-                const Rsrc rin = in_rsrc(j);
+                const Rsrc rin = in_rsrc(j, nfull_all * 16, (uint64_t)rem * E);
 #pragma unroll
                 for (int i = 0; i < (int)A; ++i) {
                     if ((uint32_t)i < rem) {
-                        if (E == 4) x[i] = ld32<kInPol>(rin, nfull * 16 + 4 * i);
-                        else x[i >> 1] |= ld16<kInPol>(rin, nfull * 16 + 2 * i) << ((i & 1) * 16);
+                        if (E == 4) x[i] = ld32<kInPol>(rin, 4 * i);
+                        else x[i >> 1] |= ld16<kInPol>(rin, 2 * i) << ((i & 1) * 16);
                     }
                 }
             }
@@ -1438,12 +1447,12 @@ __global__ __launch_bounds__(1024) void direct_kernel(RingArgs a)
 #pragma unroll
         for (int r = 0; r < NMAX; ++r) {
             if ((uint32_t)r < nout) {
-                const Rsrc rout = out_rsrc(r);
+                const Rsrc rout = out_rsrc(r, nfull_all * 16, (uint64_t)rem * E);
 #pragma unroll
                 for (int i = 0; i < (int)A; ++i) {
                     if ((uint32_t)i < rem) {
-                        if (E == 4) st32<kOutPol>(rout, nfull * 16 + 4 * i, y[i]);
-                        else st16<kOutPol>(rout, nfull * 16 + 2 * i, (y[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu);
+                        if (E == 4) st32<kOutPol>(rout, 4 * i, y[i]);
+                        else st16<kOutPol>(rout, 2 * i, (y[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu);
                     }
                 }
             }
