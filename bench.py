@@ -135,6 +135,8 @@ def main(argv=None) -> int:
     ap.add_argument("--fifo-only", type=int, default=0,
                     help="Simple ring: all-gather through the FIFOs instead of direct writes")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU-baseline budget (0 = skip)")
+    ap.add_argument("--copy-reference", type=int, default=1024,
+                    help="also time the library's streaming copy of this many MiB (0 = skip)")
     ap.add_argument("--calibrate-copy", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args(argv)
@@ -266,10 +268,36 @@ def main(argv=None) -> int:
                  "roofline": roofline_of(dinfo, dms),
                  "note": "two-shot direct algorithm on the same input: same result bits, compulsory bytes only"}
 
+    copy_ref = None
+    if args.copy_reference:
+        # What one kernel that only streams reads and writes reaches on this
+        # box: the practical ceiling beside the published 8 TB/s.
+        nb = args.copy_reference << 20
+        src = torch.empty(nb // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        cp = ar.Plan(1, nb // 4, "f32", proto="simple", nchannels=1)
+        for _ in range(3):
+            cp.run_oop([src], [dst])
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        c0.record(stream)
+        for _ in range(10):
+            cp.run_oop([src], [dst])
+        c1.record(stream)
+        torch.cuda.synchronize()
+        cms = c0.elapsed_time(c1) / 10
+        cp.destroy()
+        del src, dst
+        copy_ref = {"bytes_read": nb, "bytes_written": nb, "ms": round(cms, 4),
+                    "gbs": round(2 * nb / (cms / 1e3) / 1e9, 1),
+                    "frac_of_peak": round(2 * nb / (cms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+
     t = ms / 1e3
     busbw = ar.bus_bandwidth(s_bytes, t, n)
     algbw = ar.alg_bandwidth(s_bytes, t)
     roofline = roofline_of(info, ms)
+    if copy_ref:
+        roofline["copy_reference"] = copy_ref
 
     cpu = None
     if args.cpu_seconds > 0:

@@ -104,3 +104,29 @@ def test_allgather_block_beyond_4gib(ar):
         _check(recv[r], f"{label} rank {r}")
     del recv
     torch.cuda.empty_cache()
+
+
+def test_one_rank_copies(ar):
+    """One rank: every collective is a copy of its one block, out of place;
+    small and ragged sizes (tail bytes) and a copy over two 1 GiB windows."""
+    import torch
+
+    cases = [(c, dt) for c in (1, 3, 4, 5, 8, 12345) for dt in ("f32", "bf16")] + [((1 << 28) + 3, "f32")]
+    for count, dtype in cases:
+        tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+        for coll in ("allreduce", "reducescatter", "allgather"):
+            if coll != "allreduce" and count % (4 if dtype == "f32" else 8):
+                continue
+            label = f"one rank {coll} count={count} {dtype}"
+            say(label)
+            src = torch.randn(count, device="cuda:0").to(tdt)
+            dst = torch.full((count,), float("nan"), device="cuda:0").to(tdt)
+            plan = ar.Plan(1, count, dtype, coll=coll)
+            plan.run_oop([src], [dst])
+            torch.cuda.synchronize()
+            assert plan.status() == ar.AR_OK
+            plan.destroy()
+            assert torch.equal(src.view(torch.int16 if dtype == "bf16" else torch.int32),
+                               dst.view(torch.int16 if dtype == "bf16" else torch.int32)), label
+            del src, dst
+    torch.cuda.empty_cache()
