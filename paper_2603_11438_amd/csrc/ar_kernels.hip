@@ -1,6 +1,9 @@
 // Ring AllReduce kernels for gfx950 (MI355X): reduce-scatter then
 // all-gather around a ring of N simulated ranks whose buffers all live in
-// one GPU's memory, under one of three protocols (LL, LL128, Simple).
+// one GPU's memory, under one of three protocols (LL, LL128, Simple); the
+// same ring runs ReduceScatter and AllGather alone.  Also here: the direct
+// (two-shot) algorithm, which reads every rank's segment and writes the sum
+// to every rank with no FIFOs, and the streaming copy of the one-rank case.
 //
 // Work decomposition.  Grid = nchannels * nranks workgroups; workgroup
 // (channel c, rank r) holds `nwaves` wavefronts and each wavefront is an
@@ -18,18 +21,23 @@
 //   k = N-1       recv + own input -> y; write y, send y  (recvReduceCopySend)
 //   N-1 < k < 2N-2  recv y; write y, send y     (recvCopySend)
 //   k = 2N-2      recv y; write y               (recvCopy)
-// so segment s is summed x_s + x_{s+1} + ... + x_{s+N-1} in that order.
+// so segment s is summed x_s + x_{s+1} + ... + x_{s+N-1} in that order.  In
+// the Simple ring's peer-direct mode step 0 becomes a read of the chain
+// start's input by the second rank, and all-gather chunks are written into
+// the next rank's output instead of a FIFO slot.
 //
 // Memory model.  A FIFO slot written by one wave is read by a wave that can
 // sit on another XCD, i.e. behind another L2.  Every FIFO access therefore
 // uses the device-scope coherence bit (sc1) -- the same encoding the
 // compiler uses for device-scope atomic loads and stores on this target --
-// and every counter is a device-scope atomic.  A sender makes its slot
-// writes complete (s_waitcnt vmcnt(0)) before it stores the counter or
-// flag that publishes them; a receiver issues its slot reads only after it
-// has observed that counter or flag.  Inputs and outputs are plain accesses:
-// each rank touches only its own buffers, from the same wave, in program
-// order (the read of an element always precedes the write of its result).
+// and every counter is a device-scope atomic.  A Simple or LL128 sender
+// makes its data writes complete (s_waitcnt vmcnt(0)) before it stores the
+// counter or flags that publish them; an LL line carries its own flag.  A
+// receiver issues its slot reads only after it has observed the counter or
+// flag.  Rank inputs are read with the non-temporal hint: nothing writes an
+// input before every read of it.  Rank outputs are written non-temporally
+// by their own rank, except in the peer-direct mode, where a neighbour on
+// another XCD also writes them, so every output access there uses sc1.
 //
 // Every wait is bounded by a watchdog on the 100 MHz real-time counter; a
 // wave that times out raises the plan's abort word and status bit, and all

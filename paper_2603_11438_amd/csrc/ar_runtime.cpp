@@ -269,6 +269,8 @@ int ar_run(ar_plan_t *plan, void *const *bufs, void *stream)
     // ReduceScatter / AllGather in place: the block of rank r sits at r*count.
     const int n = plan->info.nranks;
     const size_t blk = plan->info.count * (plan->info.dtype == AR_FLOAT32 ? 4 : 2);
+    // Empty blocks: a no-op whatever the pointers (as for AllReduce).
+    if (blk == 0) return run_impl(plan, (const void *const *)bufs, bufs, stream);
     const void *send[AR_MAX_RANKS];
     void *recv[AR_MAX_RANKS];
     for (int r = 0; r < n; ++r) {

@@ -472,3 +472,27 @@ def test_direct_out_of_place_and_repeats(ar):
     for r in range(n):
         assert np.array_equal(to_bits(send[r], "f32"), x[r].view(np.uint32))
     plan.destroy()
+
+
+def test_empty_runs_are_no_ops(ar):
+    """count = 0: every algorithm and collective accepts empty buffers,
+    launches nothing and leaves the plan's status clean; a real run
+    afterwards is unaffected."""
+    import torch
+
+    for n in (2, 8):
+        for cfg in (dict(proto="simple", nchannels=2), dict(proto="ll", nchannels=2),
+                    dict(proto="ll128", nchannels=2), dict(algo="direct")):
+            for coll in ("allreduce", "reducescatter", "allgather"):
+                label = f"empty N={n} {coll} {cfg}"
+                say(label)
+                plan = ar.Plan(n, 0, "f32", coll=coll, **cfg)
+                assert plan.info["grid"] == 0, label
+                bufs = [torch.empty(0, device="cuda:0") for _ in range(n)]
+                plan.run(bufs)
+                plan.run_oop(bufs, [torch.empty(0, device="cuda:0") for _ in range(n)])
+                torch.cuda.synchronize()
+                assert plan.status() == ar.AR_OK, label
+                plan.destroy()
+    x = draw(8, 4099, "f32", "normal", seed=3)
+    run_case(ar, x, "f32", "after empty runs", proto="simple", nchannels=2)
