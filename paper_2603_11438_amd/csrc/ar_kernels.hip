@@ -585,7 +585,7 @@ struct SimpleStep {
 // dst: this step's elements in the own output; peer_dst: the same elements
 // in the next rank's output (DAG all-gather sends); peer_src: the same
 // elements of the previous rank's input (peer-direct chain starts).
-template <int DT, int KIND, bool DAG>
+template <int DT, int KIND, bool DAG, bool DBG>
 __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst, char *peer_dst,
                                             const char *peer_src, uint32_t len)
 {
@@ -617,8 +617,8 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
     // Slot writes (and slot reads) complete before either counter moves.
     drain_vmem();
     if (send) {
-        debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
-        if (!skip_this_post(g)) flag_store(g.tail_out, g.m_out + 1);
+        if constexpr (DBG) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
+        if (!(DBG && skip_this_post(g))) flag_store(g.tail_out, g.m_out + 1);
         advance_out(g);
     }
     if (recv) {
@@ -810,7 +810,7 @@ struct LLStep {
     }
 };
 
-template <int DT, int KIND>
+template <int DT, int KIND, bool DBG>
 __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uint32_t len)
 {
     const RingArgs &a = *g.a;
@@ -823,10 +823,11 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
         if (!acquire_send_slot(g)) return false;
         wslot = slot_ptr(g.fifo_out, g.slot_out, a);
     }
-    if (send) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
+    if constexpr (DBG)
+        if (send) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
     // A skipped post writes the lines with the previous message's flag, which
     // the receiver never accepts for this message.
-    const bool skip = send && skip_this_post(g);
+    const bool skip = DBG && send && skip_this_post(g);
     const uint32_t tag_out = ll_tag(skip ? g.m_out - 1 : g.m_out);
     if (!LLStep<DT, KIND>::run(a, src, dst, rslot, wslot, len, ll_tag(g.m_in), tag_out)) return false;
     if (send) advance_out(g);
@@ -1103,7 +1104,7 @@ struct LL128Step {
 
 constexpr uint32_t kLdsWordsPerWave = 240;  // 480 bf16 values
 
-template <int DT, int KIND>
+template <int DT, int KIND, bool DBG>
 __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, uint32_t len, uint32_t *lds)
 {
     const RingArgs &a = *g.a;
@@ -1118,8 +1119,9 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
         if (!acquire_send_slot(g)) return false;
         wslot = slot_ptr(g.fifo_out, (uint32_t)(g.m_out % a.depth), a);
     }
-    if (send) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
-    const bool skip = send && skip_this_post(g);
+    if constexpr (DBG)
+        if (send) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
+    const bool skip = DBG && send && skip_this_post(g);
     // A skipped post: write the data but a flag from the previous message.
     const uint64_t tag_out = skip ? g.m_out : g.m_out + 1;
     if (!LL128Step<DT, KIND>::run(a, src, dst, rslot, wslot, len, g.m_in + 1, tag_out, lds)) return false;
@@ -1134,17 +1136,17 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
 
 // ===================================================================== kernel
 
-template <int PROTO, int DT, bool DAG, int KIND>
+template <int PROTO, int DT, bool DAG, bool DBG, int KIND>
 __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, char *peer_dst, const char *peer_src,
                                         uint32_t len, uint32_t *lds)
 {
-    if (PROTO == AR_PROTO_SIMPLE) return simple_step<DT, KIND, DAG>(g, src, dst, peer_dst, peer_src, len);
-    if (PROTO == AR_PROTO_LL) return ll_step<DT, KIND>(g, src, dst, len);
-    return ll128_step<DT, KIND>(g, src, dst, len, lds);
+    if (PROTO == AR_PROTO_SIMPLE) return simple_step<DT, KIND, DAG, DBG>(g, src, dst, peer_dst, peer_src, len);
+    if (PROTO == AR_PROTO_LL) return ll_step<DT, KIND, DBG>(g, src, dst, len);
+    return ll128_step<DT, KIND, DBG>(g, src, dst, len, lds);
 }
 
 // All steps of one run for one wave; false if the wave had to give up.
-template <int PROTO, int DT, bool DAG>
+template <int PROTO, int DT, bool DAG, bool DBG>
 __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
 {
     constexpr uint32_t E = Elem<DT>::E;
@@ -1206,29 +1208,29 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
             if constexpr (DAG) {
                 if (peer_start && k == 1) {
                     if (coll == AR_COLL_ALLREDUCE && N == 2)
-                        ok = do_step<PROTO, DT, DAG, kPeerReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                        ok = do_step<PROTO, DT, DAG, DBG, kPeerReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
                     else if (N == 2)
-                        ok = do_step<PROTO, DT, DAG, kPeerReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                        ok = do_step<PROTO, DT, DAG, DBG, kPeerReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
                     else
-                        ok = do_step<PROTO, DT, DAG, kPeerReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                        ok = do_step<PROTO, DT, DAG, DBG, kPeerReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
                     if (!ok) return false;
                     continue;
                 }
             }
             if (coll == AR_COLL_ALLREDUCE) {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k == N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, DAG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k == N - 1) ok = do_step<PROTO, DT, DAG, DBG, kRecvReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, DAG, DBG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, DBG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             } else if (coll == AR_COLL_REDUCESCATTER) {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, kRecvReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, DBG, kRecvReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             } else {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, kCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, kCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, DBG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             }
             if (!ok) return false;
         }
@@ -1236,7 +1238,9 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
     return true;
 }
 
-template <int PROTO, int DT, bool DAG>
+// DBG: the debug hooks (AR_DEBUG_*) are compiled in; a plan without debug
+// flags runs the kernel without them, whose steps carry no test-only code.
+template <int PROTO, int DT, bool DAG, bool DBG>
 __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
 {
     __shared__ uint32_t lds_all[(PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? AR_MAX_WAVES * kLdsWordsPerWave : 1];
@@ -1299,7 +1303,7 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
     if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED,
                                                          __HIP_MEMORY_SCOPE_AGENT)) != 0)
         return;
-    ring_steps<PROTO, DT, DAG>(g, lds);
+    ring_steps<PROTO, DT, DAG, DBG>(g, lds);
 }
 
 // ===================================================================== direct
@@ -1517,16 +1521,19 @@ typedef void (*RingFn)(RingArgs);
 
 // dag: the Simple ring's direct all-gather (the other protocols always
 // carry the all-gather through their FIFOs).
-__host__ RingFn ring_fn(int proto, int dtype, bool dag)
+template <int DT, bool DBG>
+__host__ RingFn ring_fn_of(int proto, bool dag)
 {
-    if (dtype == AR_FLOAT32) {
-        if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, AR_FLOAT32, false>;
-        if (proto == AR_PROTO_LL128) return ring_kernel<AR_PROTO_LL128, AR_FLOAT32, false>;
-        return dag ? ring_kernel<AR_PROTO_SIMPLE, AR_FLOAT32, true> : ring_kernel<AR_PROTO_SIMPLE, AR_FLOAT32, false>;
-    }
-    if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, AR_BFLOAT16, false>;
-    if (proto == AR_PROTO_LL128) return ring_kernel<AR_PROTO_LL128, AR_BFLOAT16, false>;
-    return dag ? ring_kernel<AR_PROTO_SIMPLE, AR_BFLOAT16, true> : ring_kernel<AR_PROTO_SIMPLE, AR_BFLOAT16, false>;
+    if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, DT, false, DBG>;
+    if (proto == AR_PROTO_LL128) return ring_kernel<AR_PROTO_LL128, DT, false, DBG>;
+    return dag ? ring_kernel<AR_PROTO_SIMPLE, DT, true, DBG> : ring_kernel<AR_PROTO_SIMPLE, DT, false, DBG>;
+}
+
+// dbg: a plan with debug flags runs the instance with the debug hooks.
+__host__ RingFn ring_fn(int proto, int dtype, bool dag, bool dbg)
+{
+    if (dtype == AR_FLOAT32) return dbg ? ring_fn_of<AR_FLOAT32, true>(proto, dag) : ring_fn_of<AR_FLOAT32, false>(proto, dag);
+    return dbg ? ring_fn_of<AR_BFLOAT16, true>(proto, dag) : ring_fn_of<AR_BFLOAT16, false>(proto, dag);
 }
 
 // unroll: 16-byte units per thread and iteration.  Two keep more loads in
@@ -1548,7 +1555,8 @@ __host__ RingFn direct_fn(int dtype, int nranks, int unroll)
 int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
 {
     dev::RingFn fn = info.algo == AR_ALGO_DIRECT ? dev::direct_fn(info.dtype, info.nranks, info.direct_unroll)
-                                                 : dev::ring_fn(info.proto, info.dtype, info.peer_direct != 0);
+                                                 : dev::ring_fn(info.proto, info.dtype, info.peer_direct != 0,
+                                                                args.debug != 0);
     RingArgs a = args;
     void *kargs[] = {&a};
     hipError_t e = hipLaunchKernel((const void *)fn, dim3((unsigned)info.grid), dim3((unsigned)info.block), kargs,
@@ -1556,12 +1564,12 @@ int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
     return e == hipSuccess ? AR_OK : AR_ERR_HIP;
 }
 
-// The smaller co-residency of the protocol's kernel variants.
+// The smallest co-residency of the protocol's kernel variants.
 int ring_occupancy(int proto, int dtype, int block, int *blocks_per_cu)
 {
     int best = 1 << 30;
-    for (int dag = 0; dag < 2; ++dag) {
-        dev::RingFn fn = dev::ring_fn(proto, dtype, dag != 0);
+    for (int v = 0; v < 4; ++v) {
+        dev::RingFn fn = dev::ring_fn(proto, dtype, (v & 1) != 0, (v & 2) != 0);
         int n = 0;
         hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, (const void *)fn, block, 0);
         if (e != hipSuccess) return AR_ERR_HIP;
