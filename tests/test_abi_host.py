@@ -275,9 +275,15 @@ def test_ring_byte_counts():
 def test_direct_unroll_resolution():
     def geom(count, **kw):
         return ar.ar_plan_geometry(ar.make_desc(8, count, "f32", algo="direct", **kw))
-    # by size: two units per thread up to 8 MiB per rank, one above
-    assert geom((8 << 20) // 4)["direct_unroll"] == 2
-    assert geom((8 << 20) // 4 + 4)["direct_unroll"] == 1
+    # by size, when the tuner has no opinion: two units per thread up to
+    # 8 MiB per rank, one above
+    ar.ar_set_tuner(lambda ctx: {"proto": ar.AR_PROTO_SIMPLE, "nchannels": 4, "algo": ar.AR_ALGO_DIRECT,
+                                 "direct_unroll": 0})
+    try:
+        assert geom((8 << 20) // 4)["direct_unroll"] == 2
+        assert geom((8 << 20) // 4 + 4)["direct_unroll"] == 1
+    finally:
+        ar.ar_set_tuner(None)
     assert geom(1 << 20, direct_unroll=1)["direct_unroll"] == 1
     assert geom(1 << 28, direct_unroll=2)["direct_unroll"] == 2
     # more than 8 ranks: one unit
