@@ -111,7 +111,10 @@ enum {
  *                       watchdog: every wave still exits and the run reports
  *                       AR_ERR_TIMEOUT.
  *   AR_DEBUG_JITTER     pseudo-random short sleeps before flag posts, to
- *                       shake out ordering races. */
+ *                       shake out ordering races.
+ * A ring plan with any debug flag runs a kernel build that carries these
+ * hooks; plans without them run one that does not (the hooks cost time even
+ * when not taken). */
 enum { AR_DEBUG_SKIP_POST = 1u, AR_DEBUG_JITTER = 2u };
 
 typedef struct ar_plan_s ar_plan_t;
