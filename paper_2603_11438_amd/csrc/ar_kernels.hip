@@ -877,61 +877,92 @@ struct LL128Step {
     static constexpr uint32_t kEplRS = kLL128Data / 4;  // 30 fp32 partials
     static constexpr uint32_t kEplAG = kLL128Data / E;  // 30 fp32 or 60 bf16
 
-    // Data bytes lane p carries of one line, and the element count that is.
-    __device__ static uint32_t part_bytes(uint32_t p) { return p < 7 ? 16u : 8u; }
-
-    // Load `n` elements of size E from r at byte offset off into a 16-byte
-    // vector; n == full size uses one vector load.
-    __device__ static u32x4 load_elems(Rsrc r, uint32_t off, uint32_t n, uint32_t full)
+    // Accesses of exactly BYTES (16, 8 or 4) bytes: a lane part of a line is
+    // 16 data bytes for lanes 0..6 and 8 for lane 7, in the wire format; the
+    // matching part of a rank buffer is part_elems elements of the data type.
+    template <uint32_t BYTES, int POL>
+    __device__ static u32x4 ld_bytes(Rsrc r, uint32_t off)
     {
-        u32x4 v = {0, 0, 0, 0};
-        if (n == full) {
-            const uint32_t bytes = full * E;
-            if (bytes == 16) return ld128<kInPol>(r, off);
-            if (bytes == 8) {
-                u32x2 h = ld64<kInPol>(r, off);
-                v[0] = h[0];
-                v[1] = h[1];
-                return v;
-            }
-            v[0] = ld32<kInPol>(r, off);
-            return v;
+        if constexpr (BYTES == 16) {
+            return ld128<POL>(r, off);
+        } else if constexpr (BYTES == 8) {
+            const u32x2 h = ld64<POL>(r, off);
+            return u32x4{h[0], h[1], 0, 0};
+        } else {
+            return u32x4{ld32<POL>(r, off), 0, 0, 0};
         }
-        for (uint32_t i = 0; i < n; ++i) {
-            if (E == 4) v[i] = ld32<kInPol>(r, off + 4 * i);
-            else v[i >> 1] |= ld16<kInPol>(r, off + 2 * i) << ((i & 1) * 16);
+    }
+    template <uint32_t BYTES, int POL>
+    __device__ static void st_bytes(Rsrc r, uint32_t off, u32x4 v)
+    {
+        if constexpr (BYTES == 16) st128<POL>(r, off, v);
+        else if constexpr (BYTES == 8) st64<POL>(r, off, u32x2{v[0], v[1]});
+        else st32<POL>(r, off, v[0]);
+    }
+
+    // One lane's part of a rank buffer: `full` elements (EPART for lanes
+    // 0..6, half of that for lane 7) of which the first n exist.  Whole parts
+    // use one access of the lane's width; a part cut by the end of the
+    // message (at most one per message) goes element by element, behind a
+    // wave-uniform test.  Every access is issued by every lane, out of range
+    // where it does not apply, so no store waits on a branch.
+    template <uint32_t EPART>
+    __device__ static u32x4 load_part(Rsrc r, uint32_t off, uint32_t p, uint32_t n, uint32_t full)
+    {
+        constexpr uint32_t WB = EPART * E;
+        const bool whole = n != 0 && n == full;
+        u32x4 v = ld_bytes<WB, kInPol>(r, in_range(whole && p < 7, off)) |
+                  ld_bytes<WB / 2, kInPol>(r, in_range(whole && p == 7, off));
+        const bool cut = n != 0 && n < full;
+        if (any_lane(cut)) {
+#pragma unroll
+            for (uint32_t i = 0; i < EPART; ++i) {
+                const bool ok = cut && i < n;
+                if (E == 4) v[i] |= ld32<kInPol>(r, in_range(ok, off + 4 * i));
+                else v[i >> 1] |= ld16<kInPol>(r, in_range(ok, off + 2 * i)) << ((i & 1) * 16);
+            }
         }
         return v;
     }
-    __device__ static void store_elems(Rsrc r, uint32_t off, u32x4 v, uint32_t n, uint32_t full)
+    template <uint32_t EPART>
+    __device__ static void store_part(Rsrc r, uint32_t off, u32x4 v, uint32_t p, uint32_t n, uint32_t full)
     {
-        if (n == full) {
-            const uint32_t bytes = full * E;
-            if (bytes == 16) st128<kOutPol>(r, off, v);
-            else if (bytes == 8) st64<kOutPol>(r, off, u32x2{v[0], v[1]});
-            else st32<kOutPol>(r, off, v[0]);
-            return;
-        }
-        for (uint32_t i = 0; i < n; ++i) {
-            if (E == 4) st32<kOutPol>(r, off + 4 * i, v[i]);
-            else st16<kOutPol>(r, off + 2 * i, (v[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu);
+        constexpr uint32_t WB = EPART * E;
+        const bool whole = n != 0 && n == full;
+        st_bytes<WB, kOutPol>(r, in_range(whole && p < 7, off), v);
+        st_bytes<WB / 2, kOutPol>(r, in_range(whole && p == 7, off), v);
+        const bool cut = n != 0 && n < full;
+        if (any_lane(cut)) {
+#pragma unroll
+            for (uint32_t i = 0; i < EPART; ++i) {
+                const bool ok = cut && i < n;
+                if (E == 4) st32<kOutPol>(r, in_range(ok, off + 4 * i), v[i]);
+                else st16<kOutPol>(r, in_range(ok, off + 2 * i), (v[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu);
+            }
         }
     }
 
-    // Write one lane's part of a line (data only; lane 7's flag comes later).
-    __device__ static void put_data(Rsrc wo, uint32_t line, uint32_t p, u32x4 d)
+    // One lane's part of a line on the wire (data only; lane 7's flag comes
+    // later); act = false sends both stores out of range.
+    __device__ static void put_data(Rsrc wo, uint32_t line, uint32_t p, bool act, u32x4 d)
     {
-        if (p < 7) st128<kFifoSt>(wo, line * 128 + 16 * p, d);
-        else st64<kFifoSt>(wo, line * 128 + 112, u32x2{d[0], d[1]});
+        st128<kFifoSt>(wo, in_range(act && p < 7, line * 128 + 16 * p), d);
+        st64<kFifoSt>(wo, in_range(act && p == 7, line * 128 + 112), u32x2{d[0], d[1]});
     }
-    __device__ static void put_flag(Rsrc wo, uint32_t line, uint64_t tag)
+    // Flags of lines [lo, hi): lane 7 of each group of eight lanes writes the
+    // flag of one line.
+    __device__ static void put_flags(Rsrc wo, uint32_t lo, uint32_t hi, uint32_t p, uint32_t ls, uint64_t tag)
     {
-        st64<kFifoSt>(wo, line * 128 + 120, u32x2{(uint32_t)tag, (uint32_t)(tag >> 32)});
+        for (uint32_t lb = lo; lb < hi; lb += 8) {
+            const uint32_t line = lb + ls;
+            st64<kFifoSt>(wo, in_range(p == 7 && line < hi, line * 128 + 120),
+                          u32x2{(uint32_t)tag, (uint32_t)(tag >> 32)});
+        }
     }
 
-    // Reduce-scatter arithmetic for one lane part: n fp32 partials (<= 4)
+    // Reduce-scatter arithmetic for one lane part: up to 4 fp32 partials
     // plus the lane's input elements.
-    __device__ static u32x4 rs_reduce(const u32x4 &wire, const u32x4 &in, uint32_t n)
+    __device__ static u32x4 rs_reduce(const u32x4 &wire, const u32x4 &in)
     {
         float acc[4];
         for (int i = 0; i < 4; ++i) {
@@ -940,13 +971,13 @@ struct LL128Step {
         }
         if (kRecvRS)
             for (int i = 0; i < 4; ++i) acc[i] = as_f32(wire[i]) + acc[i];
-        (void)n;
         return u32x4{as_u32(acc[0]), as_u32(acc[1]), as_u32(acc[2]), as_u32(acc[3])};
     }
 
     // Spin until the flags of the lines held in lines[] match tag.  Lane 7 of
-    // each line carries the flag in words 2..3; every lane of a line reloads
-    // when its line is stale.
+    // each line carries the flag in words 2..3.  While any line is stale the
+    // wave reloads every line of the batch (a valid line cannot change before
+    // this wave frees the slot).
     template <int NB>
     __device__ static bool await_lines(const RingArgs &a, Rsrc wi, u32x4 *lines, const uint32_t *line_of,
                                        const bool *act, uint64_t tag)
@@ -955,23 +986,15 @@ struct LL128Step {
         const uint32_t p = lane & 7u;
         Watchdog wd;
         while (true) {
-            uint64_t stale = 0;
+            bool bad = false;
 #pragma unroll
-            for (int t = 0; t < NB; ++t) {
-                bool bad = act[t] && p == 7 &&
-                           (((uint64_t)lines[t][3] << 32) | lines[t][2]) != tag;
-                stale |= __ballot(bad);
-            }
-            if (stale == 0) break;
+            for (int t = 0; t < NB; ++t)
+                bad |= act[t] && p == 7 && (((uint64_t)lines[t][3] << 32) | lines[t][2]) != tag;
+            if (!any_lane(bad)) break;
             __builtin_amdgcn_s_sleep(1);
             if (watchdog_expired(a, wd)) return false;
 #pragma unroll
-            for (int t = 0; t < NB; ++t) {
-                bool bad = act[t] && p == 7 &&
-                           (((uint64_t)lines[t][3] << 32) | lines[t][2]) != tag;
-                uint64_t m = __ballot(bad);
-                if (act[t] && ((m >> (lane | 7u)) & 1u)) lines[t] = ld128<kFifoLd>(wi, line_of[t] * 128 + 16 * p);
-            }
+            for (int t = 0; t < NB; ++t) lines[t] = ld128<kFifoLd>(wi, in_range(act[t], line_of[t] * 128 + 16 * p));
         }
         after_observe();
         return true;
@@ -1005,39 +1028,37 @@ struct LL128Step {
                         act[t] = line_of[t] < nlines;
                         const uint32_t e0 = line_of[t] * epl + p * epart;
                         nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
-                        if (kLoadIn && nval[t]) in[t] = load_elems(rin, e0 * E, nval[t], full);
-                        else in[t] = u32x4{0, 0, 0, 0};
-                        if ((kRecvRS || kRecvAG) && act[t]) wire[t] = ld128<kFifoLd>(wi, line_of[t] * 128 + 16 * p);
+                        in[t] = u32x4{0, 0, 0, 0};
+                        if (kLoadIn) in[t] = load_part<epart>(rin, e0 * E, p, nval[t], full);
+                        if (kRecvRS || kRecvAG) wire[t] = ld128<kFifoLd>(wi, in_range(act[t], line_of[t] * 128 + 16 * p));
                     }
                     if (kRecvRS || kRecvAG) {
                         if (!await_lines<U>(a, wi, wire, line_of, act, tag_in)) return false;
                     }
 #pragma unroll
                     for (int t = 0; t < U; ++t) {
-                        if (!act[t]) continue;
                         const uint32_t e0 = line_of[t] * epl + p * epart;
                         u32x4 out;
-                        if (kSendRS || kReduceToY) out = rs_reduce(wire[t], in[t], nval[t]);
+                        if (kSendRS || kReduceToY) out = rs_reduce(wire[t], in[t]);
                         else if (kCopyInToY) out = in[t];
                         else out = wire[t];
-                        if (kWriteOut && nval[t]) {
+                        if (kWriteOut) {
                             if (KIND == kRecvReduceCopy && E == 2) {
                                 // bf16 owner: round the fp32 sums once, 4 values per lane part
                                 const u32x4 y = {pack_bf16(as_f32(out[0]), as_f32(out[1])),
                                                  pack_bf16(as_f32(out[2]), as_f32(out[3])), 0, 0};
-                                store_elems(rout, e0 * E, y, nval[t], full);
+                                store_part<epart>(rout, e0 * E, y, p, nval[t], full);
                             } else {
-                                store_elems(rout, e0 * E, out, nval[t], full);
+                                store_part<epart>(rout, e0 * E, out, p, nval[t], full);
                             }
                         }
-                        if (kSendRS || kSendAG) put_data(wo, line_of[t], p, out);
+                        if (kSendRS || kSendAG) put_data(wo, line_of[t], p, act[t], out);
                     }
                 }
                 if (kSendRS || kSendAG) {
                     drain_vmem();
                     const uint32_t gend = gbase + 8 * U * kGroup < nlines ? gbase + 8 * U * kGroup : nlines;
-                    if (p == 7)
-                        for (uint32_t line = gbase + ls; line < gend; line += 8) put_flag(wo, line, tag_out);
+                    put_flags(wo, gbase, gend, p, ls, tag_out);
                 }
             }
             return true;
@@ -1046,57 +1067,56 @@ struct LL128Step {
         // wave loads) become 8 all-gather lines (one wave store) per round.
         const uint32_t nlines_ag = (len + kEplAG - 1) / kEplAG;
         for (uint32_t gbase = 0; gbase < nlines_ag; gbase += 8 * kGroup) {
-        for (uint32_t agb = gbase; agb < gbase + 8 * kGroup && agb < nlines_ag; agb += 8) {
-            // Phase 1: receive 16 RS lines, reduce, stage bf16 results in LDS.
-            u32x4 in[2], wire[2];
-            uint32_t line_of[2], nval[2];
-            bool act[2];
-            const uint32_t rs_nlines = (len + kEplRS - 1) / kEplRS;
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                line_of[t] = 2 * agb + 8 * t + ls;
-                act[t] = line_of[t] < rs_nlines;
-                const uint32_t e0 = line_of[t] * kEplRS + p * 4;
+            for (uint32_t agb = gbase; agb < gbase + 8 * kGroup && agb < nlines_ag; agb += 8) {
+                // Phase 1: receive 16 RS lines, reduce, stage bf16 results in LDS.
+                u32x4 in[2], wire[2];
+                uint32_t line_of[2], nval[2];
+                bool act[2];
+                const uint32_t rs_nlines = (len + kEplRS - 1) / kEplRS;
                 const uint32_t full = p < 7 ? 4u : 2u;
-                nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
-                in[t] = nval[t] ? load_elems(rin, e0 * E, nval[t], full) : u32x4{0, 0, 0, 0};
-                if (act[t]) wire[t] = ld128<kFifoLd>(wi, line_of[t] * 128 + 16 * p);
-            }
-            if (!await_lines<2>(a, wi, wire, line_of, act, tag_in)) return false;
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                // Element index of this lane's first value within the 480-block.
-                const uint32_t loc = (8 * t + ls) * kEplRS + p * 4;
-                u32x4 acc = rs_reduce(wire[t], in[t], nval[t]);
-                lds[loc / 2] = pack_bf16(as_f32(acc[0]), as_f32(acc[1]));
-                if (p < 7) lds[loc / 2 + 1] = pack_bf16(as_f32(acc[2]), as_f32(acc[3]));
+                for (int t = 0; t < 2; ++t) {
+                    line_of[t] = 2 * agb + 8 * t + ls;
+                    act[t] = line_of[t] < rs_nlines;
+                    const uint32_t e0 = line_of[t] * kEplRS + p * 4;
+                    nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
+                    in[t] = load_part<4>(rin, e0 * E, p, nval[t], full);
+                    wire[t] = ld128<kFifoLd>(wi, in_range(act[t], line_of[t] * 128 + 16 * p));
+                }
+                if (!await_lines<2>(a, wi, wire, line_of, act, tag_in)) return false;
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    // Element index of this lane's first value within the 480-block.
+                    const uint32_t loc = (8 * t + ls) * kEplRS + p * 4;
+                    u32x4 acc = rs_reduce(wire[t], in[t]);
+                    lds[loc / 2] = pack_bf16(as_f32(acc[0]), as_f32(acc[1]));
+                    if (p < 7) lds[loc / 2 + 1] = pack_bf16(as_f32(acc[2]), as_f32(acc[3]));
+                }
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+                // Phase 2: read back in the 60-per-line layout, write output and AG line.
+                const uint32_t line = agb + ls;
+                const bool act2 = line < nlines_ag;
+                const uint32_t full2 = p < 7 ? 8u : 4u;
+                const uint32_t e0 = line * kEplAG + p * 8;
+                const uint32_t n2 = act2 && e0 < len ? (len - e0 < full2 ? len - e0 : full2) : 0;
+                const uint32_t loc = ls * kEplAG + p * 8;
+                u32x4 y = {lds[loc / 2], lds[loc / 2 + 1], 0, 0};
+                if (p < 7) {
+                    y[2] = lds[loc / 2 + 2];
+                    y[3] = lds[loc / 2 + 3];
+                }
+                store_part<8>(rout, e0 * E, y, p, n2, full2);
+                put_data(wo, line, p, act2, y);
+                // LDS is rewritten by the next round only after every lane has read it.
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
             }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-            // Phase 2: read back in the 60-per-line layout, write output and AG line.
-            const uint32_t line = agb + ls;
-            const bool act2 = line < nlines_ag;
-            const uint32_t full = p < 7 ? 8u : 4u;
-            const uint32_t e0 = line * kEplAG + p * 8;
-            const uint32_t n2 = act2 && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
-            const uint32_t loc = ls * kEplAG + p * 8;
-            u32x4 y = {lds[loc / 2], lds[loc / 2 + 1], 0, 0};
-            if (p < 7) {
-                y[2] = lds[loc / 2 + 2];
-                y[3] = lds[loc / 2 + 3];
-            }
-            if (n2) store_elems(rout, e0 * E, y, n2, full);
-            if (act2) put_data(wo, line, p, y);
-            // LDS is rewritten by the next round only after every lane has read it.
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-        }
-        drain_vmem();
-        const uint32_t gend = gbase + 8 * kGroup < nlines_ag ? gbase + 8 * kGroup : nlines_ag;
-        if (p == 7)
-            for (uint32_t line = gbase + ls; line < gend; line += 8) put_flag(wo, line, tag_out);
+            drain_vmem();
+            const uint32_t gend = gbase + 8 * kGroup < nlines_ag ? gbase + 8 * kGroup : nlines_ag;
+            put_flags(wo, gbase, gend, p, ls, tag_out);
         }
         return true;
     }
