@@ -187,7 +187,7 @@ def select(rows, tie=0.02, coll="allreduce"):
         if ds:
             best = max(r["busbw"] for r in ds)
             ties = [r for r in ds if r["busbw"] >= (1 - tie) * best]
-            ties.sort(key=lambda r: (r["nchannels"], r["nwaves"]))
+            ties.sort(key=lambda r: (r["nchannels"], -r["busbw"]))
             d = ties[0]
         algo = "direct" if d is not None and d["busbw"] >= (1 - tie) * rr["busbw"] else "ring"
         out[size] = {"ring": rr, "direct": d, "algo": algo}
@@ -197,7 +197,7 @@ def select(rows, tie=0.02, coll="allreduce"):
 def select_ring(rows, tie=0.02, coll="allreduce"):
     """Per size: the highest median bus bandwidth; candidates within `tie` of
     the best are ties, broken by fewer channels, fewer wire bytes, smaller
-    chunk, fewer waves.  When the fixed default is itself within `tie` of the
+    chunk, then the higher bandwidth.  When the fixed default is itself within `tie` of the
     best, the row defers to it (the paper's policy also leaves sizes where
     its choice does not help to the library default)."""
     by = {}
@@ -211,7 +211,7 @@ def select_ring(rows, tie=0.02, coll="allreduce"):
             table[size] = dict(dflt, proto="default")
             continue
         ties = [r for r in rs if r["busbw"] >= (1 - tie) * best]
-        ties.sort(key=lambda r: (r["nchannels"], WIRE_RANK[r["proto"]], r["chunk_bytes"], r["nwaves"]))
+        ties.sort(key=lambda r: (r["nchannels"], WIRE_RANK[r["proto"]], r["chunk_bytes"], -r["busbw"]))
         table[size] = ties[0]
     return table
 
