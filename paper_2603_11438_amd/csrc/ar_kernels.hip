@@ -75,8 +75,11 @@ enum : int { kPolPlain = 0, kPolSc0 = 1, kPolNt = 2, kPolSc1 = 16 };
 #ifndef AR_SIMPLE_U
 #define AR_SIMPLE_U 4
 #endif
+#ifndef AR_LL128_U
+#define AR_LL128_U 2
+#endif
 #ifndef AR_LL128_GROUP
-#define AR_LL128_GROUP 4
+#define AR_LL128_GROUP 8
 #endif
 constexpr int kFifoLd = AR_FIFO_LD_POL;  // device-coherent FIFO reads
 constexpr int kFifoSt = AR_FIFO_ST_POL;  // device-coherent FIFO writes
@@ -846,10 +849,17 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
 //
 // 128-byte lines: bytes 0..119 data, 120..127 a 64-bit flag (message index
 // + 1).  Eight lanes own one line: lanes p = 0..6 move 16 data bytes each,
-// lane 7 moves the last 8 data bytes and the flag.  A wave moves 8 lines per
-// instruction.  The writer stores the data of a batch of lines, waits for
-// those stores to complete, then stores the lines' flags; the reader loads
-// whole lines and accepts a batch once every line's flag matches.
+// lane 7 the last 8 data bytes (and, on a read, the flag).  A wave moves 8
+// lines per instruction.  The writer stores the data of a batch of lines,
+// waits for those stores to complete, then stores the lines' flags, one
+// line per lane; the reader loads whole lines and accepts a batch once every
+// line's flag matches.
+//
+// Lane 7's part is half as wide as the others.  Rather than a second, narrow
+// access for it (a whole extra instruction for one lane in eight), lane 7
+// makes the same full-width access half a part earlier: a load keeps the
+// upper half, a store sends lane 6's upper half (taken over by a lane move)
+// in front of its own, so lanes 6 and 7 write those bytes with equal values.
 // Reduce-scatter lines hold 30 fp32 partials; all-gather lines hold 30 fp32
 // or 60 bf16 values.  A bf16 recvReduceCopySend re-lays its results from the
 // 30-per-line to the 60-per-line format through LDS.
@@ -869,13 +879,39 @@ struct LL128Step {
     static constexpr bool kCopyInToY = KindTraits<KIND>::kCopyInToY;
     // bf16 recvReduceCopySend changes the line format on the way through.
     static constexpr bool kRelayout = DT == AR_BFLOAT16 && KIND == kRecvReduceCopySend;
-    static constexpr int U = 4;
-    // Batches of U wave-wide line stores per drain-and-flag group.
+    // Wave-wide line accesses (8 lines each) per batch.  Two batches are in
+    // flight: the next one's loads go out before this one's stores, so two
+    // units per batch hold as many registers as four without the overlap.
+    static constexpr int U = AR_LL128_U;
+    // Batches per drain-and-flag group.
     static constexpr uint32_t kGroup = AR_LL128_GROUP;
 
     // Elements per line on the wire this step reads / writes.
     static constexpr uint32_t kEplRS = kLL128Data / 4;  // 30 fp32 partials
     static constexpr uint32_t kEplAG = kLL128Data / E;  // 30 fp32 or 60 bf16
+
+    // Lane 6's value, read by lane 7 (lanes 8k+6 and 8k+7 share a DPP row).
+    __device__ static uint32_t from_lane_below(uint32_t x)
+    {
+        return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x111 /* row_shr:1 */, 0xF, 0xF, true);
+    }
+    // A full-width access (WB bytes) that starts half a part early carries
+    // lane 7's part in its upper half.
+    template <uint32_t WB>
+    __device__ static u32x4 upper_half(const u32x4 &v)
+    {
+        static_assert(WB == 16 || WB == 8, "lane parts are 16 or 8 bytes");
+        if constexpr (WB == 16) return u32x4{v[2], v[3], 0, 0};
+        else return u32x4{v[1], 0, 0, 0};
+    }
+    // What lane 7 stores for that access: lane 6's upper half, then its own part.
+    template <uint32_t WB>
+    __device__ static u32x4 lane7_word(const u32x4 &v)
+    {
+        static_assert(WB == 16 || WB == 8, "lane parts are 16 or 8 bytes");
+        if constexpr (WB == 16) return u32x4{from_lane_below(v[2]), from_lane_below(v[3]), v[0], v[1]};
+        else return u32x4{from_lane_below(v[1]), v[0], 0, 0};
+    }
 
     // Accesses of exactly BYTES (16, 8 or 4) bytes: a lane part of a line is
     // 16 data bytes for lanes 0..6 and 8 for lane 7, in the wire format; the
@@ -901,18 +937,30 @@ struct LL128Step {
     }
 
     // One lane's part of a rank buffer: `full` elements (EPART for lanes
-    // 0..6, half of that for lane 7) of which the first n exist.  Whole parts
-    // use one access of the lane's width; a part cut by the end of the
-    // message (at most one per message) goes element by element, behind a
-    // wave-uniform test.  Every access is issued by every lane, out of range
-    // where it does not apply, so no store waits on a branch.
+    // 0..6, half of that for lane 7) of which the first n exist.  Every
+    // access is issued by every lane, out of range where it does not apply,
+    // so no store waits on a branch.
+    //
+    // Loading takes two calls.  load_whole issues the one full-width access
+    // of a whole part (lane 7's starting half a part early) and leaves the
+    // loaded words untouched: any arithmetic on them would make the wave wait
+    // for this load before it issues the next, and a batch's loads would go
+    // out one round trip apart.  part_value, called once the batch has
+    // arrived, moves lane 7's half into place and fetches a part cut by the
+    // end of the message (at most one per message) element by element,
+    // behind a wave-uniform test.
     template <uint32_t EPART>
-    __device__ static u32x4 load_part(Rsrc r, uint32_t off, uint32_t p, uint32_t n, uint32_t full)
+    __device__ static u32x4 load_whole(Rsrc r, uint32_t off, uint32_t p, uint32_t n, uint32_t full)
     {
         constexpr uint32_t WB = EPART * E;
         const bool whole = n != 0 && n == full;
-        u32x4 v = ld_bytes<WB, kInPol>(r, in_range(whole && p < 7, off)) |
-                  ld_bytes<WB / 2, kInPol>(r, in_range(whole && p == 7, off));
+        return ld_bytes<WB, kInPol>(r, in_range(whole, p == 7 ? off - WB / 2 : off));
+    }
+    template <uint32_t EPART>
+    __device__ static u32x4 part_value(Rsrc r, uint32_t off, uint32_t p, uint32_t n, uint32_t full, const u32x4 &w)
+    {
+        constexpr uint32_t WB = EPART * E;
+        u32x4 v = p == 7 ? upper_half<WB>(w) : w;
         const bool cut = n != 0 && n < full;
         if (any_lane(cut)) {
 #pragma unroll
@@ -929,8 +977,9 @@ struct LL128Step {
     {
         constexpr uint32_t WB = EPART * E;
         const bool whole = n != 0 && n == full;
-        st_bytes<WB, kOutPol>(r, in_range(whole && p < 7, off), v);
-        st_bytes<WB / 2, kOutPol>(r, in_range(whole && p == 7, off), v);
+        // Lane 7 is whole only if lane 6 is, so the bytes it takes over exist.
+        const u32x4 l7 = lane7_word<WB>(v);
+        st_bytes<WB, kOutPol>(r, in_range(whole, p == 7 ? off - WB / 2 : off), p == 7 ? l7 : v);
         const bool cut = n != 0 && n < full;
         if (any_lane(cut)) {
 #pragma unroll
@@ -942,21 +991,20 @@ struct LL128Step {
         }
     }
 
-    // One lane's part of a line on the wire (data only; lane 7's flag comes
-    // later); act = false sends both stores out of range.
+    // One lane's part of a line on the wire (data only; the flag comes
+    // later); act = false sends the store out of range.  Lane 7 writes bytes
+    // 104..119, the first 8 of them equal to lane 6's.
     __device__ static void put_data(Rsrc wo, uint32_t line, uint32_t p, bool act, u32x4 d)
     {
-        st128<kFifoSt>(wo, in_range(act && p < 7, line * 128 + 16 * p), d);
-        st64<kFifoSt>(wo, in_range(act && p == 7, line * 128 + 112), u32x2{d[0], d[1]});
+        const u32x4 l7 = lane7_word<16>(d);
+        st128<kFifoSt>(wo, in_range(act, line * 128 + (p == 7 ? 104u : 16 * p)), p == 7 ? l7 : d);
     }
-    // Flags of lines [lo, hi): lane 7 of each group of eight lanes writes the
-    // flag of one line.
-    __device__ static void put_flags(Rsrc wo, uint32_t lo, uint32_t hi, uint32_t p, uint32_t ls, uint64_t tag)
+    // Flags of lines [lo, hi), one line per lane.
+    __device__ static void put_flags(Rsrc wo, uint32_t lo, uint32_t hi, uint32_t lane, uint64_t tag)
     {
-        for (uint32_t lb = lo; lb < hi; lb += 8) {
-            const uint32_t line = lb + ls;
-            st64<kFifoSt>(wo, in_range(p == 7 && line < hi, line * 128 + 120),
-                          u32x2{(uint32_t)tag, (uint32_t)(tag >> 32)});
+        for (uint32_t lb = lo; lb < hi; lb += 64) {
+            const uint32_t line = lb + lane;
+            st64<kFifoSt>(wo, in_range(line < hi, line * 128 + 120), u32x2{(uint32_t)tag, (uint32_t)(tag >> 32)});
         }
     }
 
@@ -974,27 +1022,48 @@ struct LL128Step {
         return u32x4{as_u32(acc[0]), as_u32(acc[1]), as_u32(acc[2]), as_u32(acc[3])};
     }
 
-    // Spin until the flags of the lines held in lines[] match tag.  Lane 7 of
-    // each line carries the flag in words 2..3.  While any line is stale the
-    // wave reloads every line of the batch (a valid line cannot change before
-    // this wave frees the slot).
+    // Wait until the lines held in lines[] (the batch's lines first..first +
+    // 8 NB, of which those below nlines exist) carry tag.  Lane 7 of each
+    // line holds the flag in words 2..3.  If any line is stale, the wave
+    // polls the 8-byte flags alone, one line per lane, and once all match it
+    // reads the lines again; a valid line cannot change before this wave
+    // frees the slot.  Polling the flags rather than whole lines costs a
+    // sixteenth of the traffic, and the loop's loads never land in the
+    // registers that carry data, which would otherwise make the compiler
+    // wait for every store of the step before the next batch's loads.
     template <int NB>
-    __device__ static bool await_lines(const RingArgs &a, Rsrc wi, u32x4 *lines, const uint32_t *line_of,
-                                       const bool *act, uint64_t tag)
+    __device__ static bool stale_lines(const u32x4 *lines, const bool *act, uint32_t p, uint64_t tag)
     {
+        bool bad = false;
+#pragma unroll
+        for (int t = 0; t < NB; ++t)
+            bad |= act[t] && p == 7 && (((uint64_t)lines[t][3] << 32) | lines[t][2]) != tag;
+        return any_lane(bad);
+    }
+    template <int NB>
+    __device__ static bool poll_flags(const RingArgs &a, Rsrc wi, uint32_t first, uint32_t nlines, uint64_t tag)
+    {
+        static_assert(8 * NB <= 64, "one flag per lane");
         const uint32_t lane = step_lane();
-        const uint32_t p = lane & 7u;
+        const uint32_t fl = first + lane;
+        const bool fact = lane < 8 * NB && fl < nlines;
         Watchdog wd;
         while (true) {
-            bool bad = false;
-#pragma unroll
-            for (int t = 0; t < NB; ++t)
-                bad |= act[t] && p == 7 && (((uint64_t)lines[t][3] << 32) | lines[t][2]) != tag;
-            if (!any_lane(bad)) break;
             __builtin_amdgcn_s_sleep(1);
             if (watchdog_expired(a, wd)) return false;
+            const u32x2 f = ld64<kFifoLd>(wi, in_range(fact, fl * 128 + 120));
+            if (!any_lane(fact && (((uint64_t)f[1] << 32) | f[0]) != tag)) return true;
+        }
+    }
+    template <int NB>
+    __device__ static bool await_lines(const RingArgs &a, Rsrc wi, u32x4 *lines, const uint32_t *line_of,
+                                       const bool *act, uint64_t tag, uint32_t first, uint32_t nlines)
+    {
+        if (stale_lines<NB>(lines, act, step_lane() & 7u, tag)) {
+            if (!poll_flags<NB>(a, wi, first, nlines, tag)) return false;
 #pragma unroll
-            for (int t = 0; t < NB; ++t) lines[t] = ld128<kFifoLd>(wi, in_range(act[t], line_of[t] * 128 + 16 * p));
+            for (int t = 0; t < NB; ++t)
+                lines[t] = ld128<kFifoLd>(wi, in_range(act[t], line_of[t] * 128 + 16 * (step_lane() & 7u)));
         }
         after_observe();
         return true;
@@ -1009,7 +1078,7 @@ struct LL128Step {
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
         const Rsrc wi = make_rsrc(rslot, a.slot_bytes);
         const Rsrc wo = make_rsrc(wslot, a.slot_bytes);
-        if (!kRelayout) {
+        if constexpr (!kRelayout) {
             // One line format in and out: the lane part maps to the same elements.
             constexpr uint32_t epl = (kRecvRS || kSendRS) ? kEplRS : kEplAG;
             constexpr uint32_t epart = 16 / ((kRecvRS || kSendRS) ? 4 : E);  // elements per full part
@@ -1017,24 +1086,53 @@ struct LL128Step {
             const uint32_t full = p < 7 ? epart : epart / 2;
             // Lines are written in groups of kGroup batches; one drain per
             // group makes the group's data complete before its flags go out.
+            // Unit t of the batch at line `base`: the lane's line, and how
+            // many of its lane part's elements exist.
+            auto unit = [&](uint32_t base, int t, uint32_t &line, bool &act, uint32_t &nval) {
+                line = base + 8 * t + ls;
+                act = line < nlines;
+                const uint32_t e0 = line * epl + p * epart;
+                nval = act && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
+            };
+            auto issue = [&](uint32_t base, u32x4 *in, u32x4 *wire) {
+#pragma unroll
+                for (int t = 0; t < U; ++t) {
+                    uint32_t line, nval;
+                    bool act;
+                    unit(base, t, line, act, nval);
+                    if (kLoadIn) in[t] = load_whole<epart>(rin, (line * epl + p * epart) * E, p, nval, full);
+                    if (kRecvRS || kRecvAG) wire[t] = ld128<kFifoLd>(wi, in_range(act, line * 128 + 16 * p));
+                }
+            };
             for (uint32_t gbase = 0; gbase < nlines; gbase += 8 * U * kGroup) {
-                for (uint32_t base = gbase; base < gbase + 8 * U * kGroup && base < nlines; base += 8 * U) {
-                    u32x4 in[U], wire[U];
+                const uint32_t gend = gbase + 8 * U * kGroup < nlines ? gbase + 8 * U * kGroup : nlines;
+                u32x4 in[U], wire[U];
+#pragma unroll
+                for (int t = 0; t < U; ++t) in[t] = wire[t] = u32x4{0, 0, 0, 0};
+                issue(gbase, in, wire);
+                for (uint32_t base = gbase; base < gend; base += 8 * U) {
                     uint32_t line_of[U], nval[U];
                     bool act[U];
 #pragma unroll
-                    for (int t = 0; t < U; ++t) {
-                        line_of[t] = base + 8 * t + ls;
-                        act[t] = line_of[t] < nlines;
-                        const uint32_t e0 = line_of[t] * epl + p * epart;
-                        nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
-                        in[t] = u32x4{0, 0, 0, 0};
-                        if (kLoadIn) in[t] = load_part<epart>(rin, e0 * E, p, nval[t], full);
-                        if (kRecvRS || kRecvAG) wire[t] = ld128<kFifoLd>(wi, in_range(act[t], line_of[t] * 128 + 16 * p));
-                    }
+                    for (int t = 0; t < U; ++t) unit(base, t, line_of[t], act[t], nval[t]);
                     if (kRecvRS || kRecvAG) {
-                        if (!await_lines<U>(a, wi, wire, line_of, act, tag_in)) return false;
+                        if (!await_lines<U>(a, wi, wire, line_of, act, tag_in, base, nlines)) return false;
                     }
+                    // All inputs in place before the first store: a cut-part
+                    // load between stores would make the stores wait.
+                    if (kLoadIn) {
+#pragma unroll
+                        for (int t = 0; t < U; ++t)
+                            in[t] = part_value<epart>(rin, (line_of[t] * epl + p * epart) * E, p, nval[t], full, in[t]);
+                    }
+                    // The next batch's loads go out before this batch's
+                    // stores: the vector memory counter retires in issue
+                    // order, so a load issued after a store cannot be waited
+                    // for without waiting for the store as well.
+                    u32x4 nin[U], nwire[U];
+#pragma unroll
+                    for (int t = 0; t < U; ++t) nin[t] = nwire[t] = u32x4{0, 0, 0, 0};
+                    if (base + 8 * U < gend) issue(base + 8 * U, nin, nwire);
 #pragma unroll
                     for (int t = 0; t < U; ++t) {
                         const uint32_t e0 = line_of[t] * epl + p * epart;
@@ -1054,71 +1152,77 @@ struct LL128Step {
                         }
                         if (kSendRS || kSendAG) put_data(wo, line_of[t], p, act[t], out);
                     }
+#pragma unroll
+                    for (int t = 0; t < U; ++t) {
+                        in[t] = nin[t];
+                        wire[t] = nwire[t];
+                    }
                 }
                 if (kSendRS || kSendAG) {
                     drain_vmem();
-                    const uint32_t gend = gbase + 8 * U * kGroup < nlines ? gbase + 8 * U * kGroup : nlines;
-                    put_flags(wo, gbase, gend, p, ls, tag_out);
+                    put_flags(wo, gbase, gend, lane, tag_out);
                 }
             }
             return true;
-        }
-        // bf16 recvReduceCopySend: 16 reduce-scatter lines (480 elements, two
-        // wave loads) become 8 all-gather lines (one wave store) per round.
-        const uint32_t nlines_ag = (len + kEplAG - 1) / kEplAG;
-        for (uint32_t gbase = 0; gbase < nlines_ag; gbase += 8 * kGroup) {
-            for (uint32_t agb = gbase; agb < gbase + 8 * kGroup && agb < nlines_ag; agb += 8) {
-                // Phase 1: receive 16 RS lines, reduce, stage bf16 results in LDS.
-                u32x4 in[2], wire[2];
-                uint32_t line_of[2], nval[2];
-                bool act[2];
-                const uint32_t rs_nlines = (len + kEplRS - 1) / kEplRS;
-                const uint32_t full = p < 7 ? 4u : 2u;
-#pragma unroll
-                for (int t = 0; t < 2; ++t) {
-                    line_of[t] = 2 * agb + 8 * t + ls;
-                    act[t] = line_of[t] < rs_nlines;
-                    const uint32_t e0 = line_of[t] * kEplRS + p * 4;
-                    nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
-                    in[t] = load_part<4>(rin, e0 * E, p, nval[t], full);
-                    wire[t] = ld128<kFifoLd>(wi, in_range(act[t], line_of[t] * 128 + 16 * p));
+        } else {
+            // bf16 recvReduceCopySend: 16 reduce-scatter lines (480 elements, two
+            // wave loads) become 8 all-gather lines (one wave store) per round.
+            const uint32_t nlines_ag = (len + kEplAG - 1) / kEplAG;
+            for (uint32_t gbase = 0; gbase < nlines_ag; gbase += 8 * kGroup) {
+                for (uint32_t agb = gbase; agb < gbase + 8 * kGroup && agb < nlines_ag; agb += 8) {
+                    // Phase 1: receive 16 RS lines, reduce, stage bf16 results in LDS.
+                    u32x4 in[2], wire[2];
+                    uint32_t line_of[2], nval[2];
+                    bool act[2];
+                    const uint32_t rs_nlines = (len + kEplRS - 1) / kEplRS;
+                    const uint32_t full = p < 7 ? 4u : 2u;
+    #pragma unroll
+                    for (int t = 0; t < 2; ++t) {
+                        line_of[t] = 2 * agb + 8 * t + ls;
+                        act[t] = line_of[t] < rs_nlines;
+                        const uint32_t e0 = line_of[t] * kEplRS + p * 4;
+                        nval[t] = act[t] && e0 < len ? (len - e0 < full ? len - e0 : full) : 0;
+                        in[t] = load_whole<4>(rin, e0 * E, p, nval[t], full);
+                        wire[t] = ld128<kFifoLd>(wi, in_range(act[t], line_of[t] * 128 + 16 * p));
+                    }
+                    if (!await_lines<2>(a, wi, wire, line_of, act, tag_in, 2 * agb, rs_nlines)) return false;
+    #pragma unroll
+                    for (int t = 0; t < 2; ++t) {
+                        // Element index of this lane's first value within the 480-block.
+                        const uint32_t loc = (8 * t + ls) * kEplRS + p * 4;
+                        const uint32_t e0 = line_of[t] * kEplRS + p * 4;
+                        u32x4 acc = rs_reduce(wire[t], part_value<4>(rin, e0 * E, p, nval[t], full, in[t]));
+                        lds[loc / 2] = pack_bf16(as_f32(acc[0]), as_f32(acc[1]));
+                        if (p < 7) lds[loc / 2 + 1] = pack_bf16(as_f32(acc[2]), as_f32(acc[3]));
+                    }
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+                    __builtin_amdgcn_wave_barrier();
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+                    // Phase 2: read back in the 60-per-line layout, write output and AG line.
+                    const uint32_t line = agb + ls;
+                    const bool act2 = line < nlines_ag;
+                    const uint32_t full2 = p < 7 ? 8u : 4u;
+                    const uint32_t e0 = line * kEplAG + p * 8;
+                    const uint32_t n2 = act2 && e0 < len ? (len - e0 < full2 ? len - e0 : full2) : 0;
+                    const uint32_t loc = ls * kEplAG + p * 8;
+                    u32x4 y = {lds[loc / 2], lds[loc / 2 + 1], 0, 0};
+                    if (p < 7) {
+                        y[2] = lds[loc / 2 + 2];
+                        y[3] = lds[loc / 2 + 3];
+                    }
+                    store_part<8>(rout, e0 * E, y, p, n2, full2);
+                    put_data(wo, line, p, act2, y);
+                    // LDS is rewritten by the next round only after every lane has read it.
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+                    __builtin_amdgcn_wave_barrier();
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
                 }
-                if (!await_lines<2>(a, wi, wire, line_of, act, tag_in)) return false;
-#pragma unroll
-                for (int t = 0; t < 2; ++t) {
-                    // Element index of this lane's first value within the 480-block.
-                    const uint32_t loc = (8 * t + ls) * kEplRS + p * 4;
-                    u32x4 acc = rs_reduce(wire[t], in[t]);
-                    lds[loc / 2] = pack_bf16(as_f32(acc[0]), as_f32(acc[1]));
-                    if (p < 7) lds[loc / 2 + 1] = pack_bf16(as_f32(acc[2]), as_f32(acc[3]));
-                }
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-                __builtin_amdgcn_wave_barrier();
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-                // Phase 2: read back in the 60-per-line layout, write output and AG line.
-                const uint32_t line = agb + ls;
-                const bool act2 = line < nlines_ag;
-                const uint32_t full2 = p < 7 ? 8u : 4u;
-                const uint32_t e0 = line * kEplAG + p * 8;
-                const uint32_t n2 = act2 && e0 < len ? (len - e0 < full2 ? len - e0 : full2) : 0;
-                const uint32_t loc = ls * kEplAG + p * 8;
-                u32x4 y = {lds[loc / 2], lds[loc / 2 + 1], 0, 0};
-                if (p < 7) {
-                    y[2] = lds[loc / 2 + 2];
-                    y[3] = lds[loc / 2 + 3];
-                }
-                store_part<8>(rout, e0 * E, y, p, n2, full2);
-                put_data(wo, line, p, act2, y);
-                // LDS is rewritten by the next round only after every lane has read it.
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-                __builtin_amdgcn_wave_barrier();
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+                drain_vmem();
+                const uint32_t gend = gbase + 8 * kGroup < nlines_ag ? gbase + 8 * kGroup : nlines_ag;
+                put_flags(wo, gbase, gend, lane, tag_out);
             }
-            drain_vmem();
-            const uint32_t gend = gbase + 8 * kGroup < nlines_ag ? gbase + 8 * kGroup : nlines_ag;
-            put_flags(wo, gbase, gend, p, ls, tag_out);
+            return true;
         }
-        return true;
     }
 };
 
