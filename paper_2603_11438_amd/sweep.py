@@ -44,18 +44,40 @@ CHUNKS = {"ll": (4096, 16384, 65536), "ll128": (15360, 61440, 245760),
           "simple": (16384, 65536, 262144, 1048576)}
 
 
-def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3, graph=False):
-    """Seconds per call, `reps` samples.  Eager: k calls launched back to back
-    from the host (small messages then measure the host's launch rate).
-    Graph: k calls captured in one HIP graph and replayed, which measures the
-    device's time per call."""
+def _runner(plan, ts):
+    """A call of the plan out of place: the inputs ts (each rank's full
+    buffer) stay fixed and the results go to separate buffers.  Timing loops
+    use it because repeated in-place AllReduces feed each call the previous
+    call's sums, which grow about N-fold per call and are inf or NaN within
+    a few dozen calls, and the HBM rate depends on the values moved."""
     import torch
 
+    coll, count = plan.info["coll"], plan.info["count"]
+    if coll == ar.AR_COLL_ALLGATHER:
+        send = [t[:count] for t in ts]
+        recv = [torch.empty_like(t) for t in ts]
+    elif coll == ar.AR_COLL_REDUCESCATTER:
+        send = ts
+        recv = [torch.empty(count, dtype=t.dtype, device=t.device) for t in ts]
+    else:
+        send = ts
+        recv = [torch.empty_like(t) for t in ts]
+    return lambda stream: plan.run_oop(send, recv, stream)
+
+
+def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3, graph=False):
+    """Seconds per call, `reps` samples, out of place on fixed inputs.
+    Eager: k calls launched back to back from the host (small messages then
+    measure the host's launch rate).  Graph: k calls captured in one HIP
+    graph and replayed, which measures the device's time per call."""
+    import torch
+
+    run = _runner(plan, ts)
     for _ in range(warm):
-        plan.run(ts, stream)
+        run(stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    plan.run(ts, stream)
+    run(stream)
     torch.cuda.synchronize()
     one = max(time.perf_counter() - t0, 1e-6)
     k = max(10, min(2000, int(min_total_s / one)))
@@ -65,7 +87,7 @@ def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3, graph=False):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=side):
             for _ in range(k):
-                plan.run(ts, side)
+                run(side)
         g.replay()
         torch.cuda.synchronize()
         out = []
@@ -85,7 +107,7 @@ def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3, graph=False):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for _ in range(k):
-            plan.run(ts, stream)
+            run(stream)
         e1.record(stream)
         torch.cuda.synchronize()
         out.append(e0.elapsed_time(e1) / k / 1e3)
@@ -187,7 +209,9 @@ def select(rows, tie=0.02, coll="allreduce"):
         if ds:
             best = max(r["busbw"] for r in ds)
             ties = [r for r in ds if r["busbw"] >= (1 - tie) * best]
-            ties.sort(key=lambda r: (r["nchannels"], -r["busbw"]))
+            # parts_eff: a row asking for the size rule (0) competes with the
+            # part count that rule resolved to
+            ties.sort(key=lambda r: (r.get("parts_eff", r["nchannels"]), -r["busbw"]))
             d = ties[0]
         algo = "direct" if d is not None and d["busbw"] >= (1 - tie) * rr["busbw"] else "ring"
         out[size] = {"ring": rr, "direct": d, "algo": algo}
@@ -211,7 +235,8 @@ def select_ring(rows, tie=0.02, coll="allreduce"):
             table[size] = dict(dflt, proto="default")
             continue
         ties = [r for r in rs if r["busbw"] >= (1 - tie) * best]
-        ties.sort(key=lambda r: (r["nchannels"], WIRE_RANK[r["proto"]], r["chunk_bytes"], -r["busbw"]))
+        ties.sort(key=lambda r: (r.get("parts_eff", r["nchannels"]), WIRE_RANK[r["proto"]],
+                                 r.get("chunk_eff", r["chunk_bytes"]), -r["busbw"]))
         table[size] = ties[0]
     return table
 
@@ -504,12 +529,13 @@ def configs(args):
                     graph = torch.cuda.CUDAGraph()
                     side = torch.cuda.Stream()
                     side.wait_stream(torch.cuda.current_stream())
+                    run = _runner(plan, ts)
                     with torch.cuda.stream(side):
-                        plan.run(ts, side)
+                        run(side)
                     torch.cuda.synchronize()
                     with torch.cuda.graph(graph, stream=side):
                         for _ in range(100):
-                            plan.run(ts, side)
+                            run(side)
                     graph.replay()
                     torch.cuda.synchronize()
                     rep = []
