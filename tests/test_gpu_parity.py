@@ -60,6 +60,21 @@ def test_small_grid(ar, proto, dtype, n):
             run_case(ar, x, dtype, f"grid-{proto}-{dtype}-{n}-{count}-{nch}", proto=proto, nchannels=nch)
 
 
+def test_ll128_line_tails(ar):
+    """LL128 messages that end at every position of a 128-byte line, in
+    both line formats (30 fp32 values or partials per line, 60 bf16
+    values): inside lane 6's part, inside lane 7's half-width part (which
+    moves on an access that starts inside lane 6's), and at every other
+    lane.  One channel and one wave, so a message is a whole segment and
+    the last segment's length walks through every remainder."""
+    for dtype in ("f32", "bf16"):
+        for n, step, hi in ((2, 1, 124), (3, 3, 190)):
+            for r in range(0, hi, step):
+                count = n * 240 + r
+                x = draw(n, count, dtype, "normal", seed=5000 + 7 * n + r)
+                run_case(ar, x, dtype, f"ll128-tail-{dtype}-{n}-{count}", proto="ll128", nchannels=1, nwaves=1)
+
+
 @pytest.mark.parametrize("n", (1, 4, 5, 16))
 def test_rank_counts(ar, n):
     for proto in PROTOS:
