@@ -444,7 +444,16 @@ int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     const TableRow *table;
     int nrows;
     switch (ctx->coll) {
-    case AR_COLL_ALLREDUCE: table = kTableAllReduce; nrows = rows_of(kTableAllReduce); break;
+    case AR_COLL_ALLREDUCE:
+        // bf16 reduce-scatter hops carry fp32 partials, so its geometry has a table of its own
+        if (ctx->dtype == AR_BFLOAT16) {
+            table = kTableAllReduceBf16;
+            nrows = rows_of(kTableAllReduceBf16);
+        } else {
+            table = kTableAllReduce;
+            nrows = rows_of(kTableAllReduce);
+        }
+        break;
     case AR_COLL_REDUCESCATTER: table = kTableReduceScatter; nrows = rows_of(kTableReduceScatter); break;
     case AR_COLL_ALLGATHER: table = kTableAllGather; nrows = rows_of(kTableAllGather); break;
     default: return ar_tuner_noop(ctx, out, nullptr);  // not tabulated: defer to the default

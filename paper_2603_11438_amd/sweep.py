@@ -44,6 +44,14 @@ CHUNKS = {"ll": (4096, 16384, 65536), "ll128": (15360, 61440, 245760),
           "simple": (16384, 65536, 262144, 1048576)}
 
 
+def _uniform(count, dtype, gen):
+    """count values uniform in [-1, 1) in the data type (bf16: rounded)."""
+    import torch
+
+    t = torch.rand(count, device="cuda:0", generator=gen) * 2 - 1
+    return t if dtype == "f32" else t.to(torch.bfloat16)
+
+
 def _runner(plan, ts):
     """A call of the plan out of place: the inputs ts (each rank's full
     buffer) stay fixed and the results go to separate buffers.  Timing loops
@@ -156,26 +164,28 @@ def measure(args):
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     sizes = [int(s) for s in args.sizes.split(",")] if args.sizes else SIZES
-    n, coll = args.nranks, args.coll
+    n, coll, dtype = args.nranks, args.coll, args.dtype
+    e = 4 if dtype == "f32" else 2
     with open(args.out, "a") as fo:
         for size in sizes:
-            count = size // 4 if coll == "allreduce" else size // 4 // n
+            count = size // e if coll == "allreduce" else size // e // n
             if count == 0:
                 continue
             g = torch.Generator(device="cuda:0").manual_seed(11438)
-            ts = [torch.rand(size // 4, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
+            ts = [_uniform(size // e, dtype, g) for _ in range(n)]
             for cfg in grid(size, **({} if coll == "allreduce" else SMALL_GRID)):
                 if args.algo and cfg.get("algo", "ring") != args.algo:
                     continue
                 try:
-                    plan = ar.Plan(n, count, "f32", coll=coll, **cfg)
+                    plan = ar.Plan(n, count, dtype, coll=coll, **cfg)
                 except ar.ARError as e:
                     continue
                 times = _timer(plan, ts, stream, graph=args.timing == "graph")
                 info = plan.info
                 med = statistics.median(times)
-                rec = {"coll": coll, "timing": args.timing, "size": size, "nranks": n, "proto": info["proto_name"], "chunk_bytes": 0, **cfg,
-                       "algo": info["algo_name"], "parts_eff": info["nchannels"], "chunk_eff": info["chunk_elems"] * 4,
+                rec = {"coll": coll, "dtype": dtype, "timing": args.timing, "size": size, "nranks": n, "proto": info["proto_name"], "chunk_bytes": 0, **cfg,
+                       "algo": info["algo_name"], "parts_eff": info["nchannels"],
+                       "chunk_eff": info["chunk_elems"] * (4 if dtype == "f32" else 2),
                        "t_med_us": med * 1e6, "t_min_us": min(times) * 1e6, "t_max_us": max(times) * 1e6,
                        "busbw": bus_bw(coll, size, med, n)}
                 fo.write(json.dumps(rec) + "\n")
@@ -186,22 +196,23 @@ def measure(args):
             torch.cuda.empty_cache()
 
 
-def default_row(size, rs, nranks=8, coll="allreduce"):
+def default_row(size, rs, nranks=8, coll="allreduce", dtype="f32"):
     """The measured row that has the fixed default's geometry (Simple, 16
     channels, default chunk and waves), if the sweep contains it."""
-    count = size // 4 if coll == "allreduce" else size // 4 // nranks
-    g = ar.ar_plan_geometry(ar.make_desc(nranks, count, "f32", "simple", 16, DEFAULT_CHUNK,
+    e = 4 if dtype == "f32" else 2
+    count = size // e if coll == "allreduce" else size // e // nranks
+    g = ar.ar_plan_geometry(ar.make_desc(nranks, count, dtype, "simple", 16, DEFAULT_CHUNK,
                                          nwaves=DEFAULT_WAVES, coll=coll))
     for r in rs:
         if (r["proto"], r["nchannels"], r["nwaves"]) == ("simple", 16, DEFAULT_WAVES) and \
-                r["chunk_eff"] == g["chunk_elems"] * 4:
+                r["chunk_eff"] == g["chunk_elems"] * e:
             return r
     return None
 
 
-def select(rows, tie=0.02, coll="allreduce"):
+def select(rows, tie=0.02, coll="allreduce", dtype="f32"):
     """Per size: {"ring": ring choice, "direct": direct choice or None, "algo": "ring" | "direct"}."""
-    ring = select_ring([r for r in rows if r.get("algo", "ring") == "ring"], tie, coll)
+    ring = select_ring([r for r in rows if r.get("algo", "ring") == "ring"], tie, coll, dtype)
     out = {}
     for size, rr in ring.items():
         ds = [r for r in rows if r["size"] == size and r.get("algo") == "direct"]
@@ -218,7 +229,7 @@ def select(rows, tie=0.02, coll="allreduce"):
     return out
 
 
-def select_ring(rows, tie=0.02, coll="allreduce"):
+def select_ring(rows, tie=0.02, coll="allreduce", dtype="f32"):
     """Per size: the highest median bus bandwidth; candidates within `tie` of
     the best are ties, broken by fewer channels, fewer wire bytes, smaller
     chunk, then the higher bandwidth.  When the fixed default is itself within `tie` of the
@@ -230,7 +241,7 @@ def select_ring(rows, tie=0.02, coll="allreduce"):
     table = {}
     for size, rs in sorted(by.items()):
         best = max(r["busbw"] for r in rs)
-        dflt = default_row(size, rs, coll=coll)
+        dflt = default_row(size, rs, coll=coll, dtype=dtype)
         if dflt is not None and dflt["busbw"] >= (1 - tie) * best:
             table[size] = dict(dflt, proto="default")
             continue
@@ -241,25 +252,34 @@ def select_ring(rows, tie=0.02, coll="allreduce"):
     return table
 
 
-TABLE_NAMES = {"allreduce": "kTableAllReduce", "reducescatter": "kTableReduceScatter",
-               "allgather": "kTableAllGather"}
+TABLE_NAMES = {("allreduce", "f32"): "kTableAllReduce", ("allreduce", "bf16"): "kTableAllReduceBf16",
+               ("reducescatter", "f32"): "kTableReduceScatter", ("allgather", "f32"): "kTableAllGather"}
 
 
 def emit(tables, path):
-    """tables: {coll: per-size selection}; writes one C array per collective."""
+    """tables: {(coll, dtype): per-size selection}; writes one C array per
+    collective, and a bf16 one for AllReduce (the fp32 rows when no bf16
+    sweep is given)."""
     out = []
-    for coll in ("allreduce", "reducescatter", "allgather"):
-        out.append(emit_one(tables.get(coll, {}), coll))
+    for key in TABLE_NAMES:
+        table = tables.get(key)
+        src = key
+        if table is None and key[1] != "f32":
+            src = (key[0], "f32")
+            table = tables.get(src, {})
+        out.append(emit_one(table or {}, key, measured_as=src))
     with open(path, "w") as f:
         f.write("\n".join(out))
 
 
-def emit_one(table, coll):
+def emit_one(table, key, measured_as=None):
+    coll, dtype = key
+    measured_as = measured_as or key
     names = {"ll": "AR_PROTO_LL", "ll128": "AR_PROTO_LL128", "simple": "AR_PROTO_SIMPLE",
              "default": "AR_PROTO_AUTO"}
     lines = [
-        f"// {coll}: MI355X size -> {{algorithm; ring protocol, channels, chunk, waves;",
-        "// direct workgroups per segment, waves, units per thread} table for 8-rank fp32",
+        f"// {coll}, {dtype}: MI355X size -> {{algorithm; ring protocol, channels, chunk, waves;",
+        f"// direct workgroups per segment, waves, units per thread}} table for 8-rank {measured_as[1]}",
         "// collectives, one row per power-of-two size of each rank's full buffer from",
         "// 4 KiB to 128 MiB.  A message of S bytes uses the row of the smallest size",
         "// >= S (sizes below 4 KiB use the first row, above 128 MiB the last).",
@@ -275,7 +295,7 @@ def emit_one(table, coll):
         "//",
         "// columns: log2(size), ring proto, nchannels, chunk_bytes, nwaves, algorithm,",
         "//          direct parts, direct waves, direct unroll   [busBW GB/s: ring / direct]",
-        f"static const TableRow {TABLE_NAMES[coll]}[] = {{",
+        f"static const TableRow {TABLE_NAMES[key]}[] = {{",
     ]
     if not table:
         lines.append("    {27, AR_PROTO_AUTO, 0, 0, 0, AR_ALGO_AUTO, 0, 0, 0},  // not measured: defer to the default")
@@ -297,12 +317,12 @@ def table_cmd(args):
     for f in args.jsonl:
         rows += [json.loads(l) for l in open(f) if l.strip()]
     tables = {}
-    for coll in ("allreduce", "reducescatter", "allgather"):
-        rs = [r for r in rows if r.get("coll", "allreduce") == coll]
+    for coll, dtype in TABLE_NAMES:
+        rs = [r for r in rows if r.get("coll", "allreduce") == coll and r.get("dtype", "f32") == dtype]
         if rs:
-            tables[coll] = select(rs, coll=coll)
-    for coll, table in tables.items():
-        print(f"== {coll}")
+            tables[(coll, dtype)] = select(rs, coll=coll, dtype=dtype)
+    for (coll, dtype), table in tables.items():
+        print(f"== {coll} {dtype}")
         print_table(table)
     if args.emit:
         emit(tables, args.emit)
@@ -323,21 +343,22 @@ def validate(args):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    n, coll = args.nranks, args.coll
+    n, coll, dtype = args.nranks, args.coll, args.dtype
+    e = 4 if dtype == "f32" else 2
     sizes = [int(s) for s in args.sizes.split(",")] if args.sizes else SIZES
     with open(args.out, "a") as fo:
         for size in sizes:
-            count = size // 4 if coll == "allreduce" else size // 4 // n
+            count = size // e if coll == "allreduce" else size // e // n
             if count == 0:
                 continue
             g = torch.Generator(device="cuda:0").manual_seed(11438 + 100)
-            ts = [torch.rand(size // 4, device="cuda:0", generator=g) * 2 - 1 for _ in range(n)]
+            ts = [_uniform(size // e, dtype, g) for _ in range(n)]
             res = {}
             bad = lambda ctx: {"proto": ar.AR_PROTO_SIMPLE, "nchannels": 1, "algo": ar.AR_ALGO_RING}
             for name, tuner, algo in (("tuned", None, "auto"), ("tuned_ring", None, "ring"),
                                       ("default", "fixed_default", "auto"), ("bad_channels", bad, "auto")):
                 ar.ar_set_tuner(tuner)
-                plan = ar.Plan(n, count, "f32", proto="auto", algo=algo, coll=coll)
+                plan = ar.Plan(n, count, dtype, proto="auto", algo=algo, coll=coll)
                 ar.ar_set_tuner(None)
                 times = _timer(plan, ts, stream, reps=7, graph=args.timing == "graph")
                 med = statistics.median(times)
@@ -347,7 +368,7 @@ def validate(args):
                              "proto": plan.info["proto_name"], "nchannels": plan.info["nchannels"],
                              "chunk": plan.info["chunk_elems"] * 4, "nwaves": plan.info["nwaves"]}
                 plan.destroy()
-            rec = {"coll": coll, "timing": args.timing, "size": size, **{f"{k}_{kk}": vv for k, v in res.items() for kk, vv in v.items()},
+            rec = {"coll": coll, "dtype": dtype, "timing": args.timing, "size": size, **{f"{k}_{kk}": vv for k, v in res.items() for kk, vv in v.items()},
                    "ratio": res["tuned"]["busbw"] / res["default"]["busbw"],
                    "ratio_ring": res["tuned_ring"]["busbw"] / res["default"]["busbw"],
                    "bad_channels_loss": 1 - res["bad_channels"]["busbw"] / res["default"]["busbw"]}
@@ -567,6 +588,7 @@ def main(argv=None):
     m.add_argument("--nranks", type=int, default=8)
     m.add_argument("--algo", default="", help="measure only this algorithm (ring or direct)")
     m.add_argument("--coll", default="allreduce", choices=("allreduce", "allgather", "reducescatter"))
+    m.add_argument("--dtype", default="f32", choices=("f32", "bf16"))
     m.add_argument("--timing", default="graph", choices=("graph", "eager"))
     t = sub.add_parser("table")
     t.add_argument("jsonl", nargs="+")
@@ -576,6 +598,7 @@ def main(argv=None):
     v.add_argument("--nranks", type=int, default=8)
     v.add_argument("--sizes", default="")
     v.add_argument("--coll", default="allreduce", choices=("allreduce", "allgather", "reducescatter"))
+    v.add_argument("--dtype", default="f32", choices=("f32", "bf16"))
     v.add_argument("--timing", default="eager", choices=("graph", "eager"))
     st = sub.add_parser("stability")
     st.add_argument("--out", required=True)

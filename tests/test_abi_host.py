@@ -60,23 +60,35 @@ def test_version_and_strerror():
 
 # ------------------------------------------------------------------ tuner
 
-def test_builtin_table_form():
-    # one decision per power-of-two bucket, small sizes latency-oriented
+@pytest.mark.parametrize("dtype", ("f32", "bf16"))
+def test_builtin_table_form(dtype):
+    # one decision per power-of-two bucket, small sizes latency-oriented;
+    # AllReduce has a table per data type (bf16 hops carry fp32 partials)
     prev = None
     for k in range(12, 28):
-        d = ar.ar_tune(1 << k)
+        d = ar.ar_tune(1 << k, dtype=dtype)
         assert d["proto"] in (ar.AR_PROTO_LL, ar.AR_PROTO_LL128, ar.AR_PROTO_SIMPLE)
         assert 1 <= d["nchannels"] <= ar.AR_MAX_CHANNELS
         assert d["chunk_bytes"] >= 16 and d["chunk_bytes"] % 16 == 0
         assert 1 <= d["nwaves"] <= ar.AR_MAX_WAVES
+        assert d["algo"] in (ar.AR_ALGO_RING, ar.AR_ALGO_DIRECT)
         # sizes between buckets use the next bucket up
         if k > 12:
-            assert ar.ar_tune((1 << (k - 1)) + 1) == d
+            assert ar.ar_tune((1 << (k - 1)) + 1, dtype=dtype) == d
         prev = d
     # beyond the table: the last / first rows
-    assert ar.ar_tune(1 << 30) == ar.ar_tune(1 << 27)
-    assert ar.ar_tune(1) == ar.ar_tune(1 << 12)
+    assert ar.ar_tune(1 << 30, dtype=dtype) == ar.ar_tune(1 << 27, dtype=dtype)
+    assert ar.ar_tune(1, dtype=dtype) == ar.ar_tune(1 << 12, dtype=dtype)
     assert prev is not None
+
+
+def test_bf16_plans_consult_the_bf16_rows():
+    # a bf16 plan asks with msg_bytes = count * 2 and dtype bf16; the
+    # geometry it resolves is the bf16 row's
+    count = (32 << 20) // 2
+    want = ar.ar_tune(32 << 20, dtype="bf16")
+    g = ar.ar_plan_geometry(ar.make_desc(8, count, "bf16", "auto", 0, algo="ring"))
+    assert (g["proto"], g["nchannels"], g["nwaves"]) == (want["proto"], want["nchannels"], want["nwaves"])
 
 
 @pytest.mark.parametrize("coll", (ar.AR_COLL_REDUCESCATTER, ar.AR_COLL_ALLGATHER))
