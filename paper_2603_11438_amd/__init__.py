@@ -360,6 +360,38 @@ class Plan:
         rc = lib().ar_run_oop(self._h, _ptr_array(send), _ptr_array(recv), _stream_ptr(stream))
         _check(rc, "ar_run_oop")
 
+    def bind(self, send: Sequence, recv: Optional[Sequence] = None, stream=None):
+        """Check the buffers once and return a callable that launches the
+        collective on them with one C call: in place on `send` when recv is
+        None, else out of place.  For tight loops and timing: the returned
+        callable keeps the tensors alive, and they must keep their storage
+        while it is used; once the plan is destroyed a call raises."""
+        coll = self.info["coll"]
+        if recv is None:
+            self._check_tensors(send, self._full)
+        else:
+            self._check_tensors(send, self.info["count"] if coll == AR_COLL_ALLGATHER else self._full)
+            self._check_tensors(recv, self.info["count"] if coll == AR_COLL_REDUCESCATTER else self._full)
+        sp = _ptr_array(send)
+        rp = None if recv is None else _ptr_array(recv)
+        st = _stream_ptr(stream)
+        L = lib()
+        keep = (list(send), None if recv is None else list(recv))
+        plan = self
+
+        if recv is None:
+            def call():
+                rc = L.ar_run(plan._h, sp, st)
+                if rc:
+                    _check(rc, "ar_run")
+        else:
+            def call():
+                rc = L.ar_run_oop(plan._h, sp, rp, st)
+                if rc:
+                    _check(rc, "ar_run_oop")
+        call.tensors = keep
+        return call
+
     @property
     def _full(self) -> int:
         c = self.info["count"]

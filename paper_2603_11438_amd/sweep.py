@@ -70,7 +70,18 @@ def _runner(plan, ts):
     else:
         send = ts
         recv = [torch.empty_like(t) for t in ts]
-    return lambda stream: plan.run_oop(send, recv, stream)
+    # one bound call per stream: the buffers are checked once, and a call
+    # costs the library's launch, not the binding's per-call checks
+    bound = {}
+
+    def run(stream):
+        key = None if stream is None else stream.cuda_stream
+        fn = bound.get(key)
+        if fn is None:
+            fn = bound[key] = plan.bind(send, recv, stream)
+        fn()
+
+    return run
 
 
 def _timer(plan, ts, stream, min_total_s=2e-3, reps=5, warm=3, graph=False):
@@ -429,7 +440,10 @@ def _stats(times_s):
 def latency(args):
     """Small-message time per call, launched back to back from the host and
     replayed from a HIP graph that holds `--graph-runs` calls (out of place,
-    so every call does the same work)."""
+    so every call does the same work).  Host launches are timed through a
+    bound call (`Plan.bind`: one C call per run) and, as `eager_checked`,
+    through `Plan.run_oop`, which checks and marshals the buffers on every
+    call."""
     import torch
 
     torch.cuda.set_device(0)
@@ -447,24 +461,26 @@ def latency(args):
                 plan = ar.Plan(n, count, "f32", **kw)
                 side = torch.cuda.Stream()
                 side.wait_stream(torch.cuda.current_stream())
+                fn = plan.bind(send, recv, side)
                 with torch.cuda.stream(side):
                     for _ in range(5):
-                        plan.run_oop(send, recv, side)
+                        fn()
                     side.synchronize()
-                    eager = []
-                    for _ in range(7):
-                        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                        e0.record(side)
-                        for _ in range(k):
-                            plan.run_oop(send, recv, side)
-                        e1.record(side)
-                        e1.synchronize()
-                        eager.append(e0.elapsed_time(e1) / k / 1e3)
+                    eager, checked = [], []
+                    for out, call in ((eager, fn), (checked, lambda: plan.run_oop(send, recv, side))):
+                        for _ in range(7):
+                            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                            e0.record(side)
+                            for _ in range(k):
+                                call()
+                            e1.record(side)
+                            e1.synchronize()
+                            out.append(e0.elapsed_time(e1) / k / 1e3)
                 torch.cuda.synchronize()
                 graph = torch.cuda.CUDAGraph()
                 with torch.cuda.graph(graph, stream=side):
                     for _ in range(k):
-                        plan.run_oop(send, recv, side)
+                        fn()
                 torch.cuda.synchronize()
                 graph.replay()
                 torch.cuda.synchronize()
@@ -481,7 +497,7 @@ def latency(args):
                 info = plan.info
                 rec = {"size": size, "policy": name, "algo": info["algo_name"], "proto": info["proto_name"],
                        "nchannels": info["nchannels"], "nwaves": info["nwaves"], "runs_per_graph": k,
-                       "eager": _stats(eager), "graph": _stats(replay)}
+                       "eager": _stats(eager), "eager_checked": _stats(checked), "graph": _stats(replay)}
                 fo.write(json.dumps(rec) + "\n")
                 print(json.dumps(rec), flush=True)
                 del graph

@@ -75,6 +75,37 @@ def test_ll128_line_tails(ar):
                 run_case(ar, x, dtype, f"ll128-tail-{dtype}-{n}-{count}", proto="ll128", nchannels=1, nwaves=1)
 
 
+def test_bound_calls(ar):
+    """Plan.bind checks the buffers once and returns a single-C-call
+    launcher: repeated calls out of place and a call in place give the
+    oracle's bits, and a call after the plan is destroyed raises."""
+    import torch
+
+    n, count = 8, 40000
+    x = draw(n, count, "f32", "uniform", seed=4242)
+    want = oracle_bits(x, "f32")
+    for algo in ("ring", "direct"):
+        say(f"bound calls, {algo}")
+        plan = ar.Plan(n, count, "f32", algo=algo)
+        send = to_device(x, "f32")
+        recv = [torch.empty_like(t) for t in send]
+        fn = plan.bind(send, recv)
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        assert plan.status() == ar.AR_OK
+        assert_ranks_equal(recv, want, "f32", f"bound out of place, {algo}")
+        ts = to_device(x, "f32")
+        plan.bind(ts)()
+        torch.cuda.synchronize()
+        assert_ranks_equal(ts, want, "f32", f"bound in place, {algo}")
+        with pytest.raises(ValueError):
+            plan.bind(send[:-1], recv)
+        plan.destroy()
+        with pytest.raises(ar.ARError):
+            fn()
+
+
 @pytest.mark.parametrize("n", (1, 4, 5, 16))
 def test_rank_counts(ar, n):
     for proto in PROTOS:
