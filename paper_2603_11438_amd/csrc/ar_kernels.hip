@@ -33,8 +33,10 @@
 // and every counter is a device-scope atomic.  A Simple or LL128 sender
 // makes its data writes complete (s_waitcnt vmcnt(0)) before it stores the
 // counter or flags that publish them; an LL line carries its own flag.  A
-// receiver issues its slot reads only after it has observed the counter or
-// flag.  Rank inputs are read with the non-temporal hint: nothing writes an
+// Simple receiver issues its slot reads only after it has observed the
+// counter; LL and LL128 receivers read data and flags together and accept a
+// line once its flag is current (for LL128 see the note at LL128Step).  Rank
+// inputs are read with the non-temporal hint: nothing writes an
 // input before every read of it.  Rank outputs are written non-temporally
 // by their own rank, except in the peer-direct mode, where a neighbour on
 // another XCD also writes them, so every output access there uses sc1.
@@ -850,10 +852,14 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
 // 128-byte lines: bytes 0..119 data, 120..127 a 64-bit flag (message index
 // + 1).  Eight lanes own one line: lanes p = 0..6 move 16 data bytes each,
 // lane 7 the last 8 data bytes (and, on a read, the flag).  A wave moves 8
-// lines per instruction.  The writer stores the data of a batch of lines,
+// lines per instruction.  The writer stores the data of a group of lines,
 // waits for those stores to complete, then stores the lines' flags, one
 // line per lane; the reader loads whole lines and accepts a batch once every
-// line's flag matches.
+// line's flag matches.  Data and flag of a line then come from one load;
+// that the data half of such a load is no older than its flag half is an
+// assumption (CDNA does not promise 128-byte single-copy atomicity), not a
+// guarantee.  A batch found stale is read again only after its flags alone
+// have been seen current, which orders that read after them.
 //
 // Lane 7's part is half as wide as the others.  Rather than a second, narrow
 // access for it (a whole extra instruction for one lane in eight), lane 7
@@ -1084,8 +1090,6 @@ struct LL128Step {
             constexpr uint32_t epart = 16 / ((kRecvRS || kSendRS) ? 4 : E);  // elements per full part
             const uint32_t nlines = (len + epl - 1) / epl;
             const uint32_t full = p < 7 ? epart : epart / 2;
-            // Lines are written in groups of kGroup batches; one drain per
-            // group makes the group's data complete before its flags go out.
             // Unit t of the batch at line `base`: the lane's line, and how
             // many of its lane part's elements exist.
             auto unit = [&](uint32_t base, int t, uint32_t &line, bool &act, uint32_t &nval) {
@@ -1104,6 +1108,8 @@ struct LL128Step {
                     if (kRecvRS || kRecvAG) wire[t] = ld128<kFifoLd>(wi, in_range(act, line * 128 + 16 * p));
                 }
             };
+            // Lines are written in groups of kGroup batches; one drain per
+            // group makes the group's data complete before its flags go out.
             for (uint32_t gbase = 0; gbase < nlines; gbase += 8 * U * kGroup) {
                 const uint32_t gend = gbase + 8 * U * kGroup < nlines ? gbase + 8 * U * kGroup : nlines;
                 u32x4 in[U], wire[U];
