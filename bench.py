@@ -142,7 +142,7 @@ def main(argv=None) -> int:
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: this build runs the simulated ring on a single MI355X "
+        print(f"bench.py measures one GPU: the simulated ring runs on a single MI355X "
               f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
         return 2
 

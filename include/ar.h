@@ -97,7 +97,7 @@ enum { AR_PLACE_RANK_SPREAD = 0, AR_PLACE_CHANNEL_LOCAL = 1 };
 enum {
     AR_OK = 0,
     AR_ERR_ARG = 1,          /* bad argument (NULL, range, alignment, overlap) */
-    AR_ERR_UNSUPPORTED = 2,  /* valid request this build does not implement */
+    AR_ERR_UNSUPPORTED = 2,  /* valid request this library does not implement */
     AR_ERR_NOMEM = 3,        /* device or host allocation failed */
     AR_ERR_HIP = 4,          /* a HIP runtime call failed */
     AR_ERR_OCCUPANCY = 5,    /* grid cannot be co-resident on the device */

@@ -31,7 +31,7 @@ def ar():
     return ar
 
 
-# ------------------------------------------------------------- D1 (configs[0])
+# ------------------------------------------- D1: 4 KiB fp32, integer values, one channel
 
 def test_d1_simple_one_channel_bitexact(ar):
     w = workloads.WORKLOADS["D1"]
