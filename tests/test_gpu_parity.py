@@ -219,6 +219,8 @@ def test_d2_ll_vs_simple_channels(ar):
 def test_d3_bf16_simple_chunks_channels(ar):
     wl = workloads.WORKLOADS["D3"]
     cfgs = [dict(proto="simple", nchannels=c, chunk_bytes=k) for c in wl.channels for k in wl.chunks]
+    # and the built-in bf16 table's own choices, ring and overall
+    cfgs += [dict(proto="auto", algo="ring"), dict(proto="auto", algo="auto")]
     _full_size_sweep(ar, wl, cfgs)
 
 
