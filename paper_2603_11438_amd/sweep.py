@@ -16,14 +16,19 @@ on MI355X for the simulated ring.
 HIP graph and replayed), so small messages are ranked by kernel time rather
 than by the host's launch rate; `validate` times end-to-end calls launched
 from the host, as an application sees them (`--timing` switches either).
+Every timing loop runs out of place on fixed inputs through a bound call
+(one C call per run); `--dtype bf16` sweeps or validates bf16 data, which
+has an AllReduce table of its own.
 
 Selection rule per size, for the ring's columns: the highest median bus
 bandwidth wins; candidates within 2 % of the best count as ties and are
 broken by fewer channels, then fewer wire bytes (Simple < LL128 < LL), then
-smaller chunk, then fewer waves; when the fixed default is within 2 % the
-row defers to it.  The direct algorithm's columns take its fastest
-{workgroups per segment, waves, units per thread}.  The algorithm column picks the faster of
-the two (the direct algorithm on a tie: it moves fewer bytes).
+smaller chunk, then the higher bandwidth, channels and chunk counted as the
+plan resolved them; when the fixed default is within 2 % the row defers to
+it.  The direct algorithm's columns take its fastest {workgroups per
+segment, waves, units per thread}, ties within 2 % going to fewer resolved
+workgroups.  The algorithm column picks the faster of the two (the direct
+algorithm on a tie: it moves fewer bytes).
 """
 from __future__ import annotations
 
