@@ -51,5 +51,24 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+ABI_CHECK_SRC = os.path.join(ROOT, "tests", "native", "abi_gpu_check.cpp")
+ABI_CHECK = os.path.join(ROOT, "tests", "native", "abi_gpu_check")
+
+
+def build_abi_check() -> str:
+    """Compile the host program that drives libar through its C ABI alone
+    (a GPU test runs it); it links the in-tree libar.so by a relative rpath."""
+    rpath = "$ORIGIN/" + os.path.relpath(LIBDIR, os.path.dirname(ABI_CHECK))
+    tmp = ABI_CHECK + ".tmp"
+    cmd = [hipcc(), "-O2", "-std=c++17", "-Wall", "-I", INCLUDE, ABI_CHECK_SRC, "-L", LIBDIR, "-lar",
+           f"-Wl,-rpath,{rpath}", "-o", tmp]
+    r = subprocess.run(cmd, cwd=ROOT, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("abi_gpu_check build failed:\n" + (r.stdout or "") + (r.stderr or ""))
+    os.replace(tmp, ABI_CHECK)
+    return ABI_CHECK
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_abi_check())

@@ -14,3 +14,5 @@ def test_build_entry_point_succeeds():
                        cwd=ROOT, capture_output=True, text=True, timeout=900)
     assert r.returncode == 0, r.stdout[-2000:] + r.stderr[-4000:]
     assert r.stdout.strip().endswith("built")
+    # the host program that drives the C ABI alone is built too
+    assert os.access(os.path.join(ROOT, "tests", "native", "abi_gpu_check"), os.X_OK)
