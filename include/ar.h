@@ -342,10 +342,9 @@ int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out);
 
 /* Built-in tuners. */
 /* ar_tuner_table: measured MI355X tables, one row per power-of-two size
- * bucket of msg_bytes (4 KiB .. 128 MiB); one table per collective, and for
- * AllReduce one per data type (bf16 reduce-scatter hops carry fp32
- * partials, which moves the best geometry).  Collectives outside the tables
- * defer to the default. */
+ * bucket of msg_bytes (4 KiB .. 128 MiB), one table per collective and data
+ * type (bf16 reduce-scatter hops carry fp32 partials, which moves the best
+ * geometry).  Collectives outside the tables defer to the default. */
 int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);
 int ar_tuner_fixed_default(const ar_tune_ctx *ctx, ar_tune_out *out, void *user); /* Simple, 16 channels */
 int ar_tuner_noop(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);          /* defers: no opinion */

@@ -445,7 +445,8 @@ int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     int nrows;
     switch (ctx->coll) {
     case AR_COLL_ALLREDUCE:
-        // bf16 reduce-scatter hops carry fp32 partials, so its geometry has a table of its own
+        // bf16 reduce-scatter hops carry fp32 partials, so the best
+        // geometry moves with the data type: every collective has a table per type
         if (ctx->dtype == AR_BFLOAT16) {
             table = kTableAllReduceBf16;
             nrows = rows_of(kTableAllReduceBf16);
@@ -454,8 +455,24 @@ int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
             nrows = rows_of(kTableAllReduce);
         }
         break;
-    case AR_COLL_REDUCESCATTER: table = kTableReduceScatter; nrows = rows_of(kTableReduceScatter); break;
-    case AR_COLL_ALLGATHER: table = kTableAllGather; nrows = rows_of(kTableAllGather); break;
+    case AR_COLL_REDUCESCATTER:
+        if (ctx->dtype == AR_BFLOAT16) {
+            table = kTableReduceScatterBf16;
+            nrows = rows_of(kTableReduceScatterBf16);
+        } else {
+            table = kTableReduceScatter;
+            nrows = rows_of(kTableReduceScatter);
+        }
+        break;
+    case AR_COLL_ALLGATHER:
+        if (ctx->dtype == AR_BFLOAT16) {
+            table = kTableAllGatherBf16;
+            nrows = rows_of(kTableAllGatherBf16);
+        } else {
+            table = kTableAllGather;
+            nrows = rows_of(kTableAllGather);
+        }
+        break;
     default: return ar_tuner_noop(ctx, out, nullptr);  // not tabulated: defer to the default
     }
     int lg = 0;

@@ -269,13 +269,14 @@ def select_ring(rows, tie=0.02, coll="allreduce", dtype="f32"):
 
 
 TABLE_NAMES = {("allreduce", "f32"): "kTableAllReduce", ("allreduce", "bf16"): "kTableAllReduceBf16",
-               ("reducescatter", "f32"): "kTableReduceScatter", ("allgather", "f32"): "kTableAllGather"}
+               ("reducescatter", "f32"): "kTableReduceScatter", ("reducescatter", "bf16"): "kTableReduceScatterBf16",
+               ("allgather", "f32"): "kTableAllGather", ("allgather", "bf16"): "kTableAllGatherBf16"}
 
 
 def emit(tables, path):
     """tables: {(coll, dtype): per-size selection}; writes one C array per
-    collective, and a bf16 one for AllReduce (the fp32 rows when no bf16
-    sweep is given)."""
+    collective and data type (a bf16 table repeats the fp32 rows when no
+    bf16 sweep is given)."""
     out = []
     for key in TABLE_NAMES:
         table = tables.get(key)

@@ -91,17 +91,19 @@ def test_bf16_plans_consult_the_bf16_rows():
     assert (g["proto"], g["nchannels"], g["nwaves"]) == (want["proto"], want["nchannels"], want["nwaves"])
 
 
+@pytest.mark.parametrize("dtype", ("f32", "bf16"))
 @pytest.mark.parametrize("coll", (ar.AR_COLL_REDUCESCATTER, ar.AR_COLL_ALLGATHER))
-def test_builtin_table_per_collective(coll):
-    # ReduceScatter and AllGather have tables of their own, keyed on the bytes
-    # of one rank's full buffer, with the same bucket rule as AllReduce.
+def test_builtin_table_per_collective(coll, dtype):
+    # ReduceScatter and AllGather have tables of their own (one per data
+    # type), keyed on the bytes of one rank's full buffer, with the same
+    # bucket rule as AllReduce.
     for k in range(12, 28):
-        d = ar.ar_tune(1 << k, coll=coll)
+        d = ar.ar_tune(1 << k, coll=coll, dtype=dtype)
         assert d["algo"] in (ar.AR_ALGO_RING, ar.AR_ALGO_DIRECT)
         assert 1 <= d["nchannels"] <= ar.AR_MAX_CHANNELS and 1 <= d["nwaves"] <= ar.AR_MAX_WAVES
         if k > 12:
-            assert ar.ar_tune((1 << (k - 1)) + 1, coll=coll) == d
-    assert ar.ar_tune(1 << 30, coll=coll) == ar.ar_tune(1 << 27, coll=coll)
+            assert ar.ar_tune((1 << (k - 1)) + 1, coll=coll, dtype=dtype) == d
+    assert ar.ar_tune(1 << 30, coll=coll, dtype=dtype) == ar.ar_tune(1 << 27, coll=coll, dtype=dtype)
     # a plan asks with msg_bytes = nranks * count * element size
     n, count = 8, (1 << 20) // 4 // 8
     g = ar.ar_plan_geometry(ar.make_desc(n, count, "f32", "auto", 0, coll=
