@@ -61,12 +61,6 @@ def segment_elems(nranks: int, count: int, elem_bytes: int) -> int:
     return -(-per_rank // a) * a
 
 
-def segment_of(i: int, nranks: int, count: int, elem_bytes: int) -> int:
-    """Index of the segment (= the chain's first rank) that element i belongs to."""
-    seg = segment_elems(nranks, count, elem_bytes)
-    return i // seg
-
-
 def _chain_f32(xf32: np.ndarray) -> np.ndarray:
     """Reduce an (N, count) float32 array along the segment-major ring chains."""
     n, count = xf32.shape

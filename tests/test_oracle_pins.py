@@ -9,11 +9,14 @@ Pins:
 * all-ones input gives exactly N everywhere (a dropped or repeated hop
   shows as N-1 or N+1);
 * integer-valued inputs give the exact integer sum (no rounding occurs);
-* a hand-worked order-revealing case (tests/golden/order_n4_f32.txt) fixes
-  the chain start and direction per segment;
-* brute force on tiny order-revealing inputs: every element equals the
-  scalar ring chain that starts at its segment's rank, with the scalar
-  chain computed by Python doubles rounded to binary32 after every add;
+* hand-worked order-revealing cases fix the chain start and direction per
+  segment, in fp32 (tests/golden/order_n4_f32.txt) and in bf16 with fp32
+  accumulation (tests/golden/order_n4_bf16.txt, where segments are cut on
+  8-element units);
+* brute force on tiny order-revealing inputs, fp32 and bf16: every element
+  equals the scalar ring chain that starts at its segment's rank, with the
+  scalar chain computed by Python doubles rounded to binary32 after every
+  add (and, for bf16, rounded once at the end by torch's CPU conversion);
 * bf16 rounding cases worked by hand (tests/golden/bf16_single_rounding.txt)
   fix one rounding at the end of an fp32 chain;
 * the recursive-summation bound against an order-free float64 sum;
@@ -81,26 +84,53 @@ def pin_integer_exact(impl):
                 assert np.array_equal(y.astype(np.int64), xi.sum(axis=0)), (dtype, n, count)
 
 
-def _read_golden_order():
+def _read_golden_kv(name):
     vals = {}
-    with open(os.path.join(GOLDEN, "order_n4_f32.txt")) as f:
+    with open(os.path.join(GOLDEN, name)) as f:
         for line in f:
             line = line.split("#", 1)[0].split()
             if line:
                 vals[line[0]] = line[1:]
+    return vals
+
+
+def _torch_bf16_bits(v):
+    """float32 values -> bf16 bits by torch's CPU conversion (a library RNE,
+    independent of the oracle's own rounding)."""
+    import torch
+
+    f = torch.from_numpy(np.ascontiguousarray(v, dtype=np.float32))
+    return f.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def _read_golden_order(name, dtype):
+    vals = _read_golden_kv(name)
     n = int(vals["nranks"][0])
     count = int(vals["count"][0])
     xr = [float(v) for v in vals["x"]]
     y = np.array([float(v) for v in vals["y"]], np.float32)
     x = np.repeat(np.array(xr, np.float32)[:, None], count, axis=1)
     assert x.shape == (n, count)
-    return x, y
+    if dtype == "bf16":
+        xb = _torch_bf16_bits(x).reshape(n, count)
+        # every input and every expected value is exact in bf16
+        assert np.array_equal(ro.bf16_to_f32(xb), x)
+        yb = _torch_bf16_bits(y)
+        assert np.array_equal(ro.bf16_to_f32(yb), y)
+        return xb, yb
+    return x, y.view(np.uint32)
 
 
 def pin_order_golden(impl):
-    x, y = _read_golden_order()
+    x, y = _read_golden_order("order_n4_f32.txt", "f32")
     got = impl(x, "f32")
-    assert np.array_equal(got.view(np.uint32), y.view(np.uint32)), got
+    assert np.array_equal(got.view(np.uint32), y), got
+
+
+def pin_order_golden_bf16(impl):
+    x, y = _read_golden_order("order_n4_bf16.txt", "bf16")
+    got = np.asarray(impl(x, "bf16"))
+    assert np.array_equal(got, y), ro.bf16_to_f32(got)
 
 
 def _f32(v: float) -> float:
@@ -137,6 +167,32 @@ def pin_brute_force_rotations(impl):
                 if any(c != want for c in chains):
                     informative += 1
     assert informative > 100  # the inputs really do tell chain orders apart
+
+
+def pin_brute_force_rotations_bf16(impl):
+    """bf16 inputs (every order value is exact in bf16), fp32 chains, one
+    rounding at the end; segments are cut on 16-byte units of the bf16
+    buffer, A = 8 elements.  The counts put segment boundaries where the
+    fp32 unit (A = 4) would cut them differently."""
+    rng = np.random.default_rng(12)
+    informative = 0
+    for n in (2, 3, 4, 5, 8):
+        for count in (1, 5, 13, 32, 64, 100, 250, 333):
+            xf = rng.choice(ORDER_VALUES, size=(n, count)).astype(np.float32)
+            xb = _torch_bf16_bits(xf).reshape(n, count)
+            assert np.array_equal(ro.bf16_to_f32(xb), xf)
+            got = np.asarray(impl(xb, "bf16"))
+            a = 8
+            seg = -(-(-(-count // n)) // a) * a
+            for i in range(count):
+                vals = [float(xf[r, i]) for r in range(n)]
+                chains = [_scalar_chain(vals, s) for s in range(n)]
+                rounded = [int(_torch_bf16_bits(np.array([c], np.float32))[0]) for c in chains]
+                want = rounded[i // seg]
+                assert int(got[i]) == want, (n, count, i, vals, chains, hex(int(got[i])))
+                if any(c != want for c in rounded):
+                    informative += 1
+    assert informative > 100  # chain orders stay distinguishable after rounding
 
 
 def _read_golden_bf16():
@@ -183,8 +239,8 @@ def pin_fp64_bound(impl):
     assert np.all(np.abs(yb - s) <= ulp + ro.recursive_sum_gamma(8) * ro.abs_sum_f64(xb, "bf16"))
 
 
-PINS = [pin_all_ones, pin_integer_exact, pin_order_golden, pin_brute_force_rotations,
-        pin_bf16_single_rounding, pin_fp64_bound]
+PINS = [pin_all_ones, pin_integer_exact, pin_order_golden, pin_order_golden_bf16, pin_brute_force_rotations,
+        pin_brute_force_rotations_bf16, pin_bf16_single_rounding, pin_fp64_bound]
 
 
 @pytest.mark.parametrize("impl_name", sorted(IMPLS))
@@ -199,22 +255,27 @@ def test_oracle_pin(pin, impl_name):
 # of them; otherwise the pins would not be worth trusting.
 
 def _mutant(chain_start, order="fwd", drop_last=False, per_hop_bf16=False, no_roundup=False,
-            negate=False):
+            negate=False, bf16_unit=None, bf16_start=None):
+    """bf16_unit / bf16_start: mistakes confined to the bf16 path (segments
+    cut on a unit of bf16_unit elements; chains started by bf16_start)."""
     def impl(x, dtype):
         n, count = x.shape
         e = 4 if dtype == "f32" else 2
         a = 16 // e
+        if dtype == "bf16" and bf16_unit is not None:
+            a = bf16_unit
         per = -(-count // n)
         seg = per if no_roundup else -(-per // a) * a
         xf = ro.bf16_to_f32(x) if dtype == "bf16" else x
         y = np.empty(count, np.float32)
         if count == 0:
             return y if dtype == "f32" else ro.f32_to_bf16_rne(y)
+        start_of = bf16_start if (dtype == "bf16" and bf16_start is not None) else chain_start
         for s in range(n):
             lo, hi = s * seg, min((s + 1) * seg, count)
             if lo >= hi:
                 continue
-            st = chain_start(s, n)
+            st = start_of(s, n)
             acc = xf[st, lo:hi].copy()
             terms = range(1, n - 1) if drop_last else range(1, n)
             for j in terms:
@@ -236,6 +297,10 @@ MUTANTS = {
     "per_hop_bf16": _mutant(lambda s, n: s, per_hop_bf16=True),
     "no_segment_roundup": _mutant(lambda s, n: s, no_roundup=True),
     "wrong_sign": _mutant(lambda s, n: s, negate=True),
+    # mistakes only the bf16 path makes
+    "bf16_fp32_unit": _mutant(lambda s, n: s, bf16_unit=4),
+    "bf16_start_next_rank": _mutant(lambda s, n: s, bf16_start=lambda s, n: (s + 1) % n),
+    "bf16_start_rank0": _mutant(lambda s, n: s, bf16_start=lambda s, n: 0),
 }
 
 
@@ -361,50 +426,127 @@ def test_bf16_rne_exhaustive_vs_torch():
 
 
 # ------------------------------------------------ ReduceScatter / AllGather
+#
+# Pins of the ReduceScatter oracle, as functions of an implementation
+# ``rs(x, dtype) -> (N, count)`` (float32 values or uint16 bf16 bits), run on
+# the oracle and on planted mistakes as above.
 
-def test_reduce_scatter_golden_order():
-    vals = {}
-    with open(os.path.join(GOLDEN, "reduce_scatter_order_n4_f32.txt")) as f:
-        for line in f:
-            line = line.split("#", 1)[0].split()
-            if line:
-                vals[line[0]] = line[1:]
-    n, count = int(vals["nranks"][0]), int(vals["count"][0])
-    x = np.repeat(np.array([float(v) for v in vals["x"]], np.float32)[:, None], n * count, axis=1)
-    y = ro.reduce_scatter(x, "f32")
-    for r, want in enumerate(vals["y"]):
-        assert np.all(y[r] == np.float32(float(want))), (r, y[r])
+def rs_pin_golden(rs):
+    for name, dtype in (("reduce_scatter_order_n4_f32.txt", "f32"), ("reduce_scatter_order_n4_bf16.txt", "bf16")):
+        vals = _read_golden_kv(name)
+        n, count = int(vals["nranks"][0]), int(vals["count"][0])
+        x = np.repeat(np.array([float(v) for v in vals["x"]], np.float32)[:, None], n * count, axis=1)
+        if dtype == "bf16":
+            xb = _torch_bf16_bits(x).reshape(n, n * count)
+            assert np.array_equal(ro.bf16_to_f32(xb), x)
+            x = xb
+        y = _as_f32(np.asarray(rs(x, dtype)).reshape(-1), dtype).reshape(n, count)
+        for r, want in enumerate(vals["y"]):
+            assert np.all(y[r] == np.float32(float(want))), (name, r, y[r])
 
 
-def test_reduce_scatter_invariants():
+def rs_pin_invariants(rs):
     rng = np.random.default_rng(21)
     for dtype in ("f32", "bf16"):
         for n in (1, 2, 3, 8, 16):
-            for count in (1, 8, 100):
+            for count in (8, 104):
                 # all ones -> n
                 ones = np.ones((n, n * count), np.float32)
                 xo = ones if dtype == "f32" else ro.f32_to_bf16_rne(ones).reshape(n, n * count)
-                y = _as_f32(ro.reduce_scatter(xo, dtype).reshape(-1), dtype)
+                y = _as_f32(np.asarray(rs(xo, dtype)).reshape(-1), dtype)
                 assert np.all(y == n)
                 # integers exact; block r of the sum lands on rank r
                 xi = rng.integers(-8, 9, size=(n, n * count))
                 xf = xi.astype(np.float32)
                 x = xf if dtype == "f32" else ro.f32_to_bf16_rne(xf).reshape(n, n * count)
-                y = _as_f32(ro.reduce_scatter(x, dtype).reshape(-1), dtype).reshape(n, count)
+                y = _as_f32(np.asarray(rs(x, dtype)).reshape(-1), dtype).reshape(n, count)
                 want = xi.sum(axis=0).reshape(n, count)
                 assert np.array_equal(y.astype(np.int64), want)
 
 
-def test_reduce_scatter_brute_force_chain():
+def rs_pin_brute_force_chain(rs):
+    """Every element of block r equals the scalar chain that starts at rank
+    r+1 (fp32), or that chain rounded once by torch's conversion (bf16)."""
     rng = np.random.default_rng(22)
-    for n in (2, 3, 5, 8):
-        count = 7
-        x = rng.choice(ORDER_VALUES, size=(n, n * count)).astype(np.float32)
-        y = ro.reduce_scatter(x, "f32")
+    informative = {"f32": 0, "bf16": 0}
+    for dtype in ("f32", "bf16"):
+        for n in (2, 3, 5, 8):
+            count = 64
+            xf = rng.choice(ORDER_VALUES, size=(n, n * count)).astype(np.float32)
+            x = xf if dtype == "f32" else _torch_bf16_bits(xf).reshape(n, n * count)
+            y = np.asarray(rs(x, dtype)).reshape(n, count)
+            for r in range(n):
+                for i in range(count):
+                    vals = [float(xf[q, r * count + i]) for q in range(n)]
+                    chains = [_scalar_chain(vals, s) for s in range(n)]
+                    if dtype == "f32":
+                        cand = [np.float32(c).view(np.uint32) for c in chains]
+                        got = np.float32(y[r, i]).view(np.uint32)
+                    else:
+                        cand = [int(_torch_bf16_bits(np.array([c], np.float32))[0]) for c in chains]
+                        got = int(y[r, i])
+                    want = cand[(r + 1) % n]
+                    assert got == want, (dtype, n, r, i, vals, chains)
+                    if any(c != want for c in cand):
+                        informative[dtype] += 1
+    assert min(informative.values()) > 50, informative
+
+
+RS_PINS = [rs_pin_golden, rs_pin_invariants, rs_pin_brute_force_chain]
+
+
+def test_reduce_scatter_pins_hold_for_the_oracle():
+    for pin in RS_PINS:
+        pin(ro.reduce_scatter)
+
+
+def _rs_mutant(start_shift=1, reverse=False, bf16_only=False, per_hop_bf16=False):
+    """A ReduceScatter oracle with one planted mistake: block r's chain starts
+    at rank r + start_shift, or runs against the ring direction, or rounds
+    to bf16 after every hop; bf16_only confines the mistake to bf16."""
+    def rs(x, dtype):
+        n = x.shape[0]
+        count = x.shape[1] // n
+        xf = ro.bf16_to_f32(x) if dtype == "bf16" else np.asarray(x, np.float32)
+        wrong = dtype == "bf16" or not bf16_only
+        y = np.empty((n, count), np.float32)
         for r in range(n):
-            for i in range(count):
-                vals = [float(x[q, r * count + i]) for q in range(n)]
-                assert float(y[r, i]) == _scalar_chain(vals, (r + 1) % n)
+            lo, hi = r * count, (r + 1) * count
+            st = (r + (start_shift if wrong else 1)) % n
+            acc = xf[st, lo:hi].copy()
+            for j in range(1, n):
+                q = (st - j) % n if (wrong and reverse) else (st + j) % n
+                acc = acc + xf[q, lo:hi]
+                if wrong and per_hop_bf16 and dtype == "bf16":
+                    acc = ro.bf16_to_f32(ro.f32_to_bf16_rne(acc)).reshape(acc.shape)
+            y[r] = acc
+        return y if dtype == "f32" else ro.f32_to_bf16_rne(y).reshape(n, count)
+    return rs
+
+
+RS_MUTANTS = {
+    "start_at_owner": _rs_mutant(start_shift=0),
+    "bf16_start_at_owner": _rs_mutant(start_shift=0, bf16_only=True),
+    "bf16_start_two_late": _rs_mutant(start_shift=2, bf16_only=True),
+    "bf16_reverse_direction": _rs_mutant(reverse=True, bf16_only=True),
+    "bf16_per_hop_rounding": _rs_mutant(per_hop_bf16=True, bf16_only=True),
+}
+
+
+def test_reduce_scatter_unmutated_passes():
+    for pin in RS_PINS:
+        pin(_rs_mutant())
+
+
+@pytest.mark.parametrize("name", sorted(RS_MUTANTS))
+def test_reduce_scatter_pins_reject_mutant(name):
+    failed = []
+    for pin in RS_PINS:
+        try:
+            pin(RS_MUTANTS[name])
+        except AssertionError:
+            failed.append(pin.__name__)
+    assert failed, f"no ReduceScatter pin rejects mutant {name}"
 
 
 def test_all_gather_is_concatenation():
