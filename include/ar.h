@@ -28,9 +28,23 @@
  * return int return AR_OK (0) or an AR_ERR_* code; functions that return a
  * pointer return NULL on error and leave the code in ar_last_error().
  * Nothing here is thread-safe for one plan: use a plan from one host thread
- * and keep at most one ar_run of a plan in flight, graph replays included
- * (its FIFOs and flag epochs are shared by all its runs).  Different plans
- * are independent.
+ * and keep at most one run of a plan in flight -- not on two streams at
+ * once, not in two graph replays at once, not in a replay and an eager run
+ * at once (its FIFOs and flag epochs are shared by all its runs; overlapping
+ * runs corrupt each other's results or end in the watchdog).
+ *
+ * Ring launches on one device are ordered across streams.  A ring kernel's
+ * workgroups wait on each other, so its grid needs the whole grid resident;
+ * two ring grids dispatched side by side could each hold part of the device
+ * while waiting for room the other occupies.  So before a ring launch on a
+ * stream, the library makes that stream wait for the device's previous ring
+ * launch if it went to another stream (an event recorded after every ring
+ * launch; one event per device, created on the first ring launch).  Ring
+ * collectives of different plans therefore never overlap in time, whatever
+ * streams they run on; the direct algorithm's kernels are not ordered (they
+ * never wait).  Launches captured into a HIP graph are not ordered this way:
+ * a graph whose replays may overlap ring launches on other streams must be
+ * ordered by its caller (replay it on the stream that runs the others).
  */
 #ifndef AR_H
 #define AR_H
@@ -52,8 +66,17 @@ enum { AR_FLOAT32 = 0, AR_BFLOAT16 = 1 };
 
 /* Protocols (paper, section 2: the tuner chooses among LL, LL128, Simple).
  *   LL     8-byte lines: 4 bytes of data + 4-byte flag in one word; the
- *          reader checks the flag in the same load that brings the data.
- *   LL128  128-byte lines: 120 bytes of data + 8-byte flag.
+ *          reader checks the flag in the same load that brings the data
+ *          (an aligned 8-byte access is single-copy atomic).
+ *   LL128  128-byte lines: 120 bytes of data + 8-byte flag.  The writer makes
+ *          a line's data complete before it stores the line's flag; the
+ *          reader loads whole lines and, once every flag of a batch is
+ *          current, uses the data of the same load.  That relies on an
+ *          assumption CDNA does not document: that one 128-byte line load
+ *          never returns its data half older than its flag half.  A stale
+ *          first look is re-read only after the flags alone were seen
+ *          current, which is ordered.  The built-in tuner table never picks
+ *          LL128 on MI355X; a caller who selects it takes the assumption.
  *   Simple bulk chunks behind separate ready (tail) / free (head) counters. */
 enum { AR_PROTO_AUTO = -1, AR_PROTO_LL = 0, AR_PROTO_LL128 = 1, AR_PROTO_SIMPLE = 2 };
 
@@ -344,7 +367,9 @@ int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out);
 /* ar_tuner_table: measured MI355X tables, one row per power-of-two size
  * bucket of msg_bytes (4 KiB .. 128 MiB), one table per collective and data
  * type (bf16 reduce-scatter hops carry fp32 partials, which moves the best
- * geometry).  Collectives outside the tables defer to the default. */
+ * geometry).  Every row was measured with 8 ranks; other rank counts get
+ * the same row (results are identical, the choice is unmeasured there).
+ * Collectives outside the tables defer to the default. */
 int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);
 int ar_tuner_fixed_default(const ar_tune_ctx *ctx, ar_tune_out *out, void *user); /* Simple, 16 channels */
 int ar_tuner_noop(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);          /* defers: no opinion */
@@ -394,11 +419,13 @@ typedef struct ar_adaptive_cfg {
 int ar_tuner_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);
 
 /* The paper's Listing 1 closed-loop policy (section 3.3) over the same
- * telemetry: no sample for ctx->comm_id -> 4 channels; messages of at most
- * 32 KiB take the small-message algorithm (here AR_ALGO_DIRECT, in place of
- * the listing's tree), larger ones the ring; Simple protocol; when the last
- * sample's latency exceeds 1 ms, one channel more than that run used (at
- * most 16), otherwise the same count.  user is unused. */
+ * telemetry: no sample for ctx->comm_id -> 4 channels and no other opinion
+ * (ar_tune then applies the default: the Simple ring); with a sample,
+ * messages of at most 32 KiB take the small-message algorithm (here
+ * AR_ALGO_DIRECT, in place of the listing's tree), larger ones the ring,
+ * with the Simple protocol, and when the last sample's latency exceeds
+ * 1 ms, one channel more than that run used (at most 16), otherwise the
+ * same count.  user is unused. */
 int ar_tuner_size_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);
 
 /* ---- errors and version ------------------------------------------------- */

@@ -215,6 +215,24 @@ def ar_tune(msg_bytes: int, nranks: int = 8, dtype="f32", max_channels: int = AR
             "direct_nwaves": out.direct_nwaves, "direct_unroll": out.direct_unroll}
 
 
+_BUILTIN_TUNERS = {"table": "ar_tuner_table", "fixed_default": "ar_tuner_fixed_default", "noop": "ar_tuner_noop",
+                   "adaptive": "ar_tuner_adaptive", "size_adaptive": "ar_tuner_size_adaptive"}
+
+
+def ar_tuner_raw(name: str, msg_bytes: int, nranks: int = 8, dtype="f32", max_channels: int = AR_MAX_CHANNELS,
+                 coll: int = AR_COLL_ALLREDUCE, comm_id: int = 0) -> dict:
+    """Call one built-in tuner directly (no validation, no defaults filled
+    in): what the policy itself answers.  Fields it leaves alone keep the
+    no-opinion values (AUTO, 0)."""
+    ctx = ar_tune_ctx(coll, msg_bytes, nranks, DTYPES[dtype] if isinstance(dtype, str) else dtype,
+                      max_channels, comm_id)
+    out = ar_tune_out(AR_PROTO_AUTO, 0, 0, 0, AR_ALGO_AUTO, 0, 0, 0)
+    rc = getattr(lib(), _BUILTIN_TUNERS[name])(ctypes.byref(ctx), ctypes.byref(out), None)
+    return {"rc": rc, "proto": out.proto, "nchannels": out.nchannels, "chunk_bytes": out.chunk_bytes,
+            "nwaves": out.nwaves, "algo": out.algo, "direct_parts": out.direct_parts,
+            "direct_nwaves": out.direct_nwaves, "direct_unroll": out.direct_unroll}
+
+
 _tuner_refs = []  # keep ctypes callbacks alive while installed
 
 
@@ -440,12 +458,17 @@ _plan_cache = {}
 
 
 def allreduce(tensors: Sequence, proto="auto", nchannels: int = 0, chunk_bytes: int = 0, stream=None, **kw):
-    """In-place sum AllReduce of N equal-shape device tensors (one per simulated rank)."""
+    """In-place sum AllReduce of N equal-shape device tensors (one per simulated rank).
+
+    Plans are cached per shape, settings and stream: a plan must never be in
+    flight on two streams at once (its FIFOs and flags are shared by all its
+    runs), so calls on different streams use different plans."""
     if not tensors:
         raise ValueError("need at least one tensor")
     t0 = tensors[0]
     dt = DTYPE_NAMES[_dtype_of(t0)]
-    key = (len(tensors), t0.numel(), dt, proto, nchannels, chunk_bytes, tuple(sorted(kw.items())))
+    key = (len(tensors), t0.numel(), dt, proto, nchannels, chunk_bytes, tuple(sorted(kw.items())),
+           _stream_ptr(stream))
     plan = _plan_cache.get(key)
     if plan is None:
         plan = Plan(len(tensors), t0.numel(), dt, proto, nchannels, chunk_bytes, **kw)

@@ -64,6 +64,24 @@ int launch_copy(const void *src, void *dst, size_t bytes, void *stream);
 int ring_occupancy(int proto, int dtype, int block, int *blocks_per_cu);
 int launch_bf16_round(const float *in, uint16_t *out, size_t n, void *stream);
 
+// Run-time helpers of ar_runtime.cpp.
+constexpr uint32_t kDefaultTimeoutUs = 2000000;  // 2 s per flag wait
+constexpr uint64_t kTicksPerUs = 100;            // 100 MHz real-time counter
+// Bytes of each rank's send and recv buffer for a collective's geometry.
+void buffer_bytes(const ar_plan_info &g, size_t *send_b, size_t *recv_b);
+// Rank buffers non-NULL, 16-byte aligned, receive buffers overlapping
+// nothing but their own rank's in-place layout: AR_OK or AR_ERR_ARG.
+int check_buffers(const ar_plan_info &g, const void *const *send, void *const *recv);
+// Workgroups of a ring launch that fit on the current device, per rank.
+int device_channel_capacity(int proto, int dtype, int nranks, int nwaves, int *cap);
+// Kernel arguments of one run.
+void fill_args(const ar_plan_info &g, uint32_t debug_flags, uint64_t timeout_ticks, const void *const *send,
+               void *const *recv, char *fifo, uint64_t *flags, uint32_t *ctl, RingArgs *out);
+// The tuner's and defaults' geometry for a description on the current device.
+int resolve_for_device(const ar_plan_desc *desc, ar_plan_desc *d_out, ar_plan_info *info_out, int *dev_out);
+// Ring memory layout: total bytes, with the flag lines and FIFO offsets.
+size_t workspace_layout(const ar_plan_info &info, size_t *flags_off, size_t *fifo_off);
+
 // Thread-local last error.
 void set_last_error(int code);
 

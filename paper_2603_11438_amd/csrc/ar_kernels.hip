@@ -59,21 +59,6 @@ typedef __amdgpu_buffer_rsrc_t Rsrc;
 
 // Cache-policy operand of gfx950 buffer instructions.
 enum : int { kPolPlain = 0, kPolSc0 = 1, kPolNt = 2, kPolSc1 = 16 };
-#ifndef AR_FIFO_POL
-#define AR_FIFO_POL kPolSc1
-#endif
-#ifndef AR_FIFO_LD_POL
-#define AR_FIFO_LD_POL AR_FIFO_POL
-#endif
-#ifndef AR_FIFO_ST_POL
-#define AR_FIFO_ST_POL AR_FIFO_POL
-#endif
-#ifndef AR_IN_POL
-#define AR_IN_POL kPolNt
-#endif
-#ifndef AR_OUT_POL
-#define AR_OUT_POL kPolNt
-#endif
 #ifndef AR_SIMPLE_U
 #define AR_SIMPLE_U 4
 #endif
@@ -83,10 +68,16 @@ enum : int { kPolPlain = 0, kPolSc0 = 1, kPolNt = 2, kPolSc1 = 16 };
 #ifndef AR_LL128_GROUP
 #define AR_LL128_GROUP 8
 #endif
-constexpr int kFifoLd = AR_FIFO_LD_POL;  // device-coherent FIFO reads
-constexpr int kFifoSt = AR_FIFO_ST_POL;  // device-coherent FIFO writes
-constexpr int kInPol = AR_IN_POL;      // rank inputs: read once, streamed
-constexpr int kOutPol = AR_OUT_POL;    // rank outputs: written once, streamed
+// The policies are fixed, not build options.  A FIFO line (or, in the
+// peer-direct mode, an output element) is written on one XCD and read on
+// another, behind a different L2; without the device-scope bit on both the
+// write and the read, a reader can be served a stale copy and the ring
+// returns wrong sums or waits until the watchdog fires.
+constexpr int kFifoLd = kPolSc1;  // device-coherent FIFO reads
+constexpr int kFifoSt = kPolSc1;  // device-coherent FIFO writes
+constexpr int kInPol = kPolNt;    // rank inputs: read once, streamed
+constexpr int kOutPol = kPolNt;   // rank outputs: written once, streamed
+static_assert((kFifoLd & kPolSc1) && (kFifoSt & kPolSc1), "FIFO accesses must be device-coherent");
 
 enum Kind : int {
     kSend = 0,            // own input -> wire (reduce-scatter start)
@@ -1714,8 +1705,9 @@ int launch_fill_u32(uint32_t *p, size_t n, uint32_t value, void *stream)
     if (n == 0) return AR_OK;
     size_t blocks = (n + 255) / 256;
     if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(dev::fill_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, p, n, value);
-    return hipGetLastError() == hipSuccess ? AR_OK : AR_ERR_HIP;
+    void *kargs[] = {&p, &n, &value};
+    return hipLaunchKernel((const void *)dev::fill_u32_kernel, dim3((unsigned)blocks), dim3(256), kargs, 0,
+                           (hipStream_t)stream) == hipSuccess ? AR_OK : AR_ERR_HIP;
 }
 
 int launch_copy(const void *src, void *dst, size_t bytes, void *stream)
@@ -1727,9 +1719,11 @@ int launch_copy(const void *src, void *dst, size_t bytes, void *stream)
     uint64_t blocks = (nunits + 4 * 256 - 1) / (4 * 256);
     if (blocks < 1) blocks = 1;
     if (blocks > 16384) blocks = 16384;
-    hipLaunchKernelGGL(dev::copy_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
-                       (const char *)src, (char *)dst, nunits, tail);
-    return hipGetLastError() == hipSuccess ? AR_OK : AR_ERR_HIP;
+    const char *s = (const char *)src;
+    char *d = (char *)dst;
+    void *kargs[] = {&s, &d, (void *)&nunits, (void *)&tail};
+    return hipLaunchKernel((const void *)dev::copy_kernel, dim3((unsigned)blocks), dim3(256), kargs, 0,
+                           (hipStream_t)stream) == hipSuccess ? AR_OK : AR_ERR_HIP;
 }
 
 int launch_bf16_round(const float *in, uint16_t *out, size_t n, void *stream)
@@ -1737,8 +1731,9 @@ int launch_bf16_round(const float *in, uint16_t *out, size_t n, void *stream)
     if (n == 0) return AR_OK;
     size_t blocks = (n + 255) / 256;
     if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(dev::bf16_round_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, in, out, n);
-    return hipGetLastError() == hipSuccess ? AR_OK : AR_ERR_HIP;
+    void *kargs[] = {&in, &out, &n};
+    return hipLaunchKernel((const void *)dev::bf16_round_kernel, dim3((unsigned)blocks), dim3(256), kargs, 0,
+                           (hipStream_t)stream) == hipSuccess ? AR_OK : AR_ERR_HIP;
 }
 
 }  // namespace ar

@@ -177,15 +177,22 @@ int ar_tuner_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
 
 // The closed-loop tuner of the paper's Listing 1 (section 3.3), with its
 // tree choice mapped to this library's small-message algorithm (direct):
-//   * no telemetry entry for the communicator: 4 channels;
-//   * messages of at most 32 KiB use the small-message algorithm, larger
-//     ones the ring; the protocol is Simple;
-//   * when the last recorded latency exceeds 1 ms, use one channel more
-//     than that run had (at most 16), otherwise the same count.
+//   * no telemetry entry for the communicator: 4 channels and nothing else
+//     (algorithm and protocol stay without an opinion, so the library's
+//     default applies);
+//   * otherwise messages of at most 32 KiB use the small-message algorithm,
+//     larger ones the ring, with the Simple protocol, and when the last
+//     recorded latency exceeds 1 ms, one channel more than that run had (at
+//     most 16), otherwise the same count.
 int ar_tuner_size_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
 {
     (void)user;
     if (!ctx || !out) return -1;
+    Entry *e = find(ctx->comm_id, false);
+    if (!e || e->samples.load(std::memory_order_acquire) == 0) {
+        out->nchannels = 4;
+        return 0;
+    }
     out->proto = AR_PROTO_SIMPLE;
     out->chunk_bytes = 0;
     out->nwaves = 0;
@@ -193,11 +200,6 @@ int ar_tuner_size_adaptive(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     out->direct_nwaves = 0;
     out->direct_unroll = 0;
     out->algo = ctx->msg_bytes <= 32u * 1024u ? AR_ALGO_DIRECT : AR_ALGO_RING;
-    Entry *e = find(ctx->comm_id, false);
-    if (!e || e->samples.load(std::memory_order_acquire) == 0) {
-        out->nchannels = 4;
-        return 0;
-    }
     const uint64_t s = e->sample.load(std::memory_order_acquire);
     const uint64_t lat = s & kLatMask;
     int ch = (int)(s >> kLatBits);

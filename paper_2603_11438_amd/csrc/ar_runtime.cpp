@@ -8,6 +8,7 @@
 
 #include "ar.h"
 #include "ar_internal.h"
+#include "ring_gate.h"
 
 using namespace ar;
 
@@ -30,9 +31,6 @@ struct ar_plan_s {
 
 namespace {
 
-constexpr uint32_t kDefaultTimeoutUs = 2000000;  // 2 s per flag wait
-constexpr uint64_t kTicksPerUs = 100;            // 100 MHz real-time counter
-
 template <typename T>
 T *fail(int code)
 {
@@ -50,33 +48,37 @@ size_t round_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
 
 bool overlap2(uintptr_t a, size_t na, uintptr_t b, size_t nb) { return a < b + nb && b < a + na; }
 
+}  // namespace
+
+namespace ar {
+
 // Bytes of each rank's send and recv buffer for the plan's collective.
-void buffer_bytes(const ar_plan_t *p, size_t *send_b, size_t *recv_b)
+void buffer_bytes(const ar_plan_info &g, size_t *send_b, size_t *recv_b)
 {
-    const size_t blk = p->info.count * (p->info.dtype == AR_FLOAT32 ? 4 : 2);
-    const size_t full = p->info.coll == AR_COLL_ALLREDUCE ? blk : blk * (size_t)p->info.nranks;
-    *send_b = p->info.coll == AR_COLL_ALLGATHER ? blk : full;
-    *recv_b = p->info.coll == AR_COLL_REDUCESCATTER ? blk : full;
+    const size_t blk = g.count * (g.dtype == AR_FLOAT32 ? 4 : 2);
+    const size_t full = g.coll == AR_COLL_ALLREDUCE ? blk : blk * (size_t)g.nranks;
+    *send_b = g.coll == AR_COLL_ALLGATHER ? blk : full;
+    *recv_b = g.coll == AR_COLL_REDUCESCATTER ? blk : full;
 }
 
 // Validate rank buffers: non-NULL, 16-byte aligned, and no recv buffer
 // overlapping another rank's send or recv buffer.  A rank's own send and
 // recv buffers may coincide only in the collective's in-place layout.
-int check_buffers(const ar_plan_t *p, const void *const *send, void *const *recv)
+int check_buffers(const ar_plan_info &g, const void *const *send, void *const *recv)
 {
     if (!send || !recv) return AR_ERR_ARG;
-    const int n = p->info.nranks;
+    const int n = g.nranks;
     size_t sb, rb;
-    buffer_bytes(p, &sb, &rb);
+    buffer_bytes(g, &sb, &rb);
     if (sb == 0) return AR_OK;
-    const size_t blk = p->info.count * (p->info.dtype == AR_FLOAT32 ? 4 : 2);
+    const size_t blk = g.count * (g.dtype == AR_FLOAT32 ? 4 : 2);
     for (int r = 0; r < n; ++r) {
         if (!send[r] || !recv[r]) return AR_ERR_ARG;
         if (((uintptr_t)send[r] | (uintptr_t)recv[r]) & 15u) return AR_ERR_ARG;
         const uintptr_t s = (uintptr_t)send[r], d = (uintptr_t)recv[r];
         bool in_place = false;
-        if (p->info.coll == AR_COLL_ALLREDUCE) in_place = s == d;
-        else if (p->info.coll == AR_COLL_REDUCESCATTER) in_place = d == s + (size_t)r * blk;
+        if (g.coll == AR_COLL_ALLREDUCE) in_place = s == d;
+        else if (g.coll == AR_COLL_REDUCESCATTER) in_place = d == s + (size_t)r * blk;
         else in_place = s == d + (size_t)r * blk;
         if (!in_place && overlap2(s, sb, d, rb)) return AR_ERR_ARG;
     }
@@ -104,6 +106,163 @@ int device_channel_capacity(int proto, int dtype, int nranks, int nwaves, int *c
     return AR_OK;
 }
 
+}  // namespace ar
+
+namespace {
+
+// HIP side of the ring launch gate (ring_gate.h).
+struct HipGateApi {
+    using Stream = hipStream_t;
+    using Event = hipEvent_t;
+    static int capturing(Stream s, bool *yes)
+    {
+        hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(s, &st) != hipSuccess) return AR_ERR_HIP;
+        *yes = st != hipStreamCaptureStatusNone;
+        return 0;
+    }
+    static int create(Event *e) { return hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess ? 0 : AR_ERR_HIP; }
+    static int wait(Stream s, Event e) { return hipStreamWaitEvent(s, e, 0) == hipSuccess ? 0 : AR_ERR_HIP; }
+    static int record(Event e, Stream s) { return hipEventRecord(e, s) == hipSuccess ? 0 : AR_ERR_HIP; }
+};
+
+RingGate<HipGateApi> g_ring_gate;
+
+}  // namespace
+
+namespace ar {
+
+// Everything a launch needs besides the plan's memory.
+void fill_args(const ar_plan_info &g, uint32_t debug_flags, uint64_t timeout_ticks, const void *const *send,
+               void *const *recv, char *fifo, uint64_t *flags, uint32_t *ctl, RingArgs *out)
+{
+    RingArgs a;
+    memset(&a, 0, sizeof a);
+    for (int r = 0; r < g.nranks; ++r) {
+        a.src[r] = (const char *)send[r];
+        a.dst[r] = (char *)recv[r];
+    }
+    a.fifo = fifo;
+    a.flags = flags;
+    a.ctl = ctl;
+    a.count = g.coll == AR_COLL_ALLREDUCE ? g.count : g.count * (uint64_t)g.nranks;
+    a.seg = g.seg_elems;
+    {
+        uint64_t full = a.seg ? a.count / a.seg : 0;
+        if (full > (uint64_t)g.nranks) full = (uint64_t)g.nranks;
+        a.full_segs = (uint32_t)full;
+        a.part = full < (uint64_t)g.nranks ? a.count - full * a.seg : 0;
+    }
+    a.coll = (uint32_t)g.coll;
+    a.cs = g.chan_elems;
+    a.chunk = g.chunk_elems;
+    a.kw = g.wave_elems;
+    a.slot_bytes = g.slot_bytes;
+    a.timeout_ticks = timeout_ticks;
+    a.nranks = (uint32_t)g.nranks;
+    a.nchannels = (uint32_t)g.nchannels;
+    a.nwaves = (uint32_t)g.nwaves;
+    a.depth = (uint32_t)g.fifo_depth;
+    a.nchunks = (uint32_t)g.nchunks;
+    a.placement = (uint32_t)g.placement;
+    a.debug = debug_flags;
+    *out = a;
+}
+
+}  // namespace ar
+
+namespace {
+
+// Launch a ring or direct kernel.  A ring launch goes through the device's
+// gate, which keeps ring grids of different streams from overlapping.
+int launch_gated(int dev, const ar_plan_info &g, const RingArgs &a, void *stream)
+{
+    if (g.algo != AR_ALGO_RING) return launch_ring(g, a, stream);
+    RingGate<HipGateApi>::Ticket t;
+    int rc = g_ring_gate.before(dev, (hipStream_t)stream, t);
+    if (rc != 0) return AR_ERR_HIP;
+    rc = launch_ring(g, a, stream);
+    if (rc != AR_OK) return rc;
+    return g_ring_gate.after(t) == 0 ? AR_OK : AR_ERR_HIP;
+}
+
+}  // namespace
+
+namespace ar {
+
+// Resolve a description for the current device: the tuner's choice under
+// the device's channel capacity, re-checked for the resolved protocol and
+// wave count.  *d receives the description the geometry was resolved from.
+int resolve_for_device(const ar_plan_desc *desc, ar_plan_desc *d_out, ar_plan_info *info_out, int *dev_out)
+{
+    ar_plan_desc d = *desc;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return AR_ERR_HIP;
+
+    // Channel capacity for the tuner: co-resident workgroups / nranks, for
+    // the wave count the request implies (the default when the tuner picks).
+    int cap = AR_MAX_CHANNELS;
+    if (d.nranks >= 1 && d.nranks <= AR_MAX_RANKS && (d.dtype == AR_FLOAT32 || d.dtype == AR_BFLOAT16)) {
+        int probe_proto = d.proto == AR_PROTO_AUTO ? AR_PROTO_SIMPLE : d.proto;
+        if (probe_proto != AR_PROTO_LL && probe_proto != AR_PROTO_LL128 && probe_proto != AR_PROTO_SIMPLE)
+            return AR_ERR_ARG;
+        int rc = device_channel_capacity(probe_proto, d.dtype, d.nranks,
+                                         d.nwaves > 0 && d.nwaves <= AR_MAX_WAVES ? d.nwaves : default_nwaves(probe_proto),
+                                         &cap);
+        if (rc != AR_OK) return rc;
+        if (cap < 1) return AR_ERR_OCCUPANCY;
+    }
+    ar_plan_info info;
+    int rc = resolve_geometry(&d, cap, &info);
+    if (rc != AR_OK) return rc;
+    if (info.grid > 0 && info.algo == AR_ALGO_RING) {
+        // Re-check co-residency for the resolved protocol and wave count.
+        int cap2 = 0;
+        rc = device_channel_capacity(info.proto, info.dtype, info.nranks, info.nwaves, &cap2);
+        if (rc != AR_OK) return rc;
+        if (info.nchannels > cap2) {
+            if (d.nchannels != 0) return AR_ERR_OCCUPANCY;
+            d.nchannels = cap2;
+            d.proto = info.proto;
+            d.chunk_bytes = info.chunk_elems * (info.dtype == AR_FLOAT32 ? 4 : 2);
+            d.nwaves = info.nwaves;
+            rc = resolve_geometry(&d, cap2, &info);
+            if (rc != AR_OK) return rc;
+        }
+    }
+    *d_out = d;
+    *info_out = info;
+    *dev_out = dev;
+    return AR_OK;
+}
+
+// Bytes of the ring's device memory: control block, flag lines, FIFO, each
+// part starting on a 256-byte boundary.
+size_t workspace_layout(const ar_plan_info &info, size_t *flags_off, size_t *fifo_off)
+{
+    const size_t ctl_bytes = kCtlU32 * 4;
+    const size_t flag_bytes = round_up(info.flag_bytes - kCtlU32 * 4, 256);
+    *flags_off = ctl_bytes;
+    *fifo_off = ctl_bytes + flag_bytes;
+    return ctl_bytes + flag_bytes + info.fifo_bytes;
+}
+
+}  // namespace ar
+
+namespace {
+
+// Zero device memory and wait for it, without waiting for the rest of the
+// device: the fill goes to a stream of its own, which the host waits for.
+int zero_and_wait(void *p, size_t bytes)
+{
+    hipStream_t s = nullptr;
+    if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) return AR_ERR_HIP;
+    int rc = AR_OK;
+    if (hipMemsetAsync(p, 0, bytes, s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess) rc = AR_ERR_HIP;
+    if (hipStreamDestroy(s) != hipSuccess) rc = AR_ERR_HIP;
+    return rc;
+}
+
 // If the last timed run has finished, record its duration as the plan's
 // latest telemetry sample.  Never blocks.
 void harvest_profile(ar_plan_t *p)
@@ -120,7 +279,7 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
 {
     if (!p) return ret(AR_ERR_ARG);
     if (p->sticky) return ret(AR_ERR_STATE);
-    int rc = check_buffers(p, send, recv);
+    int rc = check_buffers(p->info, send, recv);
     if (rc != AR_OK) return ret(rc);
     const ar_plan_info &g = p->info;
     const size_t bytes = g.count * (g.dtype == AR_FLOAT32 ? 4 : 2);
@@ -133,41 +292,13 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
         return ret(rc);
     }
     RingArgs a;
-    memset(&a, 0, sizeof a);
-    for (int r = 0; r < g.nranks; ++r) {
-        a.src[r] = (const char *)send[r];
-        a.dst[r] = (char *)recv[r];
-    }
-    a.fifo = p->fifo;
-    a.flags = p->flags;
-    a.ctl = p->ctl;
-    a.count = g.coll == AR_COLL_ALLREDUCE ? g.count : g.count * (uint64_t)g.nranks;
-    a.seg = g.seg_elems;
-    {
-        uint64_t full = a.seg ? a.count / a.seg : 0;
-        if (full > (uint64_t)g.nranks) full = (uint64_t)g.nranks;
-        a.full_segs = (uint32_t)full;
-        a.part = full < (uint64_t)g.nranks ? a.count - full * a.seg : 0;
-    }
-    a.coll = (uint32_t)g.coll;
-    a.cs = g.chan_elems;
-    a.chunk = g.chunk_elems;
-    a.kw = g.wave_elems;
-    a.slot_bytes = g.slot_bytes;
-    a.timeout_ticks = p->timeout_ticks;
-    a.nranks = (uint32_t)g.nranks;
-    a.nchannels = (uint32_t)g.nchannels;
-    a.nwaves = (uint32_t)g.nwaves;
-    a.depth = (uint32_t)g.fifo_depth;
-    a.nchunks = (uint32_t)g.nchunks;
-    a.placement = (uint32_t)g.placement;
-    a.debug = p->desc.debug_flags;
+    fill_args(g, p->desc.debug_flags, p->timeout_ticks, send, recv, p->fifo, p->flags, p->ctl, &a);
     bool timed = false;
     if (p->desc.flags & AR_PLAN_PROFILE) {
         harvest_profile(p);
         if (!p->ev_pending && hipEventRecord(p->ev_start, (hipStream_t)stream) == hipSuccess) timed = true;
     }
-    rc = launch_ring(g, a, stream);
+    rc = launch_gated(dev, g, a, stream);
     if (rc != AR_OK) return ret(rc);
     if (timed && hipEventRecord(p->ev_stop, (hipStream_t)stream) == hipSuccess) p->ev_pending = true;
     return AR_OK;
@@ -180,41 +311,11 @@ extern "C" {
 ar_plan_t *ar_plan_ex(const ar_plan_desc *desc)
 {
     if (!desc) return fail<ar_plan_t>(AR_ERR_ARG);
-    ar_plan_desc d = *desc;
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return fail<ar_plan_t>(AR_ERR_HIP);
-
-    // Channel capacity for the tuner: co-resident workgroups / nranks, for
-    // the wave count the request implies (the default when the tuner picks).
-    int cap = AR_MAX_CHANNELS;
-    if (d.nranks >= 1 && d.nranks <= AR_MAX_RANKS && (d.dtype == AR_FLOAT32 || d.dtype == AR_BFLOAT16)) {
-        int probe_proto = d.proto == AR_PROTO_AUTO ? AR_PROTO_SIMPLE : d.proto;
-        if (probe_proto != AR_PROTO_LL && probe_proto != AR_PROTO_LL128 && probe_proto != AR_PROTO_SIMPLE)
-            return fail<ar_plan_t>(AR_ERR_ARG);
-        int rc = device_channel_capacity(probe_proto, d.dtype, d.nranks,
-                                         d.nwaves > 0 && d.nwaves <= AR_MAX_WAVES ? d.nwaves : default_nwaves(probe_proto),
-                                         &cap);
-        if (rc != AR_OK) return fail<ar_plan_t>(rc);
-        if (cap < 1) return fail<ar_plan_t>(AR_ERR_OCCUPANCY);
-    }
+    ar_plan_desc d;
     ar_plan_info info;
-    int rc = resolve_geometry(&d, cap, &info);
+    int dev = 0;
+    int rc = resolve_for_device(desc, &d, &info, &dev);
     if (rc != AR_OK) return fail<ar_plan_t>(rc);
-    if (info.grid > 0 && info.algo == AR_ALGO_RING) {
-        // Re-check co-residency for the resolved protocol and wave count.
-        int cap2 = 0;
-        rc = device_channel_capacity(info.proto, info.dtype, info.nranks, info.nwaves, &cap2);
-        if (rc != AR_OK) return fail<ar_plan_t>(rc);
-        if (info.nchannels > cap2) {
-            if (d.nchannels != 0) return fail<ar_plan_t>(AR_ERR_OCCUPANCY);
-            d.nchannels = cap2;
-            d.proto = info.proto;
-            d.chunk_bytes = info.chunk_elems * (info.dtype == AR_FLOAT32 ? 4 : 2);
-            d.nwaves = info.nwaves;
-            rc = resolve_geometry(&d, cap2, &info);
-            if (rc != AR_OK) return fail<ar_plan_t>(rc);
-        }
-    }
 
     ar_plan_t *p = new (std::nothrow) ar_plan_t;
     if (!p) return fail<ar_plan_t>(AR_ERR_NOMEM);
@@ -231,17 +332,18 @@ ar_plan_t *ar_plan_ex(const ar_plan_desc *desc)
         }
     }
     if (info.grid > 0 && info.algo == AR_ALGO_RING) {
-        const size_t ctl_bytes = kCtlU32 * 4;
-        const size_t flag_bytes = round_up(info.flag_bytes - kCtlU32 * 4, 256);
-        p->ws_bytes = ctl_bytes + flag_bytes + info.fifo_bytes;
+        size_t flags_off = 0, fifo_off = 0;
+        p->ws_bytes = workspace_layout(info, &flags_off, &fifo_off);
         if (hipMalloc((void **)&p->ws, p->ws_bytes) != hipSuccess) {
             delete p;
             return fail<ar_plan_t>(AR_ERR_NOMEM);
         }
         p->ctl = (uint32_t *)p->ws;
-        p->flags = (uint64_t *)(p->ws + ctl_bytes);
-        p->fifo = p->ws + ctl_bytes + flag_bytes;
-        if (hipMemset(p->ws, 0, p->ws_bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+        p->flags = (uint64_t *)(p->ws + flags_off);
+        p->fifo = p->ws + fifo_off;
+        // The workspace must read as zeros before the first run on any
+        // stream; the zeroing waits for itself, not for the whole device.
+        if (zero_and_wait(p->ws, p->ws_bytes) != AR_OK) {
             (void)hipFree(p->ws);
             delete p;
             return fail<ar_plan_t>(AR_ERR_HIP);

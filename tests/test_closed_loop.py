@@ -109,13 +109,20 @@ def test_telemetry_concurrent_under_tsan(tmp_path):
 def test_listing1_policy():
     """The paper's Listing 1 rules over the shared telemetry."""
     ar.ar_set_tuner("size_adaptive")
-    # no map entry: 4 channels; size threshold picks the algorithm
-    d = ar.ar_tune(32 * 1024, comm_id=5)
-    assert (d["nchannels"], d["algo"], d["proto"]) == (4, ar.AR_ALGO_DIRECT, ar.AR_PROTO_SIMPLE)
-    d = ar.ar_tune(32 * 1024 + 1, comm_id=5)
-    assert (d["nchannels"], d["algo"]) == (4, ar.AR_ALGO_RING)
-    # fast runs keep the recorded channel count
+    # no map entry: the listing sets 4 channels and returns, leaving the
+    # algorithm and protocol to the library's default (the Simple ring)
+    raw = ar.ar_tuner_raw("size_adaptive", 32 * 1024, comm_id=5)
+    assert (raw["nchannels"], raw["algo"], raw["proto"]) == (4, ar.AR_ALGO_AUTO, ar.AR_PROTO_AUTO)
+    for size in (4096, 32 * 1024, 1 << 20):
+        d = ar.ar_tune(size, comm_id=5)
+        assert (d["nchannels"], d["algo"], d["proto"]) == (4, ar.AR_ALGO_RING, ar.AR_PROTO_SIMPLE)
+    # with a sample the size threshold picks the algorithm, with Simple
     ar.ar_profile_record(5, 500_000, 6)
+    d = ar.ar_tune(32 * 1024, comm_id=5)
+    assert (d["nchannels"], d["algo"], d["proto"]) == (6, ar.AR_ALGO_DIRECT, ar.AR_PROTO_SIMPLE)
+    d = ar.ar_tune(32 * 1024 + 1, comm_id=5)
+    assert (d["nchannels"], d["algo"], d["proto"]) == (6, ar.AR_ALGO_RING, ar.AR_PROTO_SIMPLE)
+    # fast runs keep the recorded channel count
     assert ar.ar_tune(1 << 20, comm_id=5)["nchannels"] == 6
     # slow runs (> 1 ms) add a channel, up to 16
     ar.ar_profile_record(5, 2_000_000, 6)

@@ -34,10 +34,11 @@ def _bits(ts, dtype):
     return np.stack([to_bits(t, dtype) for t in ts])
 
 
-def _rs_case(ar, n, count, dtype, cfg, in_place, seed):
+def _rs_case(ar, n, count, dtype, cfg, in_place, seed, x=None):
     import torch
 
-    x = draw(n, n * count, dtype, "normal", seed)
+    if x is None:
+        x = draw(n, n * count, dtype, "normal", seed)
     want = ro.reduce_scatter(x, dtype)
     want = want.view(np.uint32) if dtype == "f32" else want
     plan = ar.Plan(n, count, dtype, coll="reducescatter", **cfg)
@@ -96,6 +97,27 @@ def test_reduce_scatter(ar, dtype, n):
     for count in (a, 3 * a, 1000 * a // 8 * 8, 8192):
         for i, cfg in enumerate(CFGS):
             _rs_case(ar, n, count, dtype, cfg, in_place=bool(i % 2), seed=100 * n + count + i)
+
+
+@pytest.mark.parametrize("dtype", ("f32", "bf16"))
+def test_reduce_scatter_order_revealing(ar, dtype):
+    """Order-revealing inputs (large values that cancel, small ones a large
+    partial absorbs; all exact in bf16): block r must be summed along the
+    chain that starts at rank r+1, on the ring under each protocol and on
+    the direct algorithm.  Starting the chains one rank earlier would change
+    many results, which the test checks first."""
+    from tests.test_gpu_parity import order_input
+
+    a = 4 if dtype == "f32" else 8
+    informative = 0
+    for n in (2, 3, 4, 8):
+        for count in (a, 3 * a, 64, 200):
+            x = order_input(n, n * count, dtype, seed=700 + 13 * n + count)
+            want = ro.reduce_scatter(x, dtype)
+            informative += int(np.count_nonzero(want != ro.reduce_scatter(np.roll(x, 1, axis=0), dtype)))
+            for i, cfg in enumerate(CFGS):
+                _rs_case(ar, n, count, dtype, cfg, in_place=bool(i % 2), seed=0, x=x)
+    assert informative > 200, informative
 
 
 @pytest.mark.parametrize("dtype", ("f32", "bf16"))

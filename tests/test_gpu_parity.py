@@ -129,16 +129,53 @@ def test_all_ones_gives_n(ar):
             plan.destroy()
 
 
+ORDER_VALUES = np.array([2.0 ** 24, -(2.0 ** 24), 2.0 ** 25, 1.0, -1.0, 3.0, 0.5], np.float32)
+
+
+def order_input(n, count, dtype, seed):
+    """Order-revealing inputs: large values that cancel and small ones that
+    a large partial absorbs, so different chain orders give different sums.
+    Every value is exact in bf16, so the bf16 case carries the same values."""
+    import torch
+
+    rng = np.random.default_rng(seed)
+    xf = rng.choice(ORDER_VALUES, size=(n, count)).astype(np.float32)
+    if dtype == "f32":
+        return xf
+    xb = torch.from_numpy(xf).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ro.bf16_to_f32(xb), xf)
+    return xb
+
+
 def test_order_revealing_brute_force(ar):
     """Tiny inputs whose chain orders all differ: each element must equal the
     chain that starts at its segment's rank."""
-    vals = np.array([2.0 ** 24, -(2.0 ** 24), 2.0 ** 25, 1.0, -1.0, 3.0, 0.5], np.float32)
     rng = np.random.default_rng(5)
     for n in (2, 3, 4, 8):
         for count in (4, 13, 64, 257):
-            x = rng.choice(vals, size=(n, count)).astype(np.float32)
+            x = rng.choice(ORDER_VALUES, size=(n, count)).astype(np.float32)
             for proto in PROTOS:
                 run_case(ar, x, "f32", f"order-{n}-{count}-{proto}", proto=proto, nchannels=2, chunk_bytes=64)
+
+
+def test_order_revealing_bf16(ar):
+    """bf16 with fp32 accumulation on order-revealing inputs: the chain of
+    every 8-element-aligned segment must start at its own rank and run in
+    ring order, on the ring under each protocol (the Simple ring both
+    peer-direct and FIFO only) and on the direct algorithm.  The inputs are
+    checked to be informative: starting every chain one rank earlier
+    changes many rounded results."""
+    informative = 0
+    cfgs = [dict(proto=p, nchannels=2, chunk_bytes=64) for p in PROTOS]
+    cfgs += [dict(proto="simple", nchannels=3, chunk_bytes=32, flags=2), dict(algo="direct"),
+             dict(algo="direct", nchannels=3, nwaves=1)]
+    for n in (2, 3, 4, 8):
+        for count in (16, 40, 64, 264, 1001):
+            x = order_input(n, count, "bf16", seed=900 + 17 * n + count)
+            informative += int(np.count_nonzero(ro.allreduce_bf16(x) != ro.allreduce_bf16(np.roll(x, 1, axis=0))))
+            for cfg in cfgs:
+                run_case(ar, x, "bf16", f"order-bf16-{n}-{count}-{cfg}", **cfg)
+    assert informative > 200, informative
 
 
 # ------------------------------------------------- layout independence (U1)
@@ -238,7 +275,9 @@ def test_d4_size_sweep_tuned_and_default(ar):
         want = oracle_bits(x, "f32")
         want_dev = torch.from_numpy(want.view(np.float32)).to("cuda:0")
         base = to_device(x, "f32")
-        for cfg in (dict(proto="auto"), dict(proto="simple", nchannels=16)):
+        # the table's overall choice, its ring choice (protocol, channels,
+        # chunk, waves for this size) and the fixed default
+        for cfg in (dict(proto="auto"), dict(proto="auto", algo="ring"), dict(proto="simple", nchannels=16)):
             say(f"D4 {size} {cfg}")
             ts = [t.clone() for t in base]
             plan = ar.Plan(8, wl.count, "f32", **cfg)
