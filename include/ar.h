@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define AR_VERSION 3
+#define AR_VERSION 4
 #define AR_MAX_RANKS 16
 #define AR_MAX_CHANNELS 256
 #define AR_MAX_WAVES 16
@@ -125,7 +125,9 @@ enum {
     AR_ERR_HIP = 4,          /* a HIP runtime call failed */
     AR_ERR_OCCUPANCY = 5,    /* grid cannot be co-resident on the device */
     AR_ERR_TIMEOUT = 6,      /* a flag wait exceeded the watchdog (sticky) */
-    AR_ERR_STATE = 7         /* plan is in an error state; call ar_plan_reset */
+    AR_ERR_STATE = 7,        /* plan is in an error state; call ar_plan_reset */
+    AR_ERR_SCRATCH = 8       /* ar_run_noalloc: the request needs more memory than
+                                the static scratch holds (AR_NOALLOC_SCRATCH_BYTES) */
 };
 
 /* Debug knobs (ar_plan_desc.debug_flags); zero in normal use.
@@ -257,6 +259,33 @@ int ar_run(ar_plan_t *plan, void *const *bufs, void *stream);
  * send[r] + r*count (ReduceScatter) / contain send[r] at recv[r] + r*count
  * (AllGather), the in-place layouts.  Same numerics as ar_run. */
 int ar_run_oop(ar_plan_t *plan, const void *const *send, void *const *recv, void *stream);
+
+/* Bytes of the static scratch that ar_run_noalloc uses on each device. */
+#define AR_NOALLOC_SCRATCH_BYTES (16u << 20)
+
+/* Allocation-free collective, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  It runs the collective `desc` describes (as ar_plan_ex
+ * would plan it: the tuner, defaults and clamps are the same) from send[r]
+ * to recv[r] on `stream`, with the same numerics and buffer rules as
+ * ar_run_oop, and calls no hipMalloc, hipFree, event or stream creation:
+ * the ring's FIFOs, flags and control words live in a static device array
+ * of AR_NOALLOC_SCRATCH_BYTES per device, which every call on that device
+ * shares and which keeps the last call's contents until the process ends.
+ * Each call clears the part it uses with a fill kernel on `stream` (no
+ * memset), so a captured call replays correctly.  Calls whose runs overlap
+ * on one device race on the array: keep them on one stream, or order them.
+ * Ring launches made here are not ordered against other streams' ring
+ * launches (see the conventions above); the caller orders them.
+ * Errors: AR_ERR_SCRATCH when the ring's FIFO, flags and control words need
+ * more than AR_NOALLOC_SCRATCH_BYTES (pick smaller chunks, fewer channels or
+ * waves, or the direct algorithm, which needs no scratch); AR_ERR_UNSUPPORTED
+ * for AR_PLAN_PROFILE (it needs events); otherwise as ar_plan_ex and
+ * ar_run_oop.  A watchdog timeout inside the kernel makes every wave leave
+ * (the output is then undefined) and is not reported: the next call clears
+ * the status word.  The first call on a device looks up that device's copy
+ * of the array (with the device current). */
+int ar_run_noalloc(const ar_plan_desc *desc, const void *const *send, void *const *recv, void *stream);
 
 /* Watchdog status, to be read after the stream has been synchronised:
  * AR_OK, or AR_ERR_TIMEOUT if any wave's flag wait exceeded the watchdog in

@@ -18,14 +18,15 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "_lib", "libar.so")
 
 # ---- constants (include/ar.h) -------------------------------------------
-AR_VERSION = 3  # the interface revision include/ar.h declares
+AR_VERSION = 4  # the interface revision include/ar.h declares
 AR_FLOAT32, AR_BFLOAT16 = 0, 1
 AR_PROTO_AUTO, AR_PROTO_LL, AR_PROTO_LL128, AR_PROTO_SIMPLE = -1, 0, 1, 2
 AR_COLL_ALLREDUCE, AR_COLL_REDUCESCATTER, AR_COLL_ALLGATHER = 0, 1, 2
 COLLS = {"allreduce": AR_COLL_ALLREDUCE, "reducescatter": AR_COLL_REDUCESCATTER, "allgather": AR_COLL_ALLGATHER}
 AR_PLACE_RANK_SPREAD, AR_PLACE_CHANNEL_LOCAL = 0, 1
 (AR_OK, AR_ERR_ARG, AR_ERR_UNSUPPORTED, AR_ERR_NOMEM, AR_ERR_HIP, AR_ERR_OCCUPANCY,
- AR_ERR_TIMEOUT, AR_ERR_STATE) = range(8)
+ AR_ERR_TIMEOUT, AR_ERR_STATE, AR_ERR_SCRATCH) = range(9)
+AR_NOALLOC_SCRATCH_BYTES = 16 << 20
 AR_DEBUG_SKIP_POST, AR_DEBUG_JITTER = 1, 2
 AR_PLAN_PROFILE, AR_PLAN_FIFO_ONLY = 1, 2
 AR_ALGO_AUTO, AR_ALGO_RING, AR_ALGO_DIRECT = 0, 1, 2
@@ -103,6 +104,7 @@ SIGNATURES = {
     "ar_plan_ex": (_P, [ctypes.POINTER(ar_plan_desc)]),
     "ar_run": (ctypes.c_int, [_P, ctypes.POINTER(_P), _P]),
     "ar_run_oop": (ctypes.c_int, [_P, ctypes.POINTER(_P), ctypes.POINTER(_P), _P]),
+    "ar_run_noalloc": (ctypes.c_int, [ctypes.POINTER(ar_plan_desc), ctypes.POINTER(_P), ctypes.POINTER(_P), _P]),
     "ar_plan_status": (ctypes.c_int, [_P]),
     "ar_plan_reset": (ctypes.c_int, [_P]),
     "ar_plan_poison": (ctypes.c_int, [_P, _P]),
@@ -475,6 +477,42 @@ def allreduce(tensors: Sequence, proto="auto", nchannels: int = 0, chunk_bytes: 
         _plan_cache[key] = plan
     plan.run(tensors, stream)
     return plan
+
+
+def run_noalloc(send: Sequence, recv: Optional[Sequence] = None, stream=None, **desc_kw) -> None:
+    """ar_run_noalloc on torch tensors: the collective desc_kw describes
+    (make_desc's keywords; nranks, count and dtype come from the tensors),
+    in place on `send` when recv is None.  Allocates no device memory: the
+    ring uses the library's static scratch."""
+    if not send:
+        raise ValueError("need at least one tensor")
+    coll = desc_kw.get("coll", "allreduce")
+    coll = COLLS[coll] if isinstance(coll, str) else coll
+    n = len(send)
+    t0 = send[0]
+    if recv is None:
+        if coll == AR_COLL_ALLREDUCE:
+            recv = send
+            count = t0.numel()
+        elif coll == AR_COLL_REDUCESCATTER:
+            count = t0.numel() // n
+            recv = [t.view(-1)[r * count:(r + 1) * count] for r, t in enumerate(send)]
+        else:
+            count = t0.numel() // n
+            recv, send = send, [t.view(-1)[r * count:(r + 1) * count] for r, t in enumerate(send)]
+    else:
+        count = t0.numel() if coll != AR_COLL_REDUCESCATTER else t0.numel() // n
+    d = make_desc(n, count, DTYPE_NAMES[_dtype_of(t0)], **desc_kw)
+    full = count if coll == AR_COLL_ALLREDUCE else count * n
+    send_n = count if coll == AR_COLL_ALLGATHER else full
+    recv_n = count if coll == AR_COLL_REDUCESCATTER else full
+    if len(send) != n or len(recv) != n:
+        raise ValueError(f"expected {n} send and {n} recv tensors")
+    for t, numel in [(t, send_n) for t in send] + [(t, recv_n) for t in recv]:
+        if not t.is_cuda or not t.is_contiguous() or _dtype_of(t) != d.dtype or t.numel() != numel:
+            raise ValueError("each tensor must be a contiguous device tensor of the collective's size and dtype")
+    rc = lib().ar_run_noalloc(ctypes.byref(d), _ptr_array(send), _ptr_array(recv), _stream_ptr(stream))
+    _check(rc, "ar_run_noalloc")
 
 
 def ar_debug_bf16_round(x, stream=None):

@@ -12,7 +12,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "libar.so")
 
-SOURCES = ["ar_kernels.hip", "ar_runtime.cpp", "ar_tuner.cpp", "ar_profile.cpp"]
+SOURCES = ["ar_kernels.hip", "ar_runtime.cpp", "ar_tuner.cpp", "ar_profile.cpp", "ar_noalloc.hip"]
 
 # -packed-fp32-ops: no packed fp32 instructions in device code.
 # -ffp-contract=off / no fast-math: every fp32 add is one IEEE RNE operation.

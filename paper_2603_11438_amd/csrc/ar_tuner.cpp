@@ -557,6 +557,7 @@ const char *ar_strerror(int code)
     case AR_ERR_OCCUPANCY: return "grid cannot be co-resident on the device";
     case AR_ERR_TIMEOUT: return "flag wait exceeded the watchdog";
     case AR_ERR_STATE: return "plan is in an error state";
+    case AR_ERR_SCRATCH: return "request needs more than the static scratch of the allocation-free call";
     default: return "unknown error";
     }
 }
