@@ -137,10 +137,25 @@ enum {
  *                       AR_ERR_TIMEOUT.
  *   AR_DEBUG_JITTER     pseudo-random short sleeps before flag posts, to
  *                       shake out ordering races.
+ *   AR_DEBUG_CHECK_LINES  torn / stale line detector for the flag-in-line
+ *                       protocols (LL, LL128; paper section 2): every writer
+ *                       fills each data word of a line with a check word
+ *                       derived from the message's flag and the word's byte
+ *                       offset in the slot, instead of data; every reader,
+ *                       once it has accepted a line by its flag (by the
+ *                       normal protocol code), compares each data word of
+ *                       the line with the check word that flag implies.  A
+ *                       line whose data belongs to another message or
+ *                       another place counts as bad.  Counts are read with
+ *                       ar_plan_debug_stats.  The collective's results are
+ *                       undefined in this mode.  Simple plans ignore it.
+ *   AR_DEBUG_TRACE      channel 0 / wave 0 of every rank writes one record
+ *                       per ring step into the buffer given by
+ *                       ar_plan_debug_trace (see there).
  * A ring plan with any debug flag runs a kernel build that carries these
  * hooks; plans without them run one that does not (the hooks cost time even
  * when not taken). */
-enum { AR_DEBUG_SKIP_POST = 1u, AR_DEBUG_JITTER = 2u };
+enum { AR_DEBUG_SKIP_POST = 1u, AR_DEBUG_JITTER = 2u, AR_DEBUG_CHECK_LINES = 4u, AR_DEBUG_TRACE = 8u };
 
 typedef struct ar_plan_s ar_plan_t;
 
@@ -301,6 +316,36 @@ int ar_plan_reset(ar_plan_t *plan);
  * LL/LL128 flag) on `stream`, leaving the flags intact, so that a reader that
  * consumed a slot before it was written would see NaN.  Call between runs. */
 int ar_plan_poison(ar_plan_t *plan, void *stream);
+
+/* Line-check counts of AR_DEBUG_CHECK_LINES since the plan was created or
+ * last reset, summed over every wave of every run. */
+typedef struct ar_debug_stats {
+    uint64_t lines_checked;    /* LL / LL128 lines accepted by their flag and checked */
+    uint64_t lines_first_read; /* of those, accepted from the first load of the line
+                                  (LL128: data and flag from one 128-byte load) */
+    uint64_t lines_bad;        /* of those, with data not matching the flag */
+} ar_debug_stats;
+
+/* Read the counts (synchronous copy; call after synchronising the plan's
+ * stream).  AR_ERR_ARG for NULL arguments. */
+int ar_plan_debug_stats(ar_plan_t *plan, ar_debug_stats *out);
+
+/* Give an AR_DEBUG_TRACE plan its trace buffer: `buf` is device memory of
+ * `bytes` bytes owned by the caller, kept by the plan until replaced (NULL
+ * stops tracing) and written by every later run.  The buffer is split into
+ * equal shares per rank; rank r's k-th ring step of a run (channel 0,
+ * wave 0) writes record r * per_rank + k, per_rank = bytes / (64 * nranks),
+ * and steps beyond per_rank are not recorded.  A record is eight uint64_t:
+ * t_begin (step entered), t_recv (first data of the step accepted: flag or
+ * counter observed), polls (LL: reloads before the first batch was
+ * accepted; LL128: 1 if the first look at the first batch was stale; Simple
+ * 0), t_issued (the step's, for LL128 its first flag group's, data stores
+ * issued), t_drained (those stores complete; LL 0), t_posted (the flag or
+ * counter that publishes them stored), msg (message index sent, or taken by
+ * a receive-only step), kind (the step's kind).  Times are ticks of the
+ * device's 100 MHz real-time counter, common to all XCDs; fields a step
+ * does not reach stay 0.  AR_ERR_ARG for a NULL plan. */
+int ar_plan_debug_trace(ar_plan_t *plan, void *buf, size_t bytes);
 
 /* Free the plan.  The caller must have synchronised every stream that ran
  * it.  NULL is ignored. */

@@ -27,7 +27,8 @@ AR_PLACE_RANK_SPREAD, AR_PLACE_CHANNEL_LOCAL = 0, 1
 (AR_OK, AR_ERR_ARG, AR_ERR_UNSUPPORTED, AR_ERR_NOMEM, AR_ERR_HIP, AR_ERR_OCCUPANCY,
  AR_ERR_TIMEOUT, AR_ERR_STATE, AR_ERR_SCRATCH) = range(9)
 AR_NOALLOC_SCRATCH_BYTES = 16 << 20
-AR_DEBUG_SKIP_POST, AR_DEBUG_JITTER = 1, 2
+AR_DEBUG_SKIP_POST, AR_DEBUG_JITTER, AR_DEBUG_CHECK_LINES, AR_DEBUG_TRACE = 1, 2, 4, 8
+TRACE_FIELDS = ("t_begin", "t_recv", "polls", "t_issued", "t_drained", "t_posted", "msg", "kind")
 AR_PLAN_PROFILE, AR_PLAN_FIFO_ONLY = 1, 2
 AR_ALGO_AUTO, AR_ALGO_RING, AR_ALGO_DIRECT = 0, 1, 2
 ALGOS = {"auto": AR_ALGO_AUTO, "ring": AR_ALGO_RING, "direct": AR_ALGO_DIRECT}
@@ -66,6 +67,11 @@ class ar_plan_info(ctypes.Structure):
         d["algo_name"] = ALGO_NAMES.get(d["algo"], str(d["algo"]))
         d["dtype_name"] = DTYPE_NAMES.get(d["dtype"], str(d["dtype"]))
         return d
+
+
+class ar_debug_stats(ctypes.Structure):
+    _fields_ = [("lines_checked", ctypes.c_uint64), ("lines_first_read", ctypes.c_uint64),
+                ("lines_bad", ctypes.c_uint64)]
 
 
 class ar_tune_ctx(ctypes.Structure):
@@ -109,6 +115,8 @@ SIGNATURES = {
     "ar_plan_reset": (ctypes.c_int, [_P]),
     "ar_plan_poison": (ctypes.c_int, [_P, _P]),
     "ar_destroy": (None, [_P]),
+    "ar_plan_debug_stats": (ctypes.c_int, [_P, ctypes.POINTER(ar_debug_stats)]),
+    "ar_plan_debug_trace": (ctypes.c_int, [_P, _P, ctypes.c_size_t]),
     "ar_plan_get_info": (ctypes.c_int, [_P, ctypes.POINTER(ar_plan_info)]),
     "ar_plan_workspace_bytes": (ctypes.c_size_t, [_P]),
     "ar_plan_geometry": (ctypes.c_int, [ctypes.POINTER(ar_plan_desc), ctypes.POINTER(ar_plan_info)]),
@@ -433,6 +441,21 @@ class Plan:
 
     def poison(self, stream=None) -> None:
         _check(lib().ar_plan_poison(self._h, _stream_ptr(stream)), "ar_plan_poison")
+
+    def debug_stats(self) -> dict:
+        """Line-check counts of AR_DEBUG_CHECK_LINES (after synchronising)."""
+        st = ar_debug_stats()
+        _check(lib().ar_plan_debug_stats(self._h, ctypes.byref(st)), "ar_plan_debug_stats")
+        return {"lines_checked": st.lines_checked, "lines_first_read": st.lines_first_read,
+                "lines_bad": st.lines_bad}
+
+    def set_trace(self, buf) -> None:
+        """Give an AR_DEBUG_TRACE plan its record buffer (a device tensor,
+        kept alive by the plan; None stops tracing)."""
+        self._trace_buf = buf
+        ptr = None if buf is None else buf.data_ptr()
+        nbytes = 0 if buf is None else buf.numel() * buf.element_size()
+        _check(lib().ar_plan_debug_trace(self._h, ptr, nbytes), "ar_plan_debug_trace")
 
     @property
     def workspace_bytes(self) -> int:

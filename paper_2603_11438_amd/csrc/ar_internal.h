@@ -22,6 +22,13 @@ constexpr int kEpochU64 = 8;                     // epoch: byte 64 of the tail l
 constexpr int kCtlU32 = 64;                      // control block: 256 bytes
 constexpr int kCtlAbort = 0;                     // nonzero: every wave must leave
 constexpr int kCtlStatus = 32;                   // sticky AR_ERR_* bit set
+// Line-check counters of AR_DEBUG_CHECK_LINES, 64-bit, at these u32 indices
+// (bytes 64..87, a line of their own).
+constexpr int kCtlLinesChecked = 16;             // LL / LL128 lines accepted and checked
+constexpr int kCtlLinesFirst = 18;               // of those, accepted on the first load
+constexpr int kCtlLinesBad = 20;                 // of those, data not matching the flag
+// A step record of AR_DEBUG_TRACE: this many 64-bit fields.
+constexpr int kTraceFields = 8;
 
 // Status bits written by the kernel into ctl[kCtlStatus].
 constexpr uint32_t kStatusTimeout = 1u;
@@ -47,6 +54,9 @@ struct RingArgs {
     uint32_t coll;                   // AR_COLL_*: which steps of the ring run
     uint32_t full_segs;              // segments 0 .. full_segs-1 hold seg elements; segment
                                      // full_segs holds part, any later one none
+    uint64_t *trace;                 // AR_DEBUG_TRACE: step records, rank r's at
+                                     // [r * trace_per_rank, (r + 1) * trace_per_rank)
+    uint32_t trace_per_rank;         // records per rank (0: none kept)
 };
 
 // Resolved plan geometry.  Computed on the host only.

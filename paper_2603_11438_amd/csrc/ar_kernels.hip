@@ -324,6 +324,54 @@ __device__ __forceinline__ void debug_jitter(const RingArgs &a, uint64_t salt)
     for (uint32_t i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(8);
 }
 
+// ---- debug state (kernel builds with the debug hooks only) -----------------
+
+// One step's record of AR_DEBUG_TRACE, stamped with the 100 MHz real-time
+// counter (the same clock on every XCD).  Fields, in order:
+//   t_begin   step entered
+//   t_recv    first data of the step accepted (flag or counter observed)
+//   polls     LL: reloads before the first batch was accepted; LL128: 1 if
+//             the first look at the first batch was stale; Simple: 0
+//   t_issued  the step's (first drain group's) data stores issued
+//   t_drained those stores complete (Simple, LL128; LL has no drain: 0)
+//   t_posted  the flag / counter that publishes them stored
+//   msg       index of the message sent (or, for a receive-only step, taken)
+//   kind      the step kind (Kind)
+struct StepTrace {
+    uint64_t t_begin, t_recv, polls, t_issued, t_drained, t_posted, msg, kind;
+};
+
+struct DbgState {
+    bool check;            // AR_DEBUG_CHECK_LINES
+    bool trace;            // AR_DEBUG_TRACE, and this wave is channel 0 / wave 0
+    uint32_t checked;      // lines accepted and checked
+    uint32_t first;        // of those, accepted on the first load
+    uint32_t bad;          // of those, with data not matching the flag
+    uint32_t step;         // steps of this run so far (trace index)
+    StepTrace tr;
+};
+
+__device__ __forceinline__ uint64_t now_ticks() { return uniform64(wall_clock64()); }
+
+// AR_DEBUG_CHECK_LINES: the data word a writer stores at byte `off` of a
+// slot for the message whose 32-bit flag is `tag`.  For a fixed offset it is
+// a bijection of the tag (an odd multiplier, then fixed terms), so data left
+// by any other message never matches; for a fixed tag it changes with the
+// offset, so misplaced data does not match either.
+__device__ __forceinline__ uint32_t check_word(uint32_t tag, uint32_t off)
+{
+    return (tag * 0x9E3779B1u) ^ (off * 0x85EBCA6Bu) ^ 0x5BD1E995u;
+}
+
+// Lines with any bit set in an 8-lane group of a 64-lane mask.
+__device__ __forceinline__ uint32_t groups8_set(uint64_t m)
+{
+    m |= m >> 4;
+    m |= m >> 2;
+    m |= m >> 1;
+    return (uint32_t)__builtin_popcountll(m & 0x0101010101010101ull);
+}
+
 // ---- per-wave ring state ---------------------------------------------------
 
 struct Ring {
@@ -336,6 +384,7 @@ struct Ring {
     uint64_t m_out, m_in;           // absolute index of the next message out / in
     uint64_t head_seen, tail_seen;  // last counter values observed
     uint32_t slot_out, slot_in;     // FIFO slot of message m_out / m_in: m mod depth
+    DbgState dbg;                   // used by the builds with the debug hooks only
 };
 
 // LL flag of message m: the low 32 bits of m + 1.  A line left in a slot by
@@ -602,6 +651,8 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
         if (!wait_geq2(a, g.tail_in, g.m_in + 1, g.tail_seen, credit ? g.head_out : nullptr,
                        g.m_out + 1 - a.depth, g.head_seen))
             return false;
+        if constexpr (DBG)
+            if (g.dbg.trace) g.dbg.tr.t_recv = now_ticks();
         rslot = fifo_in ? slot_ptr(const_cast<char *>(g.fifo_in), g.slot_in, a) : dst;
     }
     if (KindTraits<KIND>::kRecvPeer) rslot = peer_src;
@@ -610,11 +661,17 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
         wslot = fifo_out ? slot_ptr(g.fifo_out, g.slot_out, a) : peer_dst;
     }
     SimpleStep<DT, KIND, DAG>::run(a, src, dst, rslot, wslot, len);
+    if constexpr (DBG)
+        if (g.dbg.trace) g.dbg.tr.t_issued = now_ticks();
     // Slot writes (and slot reads) complete before either counter moves.
     drain_vmem();
+    if constexpr (DBG)
+        if (g.dbg.trace) g.dbg.tr.t_drained = now_ticks();
     if (send) {
         if constexpr (DBG) debug_jitter(a, g.m_out ^ ((uint64_t)g.r << 40) ^ ((uint64_t)g.c << 48));
         if (!(DBG && skip_this_post(g))) flag_store(g.tail_out, g.m_out + 1);
+        if constexpr (DBG)
+            if (g.dbg.trace) g.dbg.tr.t_posted = now_ticks();
         advance_out(g);
     }
     if (recv) {
@@ -633,7 +690,7 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
 // fp32 or 4 bf16): input/output 8 bytes, RS wire G lines (placed by
 // wide_off), AG wire 2 lines (16 bytes).
 
-template <int DT, int KIND>
+template <int DT, int KIND, bool DBG>
 struct LLStep {
     static constexpr uint32_t E = Elem<DT>::E;
     static constexpr uint32_t G = 8 / E;         // elements per group
@@ -670,9 +727,10 @@ struct LLStep {
     __device__ static bool lines_ok(const u32x4 &l, uint32_t tag) { return l[1] == tag && l[3] == tag; }
 
     // One group's arithmetic and stores; ok = false sends every access out
-    // of range (a lane past the end of the message).
+    // of range (a lane past the end of the message).  chk (debug builds
+    // only): the wire carries check words instead of data.
     __device__ static void group(Rsrc rout, Rsrc wo, uint32_t q, bool ok, uint32_t valid, uint32_t ng,
-                                 u32x2 in, const u32x4 *rs, const u32x4 &ag, uint32_t tag_out)
+                                 u32x2 in, const u32x4 *rs, const u32x4 &ag, uint32_t tag_out, bool chk)
     {
         float acc[G];
         if (kSendRS || kReduceToY) {
@@ -694,8 +752,10 @@ struct LLStep {
         }
         if (kSendRS) {
             for (uint32_t v = 0; v < RSV; ++v) {
+                const uint32_t off = wide_off(q, v, RSV, ng);
                 u32x4 o = {as_u32(acc[2 * v]), tag_out, as_u32(acc[2 * v + 1]), tag_out};
-                st128<kFifoSt>(wo, in_range(ok, wide_off(q, v, RSV, ng)), o);
+                if (DBG && chk) o = u32x4{check_word(tag_out, off), tag_out, check_word(tag_out, off + 8), tag_out};
+                st128<kFifoSt>(wo, in_range(ok, off), o);
             }
         }
         u32x2 y;
@@ -711,16 +771,35 @@ struct LLStep {
             if (valid == G) st64<kOutPol>(rout, in_range(ok, q * 8), y);
             else store_part(rout, q, y, valid, ok);
         }
-        if (kSendAG) st128<kFifoSt>(wo, in_range(ok, q * 16), u32x4{y[0], tag_out, y[1], tag_out});
+        if (kSendAG) {
+            u32x4 o = {y[0], tag_out, y[1], tag_out};
+            if (DBG && chk) o = u32x4{check_word(tag_out, q * 16), tag_out, check_word(tag_out, q * 16 + 8), tag_out};
+            st128<kFifoSt>(wo, in_range(ok, q * 16), o);
+        }
+    }
+
+    // Debug builds: check the data words of the lines a lane accepted (two
+    // lines per 16-byte access) against the writer's check words.
+    __device__ static void check_access(const u32x4 &l, uint32_t off, bool ok, uint32_t tag, uint32_t first,
+                                        DbgState *dbg)
+    {
+        const bool bad0 = ok && l[0] != check_word(tag, off);
+        const bool bad1 = ok && l[2] != check_word(tag, off + 8);
+        const uint32_t n = 2 * (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(ok));
+        dbg->checked += n;
+        dbg->first += first ? n : 0u;
+        dbg->bad += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(bad0)) +
+                    (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(bad1));
     }
 
     // Full groups go in batches of U per lane as straight-line code (lanes
     // past the end use out-of-range offsets); a partial last group is done
     // afterwards by one lane, with its own poll.
     __device__ static bool run(const RingArgs &a, const char *src, char *dst, const char *rslot,
-                               char *wslot, uint32_t len, uint32_t tag_in, uint32_t tag_out)
+                               char *wslot, uint32_t len, uint32_t tag_in, uint32_t tag_out, DbgState *dbg)
     {
         const uint32_t lane = step_lane();
+        const bool chk = DBG && dbg->check;
         const uint32_t nfg = len / G, rem = len % G;
         const uint32_t ng = nfg + (rem ? 1u : 0u);
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
@@ -745,6 +824,7 @@ struct LLStep {
                 // flag, reloading all of them each time (a line that is
                 // already valid cannot change before this wave frees the slot).
                 Watchdog wd;
+                uint32_t reloads = 0;
                 while (true) {
                     bool bad = false;
 #pragma unroll
@@ -757,6 +837,7 @@ struct LLStep {
                     if (!any_lane(bad)) break;
                     __builtin_amdgcn_s_sleep(1);
                     if (watchdog_expired(a, wd)) return false;
+                    ++reloads;
 #pragma unroll
                     for (int t = 0; t < U; ++t) {
                         const uint32_t q = base + 64 * t + lane;
@@ -767,11 +848,28 @@ struct LLStep {
                         if (kRecvAG) ag[t] = ld128<kFifoLd>(wi, in_range(ok, q * 16));
                     }
                 }
+                if constexpr (DBG) {
+                    if (dbg->trace && dbg->tr.t_recv == 0) {
+                        dbg->tr.t_recv = now_ticks();
+                        dbg->tr.polls = reloads;
+                    }
+                    if (chk) {
+#pragma unroll
+                        for (int t = 0; t < U; ++t) {
+                            const uint32_t q = base + 64 * t + lane;
+                            const bool ok = q < nfg;
+                            if (kRecvRS)
+                                for (uint32_t v = 0; v < RSV; ++v)
+                                    check_access(rs[t][v], wide_off(q, v, RSV, ng), ok, tag_in, reloads == 0, dbg);
+                            if (kRecvAG) check_access(ag[t], q * 16, ok, tag_in, reloads == 0, dbg);
+                        }
+                    }
+                }
             }
 #pragma unroll
             for (int t = 0; t < U; ++t) {
                 const uint32_t q = base + 64 * t + lane;
-                group(rout, wo, q, q < nfg, G, ng, in[t], rs[t], ag[t], tag_out);
+                group(rout, wo, q, q < nfg, G, ng, in[t], rs[t], ag[t], tag_out, chk);
             }
         }
         if (rem) {
@@ -784,6 +882,7 @@ struct LLStep {
             if (kLoadIn) in = load_part(rin, q, rem, me);
             if (kRecvRS || kRecvAG) {
                 Watchdog wd;
+                uint32_t reloads = 0;
                 while (true) {
                     bool bad = false;
                     if (kRecvRS)
@@ -798,9 +897,22 @@ struct LLStep {
                     if (!any_lane(bad)) break;
                     __builtin_amdgcn_s_sleep(1);
                     if (watchdog_expired(a, wd)) return false;
+                    ++reloads;
+                }
+                if constexpr (DBG) {
+                    if (dbg->trace && dbg->tr.t_recv == 0) {
+                        dbg->tr.t_recv = now_ticks();
+                        dbg->tr.polls = reloads;
+                    }
+                    if (chk) {
+                        if (kRecvRS)
+                            for (uint32_t v = 0; v < RSV; ++v)
+                                check_access(rs[v], wide_off(q, v, RSV, ng), me, tag_in, reloads == 0, dbg);
+                        if (kRecvAG) check_access(ag, q * 16, me, tag_in, reloads == 0, dbg);
+                    }
                 }
             }
-            group(rout, wo, q, me, rem, ng, in, rs, ag, tag_out);
+            group(rout, wo, q, me, rem, ng, in, rs, ag, tag_out, chk);
         }
         return true;
     }
@@ -825,7 +937,9 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
     // the receiver never accepts for this message.
     const bool skip = DBG && send && skip_this_post(g);
     const uint32_t tag_out = ll_tag(skip ? g.m_out - 1 : g.m_out);
-    if (!LLStep<DT, KIND>::run(a, src, dst, rslot, wslot, len, ll_tag(g.m_in), tag_out)) return false;
+    if (!LLStep<DT, KIND, DBG>::run(a, src, dst, rslot, wslot, len, ll_tag(g.m_in), tag_out, &g.dbg)) return false;
+    if constexpr (DBG)
+        if (g.dbg.trace) g.dbg.tr.t_issued = g.dbg.tr.t_posted = now_ticks();
     if (send) advance_out(g);
     if (recv) {
         // Every line of the message has been loaded and its flag checked, so
@@ -863,7 +977,7 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
 
 constexpr uint32_t kLL128Data = 120;
 
-template <int DT, int KIND>
+template <int DT, int KIND, bool DBG>
 struct LL128Step {
     static constexpr uint32_t E = Elem<DT>::E;
     static constexpr bool kRecvRS = KindTraits<KIND>::kRecvRS;
@@ -1054,9 +1168,11 @@ struct LL128Step {
     }
     template <int NB>
     __device__ static bool await_lines(const RingArgs &a, Rsrc wi, u32x4 *lines, const uint32_t *line_of,
-                                       const bool *act, uint64_t tag, uint32_t first, uint32_t nlines)
+                                       const bool *act, uint64_t tag, uint32_t first, uint32_t nlines,
+                                       bool &was_stale)
     {
-        if (stale_lines<NB>(lines, act, step_lane() & 7u, tag)) {
+        was_stale = stale_lines<NB>(lines, act, step_lane() & 7u, tag);
+        if (was_stale) {
             if (!poll_flags<NB>(a, wi, first, nlines, tag)) return false;
 #pragma unroll
             for (int t = 0; t < NB; ++t)
@@ -1066,11 +1182,38 @@ struct LL128Step {
         return true;
     }
 
+    // Debug builds (AR_DEBUG_CHECK_LINES): the check words lane part p of
+    // `line` carries for the message with flag `tag` (lane 7: words 0..1).
+    __device__ static u32x4 check_part(uint32_t tag, uint32_t line, uint32_t p)
+    {
+        const uint32_t b = line * 128 + 16 * p;
+        return u32x4{check_word(tag, b), check_word(tag, b + 4), check_word(tag, b + 8), check_word(tag, b + 12)};
+    }
+    // Check every accepted line of a batch against the writer's check words:
+    // a line counts as bad if any of its eight lane parts differs.
+    template <int NB>
+    __device__ static void check_lines(const u32x4 *lines, const uint32_t *line_of, const bool *act, uint32_t p,
+                                       uint32_t tag, bool first, DbgState *dbg)
+    {
+#pragma unroll
+        for (int t = 0; t < NB; ++t) {
+            const u32x4 w = check_part(tag, line_of[t], p);
+            const bool bad = act[t] && (lines[t][0] != w[0] || lines[t][1] != w[1] ||
+                                        (p < 7 && (lines[t][2] != w[2] || lines[t][3] != w[3])));
+            const uint32_t n = (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(act[t] && p == 7));
+            dbg->checked += n;
+            dbg->first += first ? n : 0u;
+            dbg->bad += groups8_set(__builtin_amdgcn_ballot_w64(bad));
+        }
+    }
+
     __device__ static bool run(const RingArgs &a, const char *src, char *dst, const char *rslot,
-                               char *wslot, uint32_t len, uint64_t tag_in, uint64_t tag_out, uint32_t *lds)
+                               char *wslot, uint32_t len, uint64_t tag_in, uint64_t tag_out, uint32_t *lds,
+                               DbgState *dbg)
     {
         const uint32_t lane = step_lane();
         const uint32_t p = lane & 7u, ls = lane >> 3;
+        const bool chk = DBG && dbg->check;
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
         const Rsrc wi = make_rsrc(rslot, a.slot_bytes);
@@ -1113,7 +1256,15 @@ struct LL128Step {
 #pragma unroll
                     for (int t = 0; t < U; ++t) unit(base, t, line_of[t], act[t], nval[t]);
                     if (kRecvRS || kRecvAG) {
-                        if (!await_lines<U>(a, wi, wire, line_of, act, tag_in, base, nlines)) return false;
+                        bool stale = false;
+                        if (!await_lines<U>(a, wi, wire, line_of, act, tag_in, base, nlines, stale)) return false;
+                        if constexpr (DBG) {
+                            if (dbg->trace && dbg->tr.t_recv == 0) {
+                                dbg->tr.t_recv = now_ticks();
+                                dbg->tr.polls = stale ? 1u : 0u;
+                            }
+                            if (chk) check_lines<U>(wire, line_of, act, p, (uint32_t)tag_in, !stale, dbg);
+                        }
                     }
                     // All inputs in place before the first store: a cut-part
                     // load between stores would make the stores wait.
@@ -1147,7 +1298,7 @@ struct LL128Step {
                                 store_part<epart>(rout, e0 * E, out, p, nval[t], full);
                             }
                         }
-                        if (kSendRS || kSendAG) put_data(wo, line_of[t], p, act[t], out);
+                        if (kSendRS || kSendAG) put_data(wo, line_of[t], p, act[t], chk ? check_part((uint32_t)tag_out, line_of[t], p) : out);
                     }
 #pragma unroll
                     for (int t = 0; t < U; ++t) {
@@ -1156,8 +1307,14 @@ struct LL128Step {
                     }
                 }
                 if (kSendRS || kSendAG) {
+                    if constexpr (DBG)
+                        if (dbg->trace && dbg->tr.t_issued == 0) dbg->tr.t_issued = now_ticks();
                     drain_vmem();
+                    if constexpr (DBG)
+                        if (dbg->trace && dbg->tr.t_drained == 0) dbg->tr.t_drained = now_ticks();
                     put_flags(wo, gbase, gend, lane, tag_out);
+                    if constexpr (DBG)
+                        if (dbg->trace && dbg->tr.t_posted == 0) dbg->tr.t_posted = now_ticks();
                 }
             }
             return true;
@@ -1182,7 +1339,15 @@ struct LL128Step {
                         in[t] = load_whole<4>(rin, e0 * E, p, nval[t], full);
                         wire[t] = ld128<kFifoLd>(wi, in_range(act[t], line_of[t] * 128 + 16 * p));
                     }
-                    if (!await_lines<2>(a, wi, wire, line_of, act, tag_in, 2 * agb, rs_nlines)) return false;
+                    bool stale = false;
+                    if (!await_lines<2>(a, wi, wire, line_of, act, tag_in, 2 * agb, rs_nlines, stale)) return false;
+                    if constexpr (DBG) {
+                        if (dbg->trace && dbg->tr.t_recv == 0) {
+                            dbg->tr.t_recv = now_ticks();
+                            dbg->tr.polls = stale ? 1u : 0u;
+                        }
+                        if (chk) check_lines<2>(wire, line_of, act, p, (uint32_t)tag_in, !stale, dbg);
+                    }
     #pragma unroll
                     for (int t = 0; t < 2; ++t) {
                         // Element index of this lane's first value within the 480-block.
@@ -1208,15 +1373,21 @@ struct LL128Step {
                         y[3] = lds[loc / 2 + 3];
                     }
                     store_part<8>(rout, e0 * E, y, p, n2, full2);
-                    put_data(wo, line, p, act2, y);
+                    put_data(wo, line, p, act2, chk ? check_part((uint32_t)tag_out, line, p) : y);
                     // LDS is rewritten by the next round only after every lane has read it.
                     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
                     __builtin_amdgcn_wave_barrier();
                     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
                 }
+                if constexpr (DBG)
+                    if (dbg->trace && dbg->tr.t_issued == 0) dbg->tr.t_issued = now_ticks();
                 drain_vmem();
+                if constexpr (DBG)
+                    if (dbg->trace && dbg->tr.t_drained == 0) dbg->tr.t_drained = now_ticks();
                 const uint32_t gend = gbase + 8 * kGroup < nlines_ag ? gbase + 8 * kGroup : nlines_ag;
                 put_flags(wo, gbase, gend, lane, tag_out);
+                if constexpr (DBG)
+                    if (dbg->trace && dbg->tr.t_posted == 0) dbg->tr.t_posted = now_ticks();
             }
             return true;
         }
@@ -1245,7 +1416,7 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
     const bool skip = DBG && send && skip_this_post(g);
     // A skipped post: write the data but a flag from the previous message.
     const uint64_t tag_out = skip ? g.m_out : g.m_out + 1;
-    if (!LL128Step<DT, KIND>::run(a, src, dst, rslot, wslot, len, g.m_in + 1, tag_out, lds)) return false;
+    if (!LL128Step<DT, KIND, DBG>::run(a, src, dst, rslot, wslot, len, g.m_in + 1, tag_out, lds, &g.dbg)) return false;
     if (send) advance_out(g);
     if (recv) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -1257,13 +1428,54 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
 
 // ===================================================================== kernel
 
+// Debug builds: store the step's trace record, one field per store from
+// lane 0 (records beyond the rank's share of the buffer are dropped).  A
+// field picked by lane index would read the record as an array with a
+// variable index, which puts it, and everything it lives in, into scratch.
+__device__ __forceinline__ void write_trace(const Ring &g)
+{
+    const RingArgs &a = *g.a;
+    const bool keep = lane_id() == 0 && g.dbg.step < a.trace_per_rank;
+    const uint64_t rec = (uint64_t)g.r * a.trace_per_rank + g.dbg.step;
+    const Rsrc rt = make_rsrc(a.trace + rec * kTraceFields, kTraceFields * 8);
+    const StepTrace &t = g.dbg.tr;
+    auto put = [&](uint32_t i, uint64_t v) {
+        st64<kPolPlain>(rt, in_range(keep, i * 8), u32x2{(uint32_t)v, (uint32_t)(v >> 32)});
+    };
+    put(0, t.t_begin);
+    put(1, t.t_recv);
+    put(2, t.polls);
+    put(3, t.t_issued);
+    put(4, t.t_drained);
+    put(5, t.t_posted);
+    put(6, t.msg);
+    put(7, t.kind);
+}
+
 template <int PROTO, int DT, bool DAG, bool DBG, int KIND>
 __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, char *peer_dst, const char *peer_src,
                                         uint32_t len, uint32_t *lds)
 {
-    if (PROTO == AR_PROTO_SIMPLE) return simple_step<DT, KIND, DAG, DBG>(g, src, dst, peer_dst, peer_src, len);
-    if (PROTO == AR_PROTO_LL) return ll_step<DT, KIND, DBG>(g, src, dst, len);
-    return ll128_step<DT, KIND, DBG>(g, src, dst, len, lds);
+    if constexpr (DBG) {
+        if (g.dbg.trace) {
+            g.dbg.tr = StepTrace{};
+            g.dbg.tr.t_begin = now_ticks();
+            g.dbg.tr.kind = KIND;
+            constexpr bool send = KindTraits<KIND>::kSendRS || KindTraits<KIND>::kSendAG;
+            g.dbg.tr.msg = send ? g.m_out : g.m_in;
+        }
+    }
+    bool ok;
+    if (PROTO == AR_PROTO_SIMPLE) ok = simple_step<DT, KIND, DAG, DBG>(g, src, dst, peer_dst, peer_src, len);
+    else if (PROTO == AR_PROTO_LL) ok = ll_step<DT, KIND, DBG>(g, src, dst, len);
+    else ok = ll128_step<DT, KIND, DBG>(g, src, dst, len, lds);
+    if constexpr (DBG) {
+        if (g.dbg.trace) {
+            write_trace(g);
+            ++g.dbg.step;
+        }
+    }
+    return ok;
 }
 
 // All steps of one run for one wave; false if the wave had to give up.
@@ -1420,11 +1632,28 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
     g.tail_seen = 0;
     uint32_t *lds = lds_all + ((PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? w * kLdsWordsPerWave : 0);
 
+    g.dbg = DbgState{};
+    if constexpr (DBG) {
+        g.dbg.check = (a.debug & AR_DEBUG_CHECK_LINES) != 0 && PROTO != AR_PROTO_SIMPLE;
+        g.dbg.trace = (a.debug & AR_DEBUG_TRACE) != 0 && a.trace != nullptr && c == 0 && w == 0;
+    }
+
     // A previous run that timed out leaves the abort word raised: do nothing.
     if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED,
                                                          __HIP_MEMORY_SCOPE_AGENT)) != 0)
         return;
     ring_steps<PROTO, DT, DAG, DBG>(g, lds);
+    if constexpr (DBG) {
+        // One lane adds the wave's line-check counts (nothing follows).
+        if (g.dbg.check && lane_id() == 0) {
+            uint64_t *cnt = (uint64_t *)(a.ctl + kCtlLinesChecked);
+            __hip_atomic_fetch_add(cnt, (uint64_t)g.dbg.checked, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            cnt = (uint64_t *)(a.ctl + kCtlLinesFirst);
+            __hip_atomic_fetch_add(cnt, (uint64_t)g.dbg.first, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            cnt = (uint64_t *)(a.ctl + kCtlLinesBad);
+            __hip_atomic_fetch_add(cnt, (uint64_t)g.dbg.bad, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
 }
 
 // ===================================================================== direct

@@ -27,6 +27,9 @@ struct ar_plan_s {
     // timed launch, harvested without blocking.
     hipEvent_t ev_start, ev_stop;
     bool ev_pending;
+    // AR_DEBUG_TRACE: the caller's record buffer.
+    uint64_t *trace;
+    uint32_t trace_per_rank;
 };
 
 namespace {
@@ -293,6 +296,8 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
     }
     RingArgs a;
     fill_args(g, p->desc.debug_flags, p->timeout_ticks, send, recv, p->fifo, p->flags, p->ctl, &a);
+    a.trace = p->trace;
+    a.trace_per_rank = p->trace ? p->trace_per_rank : 0;
     bool timed = false;
     if (p->desc.flags & AR_PLAN_PROFILE) {
         harvest_profile(p);
@@ -426,6 +431,29 @@ int ar_plan_poison(ar_plan_t *p, void *stream)
     if (!p) return ret(AR_ERR_ARG);
     if (!p->fifo || p->info.fifo_bytes == 0) return AR_OK;
     return ret(launch_fill_u32((uint32_t *)p->fifo, p->info.fifo_bytes / 4, 0xFFFFFFFFu, stream));
+}
+
+int ar_plan_debug_stats(ar_plan_t *p, ar_debug_stats *out)
+{
+    if (!p || !out) return ret(AR_ERR_ARG);
+    memset(out, 0, sizeof *out);
+    if (!p->ctl) return AR_OK;
+    uint64_t v[3] = {0, 0, 0};
+    if (hipMemcpy(v, p->ctl + kCtlLinesChecked, sizeof v, hipMemcpyDeviceToHost) != hipSuccess) return ret(AR_ERR_HIP);
+    out->lines_checked = v[0];
+    out->lines_first_read = v[1];
+    out->lines_bad = v[2];
+    return AR_OK;
+}
+
+int ar_plan_debug_trace(ar_plan_t *p, void *buf, size_t bytes)
+{
+    if (!p) return ret(AR_ERR_ARG);
+    const size_t per = buf ? bytes / ((size_t)kTraceFields * 8 * (size_t)p->info.nranks) : 0;
+    if (buf && ((uintptr_t)buf & 7u)) return ret(AR_ERR_ARG);
+    p->trace = per ? (uint64_t *)buf : nullptr;
+    p->trace_per_rank = per > 0xFFFFFFFFu ? 0xFFFFFFFFu : (uint32_t)per;
+    return AR_OK;
 }
 
 void ar_destroy(ar_plan_t *p)
