@@ -59,15 +59,6 @@ typedef __amdgpu_buffer_rsrc_t Rsrc;
 
 // Cache-policy operand of gfx950 buffer instructions.
 enum : int { kPolPlain = 0, kPolSc0 = 1, kPolNt = 2, kPolSc1 = 16 };
-#ifndef AR_SIMPLE_U
-#define AR_SIMPLE_U 4
-#endif
-#ifndef AR_LL128_U
-#define AR_LL128_U 2
-#endif
-#ifndef AR_LL128_GROUP
-#define AR_LL128_GROUP 8
-#endif
 // The policies are fixed, not build options.  A FIFO line (or, in the
 // peer-direct mode, an output element) is written on one XCD and read on
 // another, behind a different L2; without the device-scope bit on both the
@@ -485,7 +476,7 @@ struct SimpleStep {
     static constexpr bool kReduceToY = KindTraits<KIND>::kReduceToY;
     static constexpr bool kCopyInToY = KindTraits<KIND>::kCopyInToY;
     static constexpr bool kRecvPeer = KindTraits<KIND>::kRecvPeer;
-    static constexpr int U = AR_SIMPLE_U;
+    static constexpr int U = 4;
     // With DAG a received all-gather message is already in the own output.
     static constexpr bool kWriteOwn = kWriteOut && !(DAG && kRecvAG);
     static constexpr int kOwnPol = DAG ? kFifoSt : kOutPol;  // own output stores
@@ -977,7 +968,12 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
 
 constexpr uint32_t kLL128Data = 120;
 
-template <int DT, int KIND, bool DBG>
+// LU: 16-byte accesses per lane and batch (8 lines each per wave), chosen
+// per plan: 2 when a wave's message spans at most one such batch (16
+// lines: fewer instructions and registers per step, which decides a
+// latency-bound hop), 4 for longer messages (more lines in flight per
+// wait: 9-27 % less time from 64 KiB to 32 MiB per rank at 8 ranks).
+template <int DT, int KIND, bool DBG, int LU>
 struct LL128Step {
     static constexpr uint32_t E = Elem<DT>::E;
     static constexpr bool kRecvRS = KindTraits<KIND>::kRecvRS;
@@ -991,11 +987,10 @@ struct LL128Step {
     // bf16 recvReduceCopySend changes the line format on the way through.
     static constexpr bool kRelayout = DT == AR_BFLOAT16 && KIND == kRecvReduceCopySend;
     // Wave-wide line accesses (8 lines each) per batch.  Two batches are in
-    // flight: the next one's loads go out before this one's stores, so two
-    // units per batch hold as many registers as four without the overlap.
-    static constexpr int U = AR_LL128_U;
+    // flight: the next one's loads go out before this one's stores.
+    static constexpr int U = LU;
     // Batches per drain-and-flag group.
-    static constexpr uint32_t kGroup = AR_LL128_GROUP;
+    static constexpr uint32_t kGroup = 8;
 
     // Elements per line on the wire this step reads / writes.
     static constexpr uint32_t kEplRS = kLL128Data / 4;  // 30 fp32 partials
@@ -1396,7 +1391,7 @@ struct LL128Step {
 
 constexpr uint32_t kLdsWordsPerWave = 240;  // 480 bf16 values
 
-template <int DT, int KIND, bool DBG>
+template <int DT, int KIND, bool DBG, int LU>
 __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, uint32_t len, uint32_t *lds)
 {
     const RingArgs &a = *g.a;
@@ -1416,7 +1411,7 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
     const bool skip = DBG && send && skip_this_post(g);
     // A skipped post: write the data but a flag from the previous message.
     const uint64_t tag_out = skip ? g.m_out : g.m_out + 1;
-    if (!LL128Step<DT, KIND, DBG>::run(a, src, dst, rslot, wslot, len, g.m_in + 1, tag_out, lds, &g.dbg)) return false;
+    if (!LL128Step<DT, KIND, DBG, LU>::run(a, src, dst, rslot, wslot, len, g.m_in + 1, tag_out, lds, &g.dbg)) return false;
     if (send) advance_out(g);
     if (recv) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -1452,7 +1447,7 @@ __device__ __forceinline__ void write_trace(const Ring &g)
     put(7, t.kind);
 }
 
-template <int PROTO, int DT, bool DAG, bool DBG, int KIND>
+template <int PROTO, int DT, bool DAG, bool DBG, int LU, int KIND>
 __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, char *peer_dst, const char *peer_src,
                                         uint32_t len, uint32_t *lds)
 {
@@ -1468,7 +1463,7 @@ __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, cha
     bool ok;
     if (PROTO == AR_PROTO_SIMPLE) ok = simple_step<DT, KIND, DAG, DBG>(g, src, dst, peer_dst, peer_src, len);
     else if (PROTO == AR_PROTO_LL) ok = ll_step<DT, KIND, DBG>(g, src, dst, len);
-    else ok = ll128_step<DT, KIND, DBG>(g, src, dst, len, lds);
+    else ok = ll128_step<DT, KIND, DBG, LU>(g, src, dst, len, lds);
     if constexpr (DBG) {
         if (g.dbg.trace) {
             write_trace(g);
@@ -1479,7 +1474,7 @@ __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, cha
 }
 
 // All steps of one run for one wave; false if the wave had to give up.
-template <int PROTO, int DT, bool DAG, bool DBG>
+template <int PROTO, int DT, bool DAG, bool DBG, int LU>
 __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
 {
     constexpr uint32_t E = Elem<DT>::E;
@@ -1541,29 +1536,29 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
             if constexpr (DAG) {
                 if (peer_start && k == 1) {
                     if (coll == AR_COLL_ALLREDUCE && N == 2)
-                        ok = do_step<PROTO, DT, DAG, DBG, kPeerReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                        ok = do_step<PROTO, DT, DAG, DBG, LU, kPeerReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
                     else if (N == 2)
-                        ok = do_step<PROTO, DT, DAG, DBG, kPeerReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                        ok = do_step<PROTO, DT, DAG, DBG, LU, kPeerReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
                     else
-                        ok = do_step<PROTO, DT, DAG, DBG, kPeerReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                        ok = do_step<PROTO, DT, DAG, DBG, LU, kPeerReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
                     if (!ok) return false;
                     continue;
                 }
             }
             if (coll == AR_COLL_ALLREDUCE) {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k == N - 1) ok = do_step<PROTO, DT, DAG, DBG, kRecvReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, DAG, DBG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, DBG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, LU, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k == N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             } else if (coll == AR_COLL_REDUCESCATTER) {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, DBG, kRecvReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, LU, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             } else {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, kCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, DBG, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, LU, kCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             }
             if (!ok) return false;
         }
@@ -1573,7 +1568,8 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
 
 // DBG: the debug hooks (AR_DEBUG_*) are compiled in; a plan without debug
 // flags runs the kernel without them, whose steps carry no test-only code.
-template <int PROTO, int DT, bool DAG, bool DBG>
+// LU: the LL128 batch width (LL128Step); 2 for the other protocols.
+template <int PROTO, int DT, bool DAG, bool DBG, int LU>
 __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
 {
     __shared__ uint32_t lds_all[(PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? AR_MAX_WAVES * kLdsWordsPerWave : 1];
@@ -1642,7 +1638,7 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
     if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED,
                                                          __HIP_MEMORY_SCOPE_AGENT)) != 0)
         return;
-    ring_steps<PROTO, DT, DAG, DBG>(g, lds);
+    ring_steps<PROTO, DT, DAG, DBG, LU>(g, lds);
     if constexpr (DBG) {
         // One lane adds the wave's line-check counts (nothing follows).
         if (g.dbg.check && lane_id() == 0) {
@@ -1872,18 +1868,28 @@ typedef void (*RingFn)(RingArgs);
 // dag: the Simple ring's direct all-gather (the other protocols always
 // carry the all-gather through their FIFOs).
 template <int DT, bool DBG>
-__host__ RingFn ring_fn_of(int proto, bool dag)
+__host__ RingFn ring_fn_of(int proto, bool dag, bool wide)
 {
-    if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, DT, false, DBG>;
-    if (proto == AR_PROTO_LL128) return ring_kernel<AR_PROTO_LL128, DT, false, DBG>;
-    return dag ? ring_kernel<AR_PROTO_SIMPLE, DT, true, DBG> : ring_kernel<AR_PROTO_SIMPLE, DT, false, DBG>;
+    if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, DT, false, DBG, 2>;
+    if (proto == AR_PROTO_LL128)
+        return wide ? ring_kernel<AR_PROTO_LL128, DT, false, DBG, 4> : ring_kernel<AR_PROTO_LL128, DT, false, DBG, 2>;
+    return dag ? ring_kernel<AR_PROTO_SIMPLE, DT, true, DBG, 2> : ring_kernel<AR_PROTO_SIMPLE, DT, false, DBG, 2>;
 }
 
 // dbg: a plan with debug flags runs the instance with the debug hooks.
-__host__ RingFn ring_fn(int proto, int dtype, bool dag, bool dbg)
+// wide: LL128 with four-access batches.
+__host__ RingFn ring_fn(int proto, int dtype, bool dag, bool dbg, bool wide)
 {
-    if (dtype == AR_FLOAT32) return dbg ? ring_fn_of<AR_FLOAT32, true>(proto, dag) : ring_fn_of<AR_FLOAT32, false>(proto, dag);
-    return dbg ? ring_fn_of<AR_BFLOAT16, true>(proto, dag) : ring_fn_of<AR_BFLOAT16, false>(proto, dag);
+    if (dtype == AR_FLOAT32)
+        return dbg ? ring_fn_of<AR_FLOAT32, true>(proto, dag, wide) : ring_fn_of<AR_FLOAT32, false>(proto, dag, wide);
+    return dbg ? ring_fn_of<AR_BFLOAT16, true>(proto, dag, wide) : ring_fn_of<AR_BFLOAT16, false>(proto, dag, wide);
+}
+
+// LL128 takes four-access batches when one wave's message spans more than
+// one two-access batch (16 lines of 30 fp32 reduce-scatter partials).
+__host__ bool ll128_wide(const ar_plan_info &info)
+{
+    return info.proto == AR_PROTO_LL128 && (info.wave_elems * 4 + 119) / 120 > 16;
 }
 
 // unroll: 16-byte units per thread and iteration.  Two keep more loads in
@@ -1906,7 +1912,7 @@ int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
 {
     dev::RingFn fn = info.algo == AR_ALGO_DIRECT ? dev::direct_fn(info.dtype, info.nranks, info.direct_unroll)
                                                  : dev::ring_fn(info.proto, info.dtype, info.peer_direct != 0,
-                                                                args.debug != 0);
+                                                                args.debug != 0, dev::ll128_wide(info));
     RingArgs a = args;
     void *kargs[] = {&a};
     hipError_t e = hipLaunchKernel((const void *)fn, dim3((unsigned)info.grid), dim3((unsigned)info.block), kargs,
@@ -1918,8 +1924,8 @@ int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
 int ring_occupancy(int proto, int dtype, int block, int *blocks_per_cu)
 {
     int best = 1 << 30;
-    for (int v = 0; v < 4; ++v) {
-        dev::RingFn fn = dev::ring_fn(proto, dtype, (v & 1) != 0, (v & 2) != 0);
+    for (int v = 0; v < 8; ++v) {
+        dev::RingFn fn = dev::ring_fn(proto, dtype, (v & 1) != 0, (v & 2) != 0, (v & 4) != 0);
         int n = 0;
         hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, (const void *)fn, block, 0);
         if (e != hipSuccess) return AR_ERR_HIP;

@@ -11,6 +11,7 @@ on MI355X for the simulated ring.
     python -m paper_2603_11438_amd.sweep stability --coll allgather --out stability.jsonl
     python -m paper_2603_11438_amd.sweep latency --out latency.jsonl
     python -m paper_2603_11438_amd.sweep configs --out configs.jsonl
+    python -m paper_2603_11438_amd.sweep trace --out trace.jsonl
 
 `measure` times each candidate as the device runs it (calls captured in a
 HIP graph and replayed), so small messages are ranked by kernel time rather
@@ -510,6 +511,105 @@ def latency(args):
                 plan.destroy()
 
 
+def _median(v):
+    return float(statistics.median(v)) if len(v) else float("nan")
+
+
+def trace(args):
+    """Where a ring hop's time goes, from AR_DEBUG_TRACE records (channel 0 /
+    wave 0 of every rank; 100 MHz real-time stamps).  For every message a
+    rank r publishes at its step j, paired with rank r+1's step j+1 that
+    takes it:
+
+        recv->issued   rank r took its input message and issued its stores
+                       (LL128 / Simple: includes reading the data)
+        issued->drained  those stores completed (Simple, LL128)
+        drained->posted  the flag or counter store issued
+        posted->taken  until rank r+1 accepted the message (visibility
+                       latency plus polling)
+        hop            rank r's acceptance to rank r+1's acceptance
+
+    Medians over all pairs and runs.  The traced kernels are the builds with
+    the debug hooks, which are somewhat slower than the production ones;
+    `prod_us_per_hop` and `dbg_us_per_hop` give the whole-run time per hop of
+    both for the same plan (graph replay, out of place)."""
+    import numpy as np
+    import torch
+
+    torch.cuda.set_device(0)
+    n = args.nranks
+    sizes = [int(s) for s in args.sizes.split(",")]
+    with open(args.out, "a") as fo:
+        for proto in args.protos.split(","):
+            for size in sizes:
+                count = size // 4
+                g0 = torch.Generator(device="cuda:0").manual_seed(11438 + 300)
+                send = [torch.rand(count, device="cuda:0", generator=g0) * 2 - 1 for _ in range(n)]
+                recv = [torch.empty(count, device="cuda:0") for _ in range(n)]
+                flags = ar.AR_PLAN_FIFO_ONLY if args.fifo_only else 0
+                kw = dict(proto=proto, nchannels=args.channels, nwaves=args.waves, flags=flags)
+                if args.chunk:
+                    kw["chunk_bytes"] = args.chunk
+                per_hop = {}
+                for label, dbg in (("prod", 0), ("dbg", ar.AR_DEBUG_TRACE)):
+                    plan = ar.Plan(n, count, "f32", debug_flags=dbg, **kw)
+                    buf = None
+                    if dbg:
+                        buf = torch.zeros(n * args.records * 8, dtype=torch.int64, device="cuda:0")
+                        plan.set_trace(buf)
+                    side = torch.cuda.Stream()
+                    side.wait_stream(torch.cuda.current_stream())
+                    t = _timer(plan, send, side, graph=True)
+                    info = plan.info
+                    hops = info["nchunks"] * (2 * n - 2)
+                    per_hop[label] = statistics.median(t) / hops * 1e6
+                    if not dbg:
+                        plan.destroy()
+                        continue
+                    samples = {k: [] for k in ("recv_issued", "issued_drained", "drained_posted", "posted_taken",
+                                               "hop")}
+                    stale = []
+                    fn = plan.bind(send, recv, side)
+                    for _ in range(args.runs):
+                        buf.zero_()
+                        with torch.cuda.stream(side):
+                            fn()
+                        torch.cuda.synchronize()
+                        rec = buf.cpu().numpy().view(np.uint64).reshape(n, args.records, 8).astype(np.int64)
+                        nrec = int(np.count_nonzero(rec[0, :, 0]))
+                        for r in range(n):
+                            q = (r + 1) % n
+                            for j in range(nrec - 1):
+                                t_begin, t_recv, polls, t_iss, t_dr, t_post, msg, kind = rec[r, j]
+                                if kind == 4 or t_post == 0:
+                                    continue  # sends nothing
+                                taken = rec[q, j + 1, 1]
+                                if taken == 0:
+                                    continue
+                                samples["posted_taken"].append(taken - t_post)
+                                if t_dr:
+                                    samples["issued_drained"].append(t_dr - t_iss)
+                                    samples["drained_posted"].append(t_post - t_dr)
+                                if t_recv:
+                                    samples["recv_issued"].append(t_iss - t_recv)
+                                    samples["hop"].append(taken - t_recv)
+                                    stale.append(1.0 if polls else 0.0)
+                    if plan.status() != ar.AR_OK:
+                        raise RuntimeError(f"trace {proto} {size}: plan status {plan.status()}")
+                    plan.destroy()
+                    row = {"proto": proto, "size": size, "nranks": n, "nchannels": info["nchannels"],
+                           "nwaves": info["nwaves"], "chunk_bytes": info["chunk_elems"] * 4,
+                           "nchunks": info["nchunks"], "peer_direct": info["peer_direct"],
+                           "pairs": len(samples["hop"])}
+                    for k, v in samples.items():
+                        row[k + "_us"] = round(_median(v) / 100.0, 3)
+                    row["first_look_stale"] = round(_median(stale) if not stale else sum(stale) / len(stale), 3)
+                    row["prod_us_per_hop"] = round(per_hop["prod"], 3)
+                    row["dbg_us_per_hop"] = round(per_hop["dbg"], 3)
+                    fo.write(json.dumps(row) + "\n")
+                    print(json.dumps(row), flush=True)
+
+
 def _to_device(x, dtype):
     """(N, count) numpy array (float32, or uint16 bf16 bits) -> one device tensor per rank."""
     import numpy as np
@@ -636,9 +736,20 @@ def main(argv=None):
     la.add_argument("--sizes", default="")
     la.add_argument("--nranks", type=int, default=8)
     la.add_argument("--graph-runs", type=int, default=100)
+    tr = sub.add_parser("trace")
+    tr.add_argument("--out", required=True)
+    tr.add_argument("--protos", default="simple,ll,ll128")
+    tr.add_argument("--sizes", default="4096,65536,1048576")
+    tr.add_argument("--nranks", type=int, default=8)
+    tr.add_argument("--channels", type=int, default=1)
+    tr.add_argument("--waves", type=int, default=1)
+    tr.add_argument("--chunk", type=int, default=0)
+    tr.add_argument("--records", type=int, default=4096, help="trace records kept per rank")
+    tr.add_argument("--runs", type=int, default=20)
+    tr.add_argument("--fifo-only", action="store_true")
     args = ap.parse_args(argv)
     {"measure": measure, "table": table_cmd, "validate": validate, "stability": stability,
-     "latency": latency, "configs": configs}[args.cmd](args)
+     "latency": latency, "configs": configs, "trace": trace}[args.cmd](args)
 
 
 if __name__ == "__main__":

@@ -66,11 +66,13 @@ def test_ll128_line_tails(ar):
     values): inside lane 6's part, inside lane 7's half-width part (which
     moves on an access that starts inside lane 6's), and at every other
     lane.  One channel and one wave, so a message is a whole segment and
-    the last segment's length walks through every remainder."""
+    the last segment's length walks through every remainder.  Segments of
+    about 240 elements (8 to 17 reduce-scatter lines) run the two-access
+    batches; about 1200 elements (40 lines), the four-access ones."""
     for dtype in ("f32", "bf16"):
-        for n, step, hi in ((2, 1, 124), (3, 3, 190)):
+        for n, step, hi, base in ((2, 1, 124, 240), (3, 3, 190, 240), (2, 1, 124, 1200), (3, 5, 190, 1200)):
             for r in range(0, hi, step):
-                count = n * 240 + r
+                count = n * base + r
                 x = draw(n, count, dtype, "normal", seed=5000 + 7 * n + r)
                 run_case(ar, x, dtype, f"ll128-tail-{dtype}-{n}-{count}", proto="ll128", nchannels=1, nwaves=1)
 
