@@ -10,9 +10,21 @@ direct (two-shot) algorithm on the same input, which produces the same bits
 with only the compulsory bytes (`--algo direct` makes it the step).
 
 Prints one JSON line.  `value` is the bus bandwidth (S / t * 2(N-1)/N, in
-GB/s = 1e9 B/s, S = bytes per rank); `roofline` prices the ring kernel's
-algorithmic bytes against MI355X's 8 TB/s HBM peak; `cpu_baseline` times
-the plain-C CPU oracle on the host on the same workload.
+GB/s = 1e9 B/s, S = bytes per rank); `cpu_baseline` times the plain-C CPU
+oracle on the host on the same workload.  `roofline` prices the kernel
+against MI355X's 8 TB/s HBM peak on two bases:
+  * achieved / frac: the ring's algorithmic bytes, every rank-buffer, peer
+    and FIFO access the ring formulation issues (34 S for the peer-direct
+    Simple ring at 8 ranks fp32).  Its FIFO and forwarding traffic is partly
+    served by the 256 MB last-level cache, so this is memory-side traffic,
+    not HBM traffic alone (it exceeds what a pure HBM stream reaches here);
+  * achieved_compulsory / frac_compulsory: 2 N S, each input read once and
+    each output written once, the HBM lower bound of any AllReduce of N
+    buffers in one memory: the HBM figure.
+Both are also given as fractions of copy_reference, the rate of the
+library's own streaming copy on the same box.  `traffic` is measured from
+rocprofv3 TCC counters, i.e. bytes crossing the L2's memory-side interface
+(last-level-cache hits included: gfx950 exposes no DRAM-side counter).
 
 Timing: W untimed warm-up steps, then K steps between HIP events recorded
 on the stream the kernel is launched on, with a device synchronisation on
@@ -56,7 +68,7 @@ def geometry_key(info: dict) -> str:
 
 
 def read_traffic(workload: str, kernel: str, geometry: str) -> dict | None:
-    """HBM-side bytes per launch from a committed rocprofv3 counter summary,
+    """Memory-side (L2 egress) bytes per launch from a committed rocprofv3 counter summary,
     or None when there is none, it was taken with another launch geometry,
     or the kernel source has changed since."""
     path = os.path.join(PROFILES, f"{kernel}_{workload}_pmc.txt")
@@ -219,25 +231,42 @@ def main(argv=None) -> int:
             raise RuntimeError("timed runs timed out")
         return e0.elapsed_time(e1) / args.steps, t_wall * 1e3
 
-    def roofline_of(info, ms):
+    def roofline_of(info, ms, copy_gbs=None):
         t = ms / 1e3
         algo = info["algo_name"]
         kernel = f"ring_{info['proto_name']}" if algo == "ring" else "direct"
+        if algo == "ring" and not info["peer_direct"] and info["proto_name"] == "simple":
+            kernel = "ring_simple_fifo"
         b_comp = ar.compulsory_bytes(s_bytes, n)
         b_alg = (ar.ring_bytes(s_bytes, n, dtype, info["proto_name"], peer_direct=bool(info["peer_direct"]))
                  if algo == "ring" else b_comp)
         achieved = b_alg / t / 1e9
+        comp = b_comp / t / 1e9
         traffic = read_traffic(wl.name, kernel, geometry_key(info))
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": round(traffic["bytes"]) if traffic else None,
                 "kernel": (f"ring_kernel<{info['proto_name']}, {dtype}>" if algo == "ring"
                            else f"direct_kernel<{dtype}>"),
-                "algorithmic_bytes_per_launch": b_alg, "geometry": geometry_key(info),
-                "achieved_compulsory": round(b_comp / t / 1e9, 1),
-                "frac_compulsory": round(b_comp / t / 1e9 / HBM_PEAK_GBS, 4)}
+                "algorithmic_bytes_per_launch": b_alg,
+                "basis": (f"{b_alg / s_bytes:.2f} S algorithmic bytes of the "
+                          + ("ring: rank buffers, peer reads and FIFOs; memory-side traffic, partly served by "
+                             "the last-level cache, not HBM alone" if algo == "ring" else
+                             "direct algorithm: each input read once, each output written once")),
+                "geometry": geometry_key(info),
+                "achieved_compulsory": round(comp, 1),
+                "frac_compulsory": round(comp / HBM_PEAK_GBS, 4),
+                "compulsory_basis": f"{b_comp / s_bytes:.0f} S = 2 N S, the HBM lower bound of any AllReduce "
+                                    "of N buffers in one memory (the HBM figure)",
+                "traffic_counter": "rocprofv3 TCC FETCH_SIZE and WRITE_SIZE, scaled on a copy of known size: "
+                                   "bytes crossing the L2's memory-side interface, last-level-cache hits "
+                                   "included (gfx950 exposes no DRAM-side counter)"}
+        if copy_gbs:
+            roof["frac_of_copy_ceiling"] = round(achieved / copy_gbs, 4)
+            roof["frac_compulsory_of_copy_ceiling"] = round(comp / copy_gbs, 4)
         if traffic:
             roof["traffic_source"] = traffic["file"]
+            roof["traffic_over_algorithmic"] = round(traffic["bytes"] / b_alg, 4)
         return roof
 
     plan = ar.Plan(n, count, dtype, proto=args.proto, nchannels=args.nchannels, chunk_bytes=args.chunk_bytes,
@@ -257,16 +286,12 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         cp.destroy()
 
-    other = None
+    direct = None
     if args.algo == "ring" and args.compare_direct:
         dplan = ar.Plan(n, count, dtype, algo="direct")
         dms, _ = measure(dplan)
-        dinfo = dplan.info
+        direct = (dplan.info, dms)
         dplan.destroy()
-        other = {"algo": "direct", "value": round(ar.bus_bandwidth(s_bytes, dms / 1e3, n), 2), "unit": "GB/s",
-                 "ms_per_step": round(dms, 4), "parts": dinfo["nchannels"], "nwaves": dinfo["nwaves"],
-                 "roofline": roofline_of(dinfo, dms),
-                 "note": "two-shot direct algorithm on the same input: same result bits, compulsory bytes only"}
 
     copy_ref = None
     if args.copy_reference:
@@ -297,9 +322,17 @@ def main(argv=None) -> int:
     t = ms / 1e3
     busbw = ar.bus_bandwidth(s_bytes, t, n)
     algbw = ar.alg_bandwidth(s_bytes, t)
-    roofline = roofline_of(info, ms)
+    copy_gbs = copy_ref["gbs"] if copy_ref else None
+    roofline = roofline_of(info, ms, copy_gbs)
     if copy_ref:
         roofline["copy_reference"] = copy_ref
+    other = None
+    if direct:
+        dinfo, dms = direct
+        other = {"algo": "direct", "value": round(ar.bus_bandwidth(s_bytes, dms / 1e3, n), 2), "unit": "GB/s",
+                 "ms_per_step": round(dms, 4), "parts": dinfo["nchannels"], "nwaves": dinfo["nwaves"],
+                 "roofline": roofline_of(dinfo, dms, copy_gbs),
+                 "note": "two-shot direct algorithm on the same input: same result bits, compulsory bytes only"}
 
     cpu = None
     if args.cpu_seconds > 0:

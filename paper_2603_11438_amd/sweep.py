@@ -227,9 +227,18 @@ def default_row(size, rs, nranks=8, coll="allreduce", dtype="f32"):
     return None
 
 
-def select(rows, tie=0.02, coll="allreduce", dtype="f32"):
-    """Per size: {"ring": ring choice, "direct": direct choice or None, "algo": "ring" | "direct"}."""
+def select(rows, tie=0.02, coll="allreduce", dtype="f32", validated=None):
+    """Per size: {"ring": ring choice, "direct": direct choice or None, "algo": "ring" | "direct"}.
+
+    validated: {size: ring/default bus-bandwidth ratio measured by `validate`
+    on fresh repeats}.  A ring choice whose validated ratio is below 1 + tie
+    defers to the fixed default after all: the selection is made on one set
+    of repeats and must hold on another."""
     ring = select_ring([r for r in rows if r.get("algo", "ring") == "ring"], tie, coll, dtype)
+    for size, rr in ring.items():
+        ratio = (validated or {}).get(size)
+        if ratio is not None and rr["proto"] != "default" and ratio < 1 + tie:
+            ring[size] = dict(rr, proto="default", validated_ratio=ratio)
     out = {}
     for size, rr in ring.items():
         ds = [r for r in rows if r["size"] == size and r.get("algo") == "direct"]
@@ -307,7 +316,8 @@ def emit_one(table, key, measured_as=None):
         "// on MI355X by paper_2603_11438_amd/sweep.py (highest median bus bandwidth,",
         "// ties within 2% broken by fewer channels, fewer wire bytes, smaller chunk).",
         "// AR_PROTO_AUTO ring columns defer to the fixed default (Simple, 16 channels):",
-        "// there the default measured within 2% of the best ring choice.  The",
+        "// there the default measured within 2% of the best ring choice (on the",
+        "// sweep, or when validated on fresh repeats).  The",
         "// algorithm column picks the faster of the best ring and the best direct",
         "// choice (direct on a tie, as it moves fewer bytes).",
         "//",
@@ -325,7 +335,8 @@ def emit_one(table, key, measured_as=None):
         algo = "AR_ALGO_DIRECT" if row["algo"] == "direct" else "AR_ALGO_RING"
         dcols = f"{d['nchannels']}, {d['nwaves']}, {d.get('direct_unroll', 0)}" if d else "0, 0, 0"
         dbw = f"{d['busbw']:.1f}" if d else "-"
-        lines.append(f"    {{{lg}, {ring_cols}, {algo}, {dcols}}},  // {r['busbw']:.1f} / {dbw}")
+        note = " (ring validated within 2 % of the default: defers)" if "validated_ratio" in r else ""
+        lines.append(f"    {{{lg}, {ring_cols}, {algo}, {dcols}}},  // {r['busbw']:.1f} / {dbw}{note}")
     lines.append("};")
     return "\n".join(lines) + "\n"
 
@@ -334,11 +345,17 @@ def table_cmd(args):
     rows = []
     for f in args.jsonl:
         rows += [json.loads(l) for l in open(f) if l.strip()]
+    val = {}
+    for f in getattr(args, "validated", None) or []:
+        for l in open(f):
+            if l.strip():
+                v = json.loads(l)
+                val.setdefault((v.get("coll", "allreduce"), v.get("dtype", "f32")), {})[v["size"]] = v["ratio_ring"]
     tables = {}
     for coll, dtype in TABLE_NAMES:
         rs = [r for r in rows if r.get("coll", "allreduce") == coll and r.get("dtype", "f32") == dtype]
         if rs:
-            tables[(coll, dtype)] = select(rs, coll=coll, dtype=dtype)
+            tables[(coll, dtype)] = select(rs, coll=coll, dtype=dtype, validated=val.get((coll, dtype)))
     for (coll, dtype), table in tables.items():
         print(f"== {coll} {dtype}")
         print_table(table)
@@ -715,6 +732,8 @@ def main(argv=None):
     t = sub.add_parser("table")
     t.add_argument("jsonl", nargs="+")
     t.add_argument("--emit", default="")
+    t.add_argument("--validated", nargs="*", default=[],
+                   help="`validate` outputs: ring rows within 2 %% of the default there defer to it")
     v = sub.add_parser("validate")
     v.add_argument("--out", required=True)
     v.add_argument("--nranks", type=int, default=8)

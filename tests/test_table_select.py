@@ -107,3 +107,21 @@ def test_bf16_table_falls_back_to_the_fp32_rows(tmp_path):
     f32 = text.split("kTableAllReduce[]")[1].split("};")[0]
     bf16 = text.split("kTableAllReduceBf16[]")[1].split("};")[0]
     assert f32.strip() and f32 == bf16
+
+
+def test_validated_ratio_within_tie_defers_to_default():
+    """A ring choice made on the sweep's repeats that validates within 2 % of
+    the fixed default on fresh repeats defers to the default; one that
+    validates clearly faster keeps its row."""
+    rows = [ring("ll", 16, 4096, 4, 300.0), ring("simple", 32, 65536, 4, 250.0)]
+    keep = sweep.select(rows, validated={SIZE: 1.25})[SIZE]["ring"]
+    assert keep["proto"] == "ll"
+    dropped = sweep.select(rows, validated={SIZE: 0.99})[SIZE]["ring"]
+    assert dropped["proto"] == "default" and dropped["validated_ratio"] == 0.99
+    edge = sweep.select(rows, validated={SIZE: 1.019})[SIZE]["ring"]
+    assert edge["proto"] == "default"
+    # sizes without a validation keep the sweep's choice
+    assert sweep.select(rows, validated={SIZE * 2: 0.5})[SIZE]["ring"]["proto"] == "ll"
+    # the emitted row leaves the ring columns to the default
+    text = sweep.emit_one({SIZE: sweep.select(rows, validated={SIZE: 0.99})[SIZE]}, ("allreduce", "f32"))
+    assert "{24, AR_PROTO_AUTO, 0, 0, 0," in text
