@@ -124,7 +124,13 @@ struct HipGateApi {
         *yes = st != hipStreamCaptureStatusNone;
         return 0;
     }
-    static int create(Event *e) { return hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess ? 0 : AR_ERR_HIP; }
+    static int sync_device() { return hipDeviceSynchronize() == hipSuccess ? 0 : AR_ERR_HIP; }
+    // Ordering kernels of one device needs no system-scope release.
+    static int create(Event *e)
+    {
+        return hipEventCreateWithFlags(e, hipEventDisableTiming | hipEventDisableSystemFence) == hipSuccess
+                   ? 0 : AR_ERR_HIP;
+    }
     static int wait(Stream s, Event e) { return hipStreamWaitEvent(s, e, 0) == hipSuccess ? 0 : AR_ERR_HIP; }
     static int record(Event e, Stream s) { return hipEventRecord(e, s) == hipSuccess ? 0 : AR_ERR_HIP; }
 };

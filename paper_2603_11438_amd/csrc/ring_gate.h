@@ -7,17 +7,23 @@
 // then holds part of the device with spinning waves while the rest of its
 // grid waits for room the other one occupies, and both end in the watchdog.
 // The gate rules that out by never letting two ring grids overlap on one
-// device: before a ring launch on stream S, S waits for an event recorded
-// after the device's previous ring launch if that launch went to another
-// stream; after the launch the event is recorded again on S.  Launches on
-// one stream are ordered by the stream itself.  Launches being captured into
-// a graph are not gated (the graph's own edges order them; a graph replayed
+// device.  Launches on one stream are ordered by the stream itself, and an
+// event recorded between two kernels costs device time (a marker packet
+// the command processor handles between them: about 2-3 us per launch on
+// MI355X), so a device pays nothing while all its ring launches use one
+// stream.  The first ring launch on a second stream waits, once, for the
+// whole device (the earlier launches carry no event), and switches the
+// device to ordered mode: from then on every ring launch records an event
+// after itself, and a launch on another stream than the last one first
+// makes its stream wait for that event.  Launches being captured into a
+// graph are not gated (the graph's own edges order them; a graph replayed
 // beside ring launches on other streams must be ordered by its caller).
 //
 // The policy is written against a small API so that it can be exercised on
 // the host alone with a fake one; the library instantiates it with HIP.
 //   Api::Stream, Api::Event                       handle types
 //   int Api::capturing(Stream, bool *yes)         0 on success
+//   int Api::sync_device()                        wait for all work of the device
 //   int Api::create(Event *)                      0 on success
 //   int Api::wait(Stream, Event)                  stream waits for the event
 //   int Api::record(Event, Stream)                0 on success
@@ -68,16 +74,20 @@ public:
         if (rc != 0) return rc;
         t.gated_ = !cap;
         if (!t.gated_) return 0;
-        if (!st.have_event) {
-            rc = Api::create(&st.event);
+        if (!st.have_last || st.last == stream) return 0;
+        if (!st.ordered) {
+            // A second stream: the launches so far carry no event.
+            if (!st.have_event) {
+                rc = Api::create(&st.event);
+                if (rc != 0) return rc;
+                st.have_event = true;
+            }
+            rc = Api::sync_device();
             if (rc != 0) return rc;
-            st.have_event = true;
+            st.ordered = true;
+            return 0;
         }
-        if (st.have_last && !(st.last == stream)) {
-            rc = Api::wait(stream, st.event);
-            if (rc != 0) return rc;
-        }
-        return 0;
+        return Api::wait(stream, st.event);
     }
 
     // After the launch was enqueued on the ticket's stream.
@@ -86,7 +96,7 @@ public:
         int rc = 0;
         if (t.gated_) {
             State &st = state_[t.dev_];
-            rc = Api::record(st.event, t.stream_);
+            if (st.ordered) rc = Api::record(st.event, t.stream_);
             if (rc == 0) {
                 st.last = t.stream_;
                 st.have_last = true;
@@ -96,6 +106,14 @@ public:
         }
         t.release();
         return rc;
+    }
+
+    // Whether the device has switched to ordered mode (tests).
+    bool ordered(int dev)
+    {
+        if (dev < 0 || dev >= kMaxDevices) return false;
+        std::lock_guard<std::mutex> g(state_[dev].mu);
+        return state_[dev].ordered;
     }
 
     // The stream of the device's last gated ring launch (tests).
@@ -113,6 +131,7 @@ private:
         std::mutex mu;
         Event event{};
         bool have_event = false;
+        bool ordered = false;    // a second stream has been seen: record after every launch
         Stream last{};
         bool have_last = false;
     };

@@ -1,13 +1,16 @@
 // Host-only test of the ring launch gate (ring_gate.h) with a fake stream
-// API that keeps a log of waits and records.  Checks:
-//   * launches on one stream never wait; the event is recorded after each;
-//   * a launch on another stream waits for the event of the last launch;
+// API that keeps a log of device waits, event waits and records.  Checks:
+//   * while a device has seen one stream, launches cost nothing (no event);
+//   * the first launch on a second stream waits for the whole device once
+//     and switches the device to ordered mode;
+//   * in ordered mode the event is recorded after every launch, and a launch
+//     on another stream than the last waits for the event of that launch;
 //   * launches being captured are neither ordered nor recorded;
 //   * devices keep separate state; out-of-range devices are refused;
 //   * an API error stops the launch sequence and is returned;
-//   * under concurrent launchers (run with ThreadSanitizer) every launch on a
-//     stream other than the previous launch's waits for exactly that
-//     previous launch: the log, replayed, shows no two launches overlapping.
+//   * under concurrent launchers (run with ThreadSanitizer) no two launches
+//     on different streams overlap: replayed, the log shows every stream
+//     switch behind a device wait or a wait for the previous launch.
 #include <stdio.h>
 #include <stdlib.h>
 
@@ -22,7 +25,7 @@
 namespace {
 
 struct Op {
-    char kind;    // 'w' wait, 'r' record, 'c' create, 'L' launch
+    char kind;    // 'w' wait, 'r' record, 'c' create, 'S' device wait, 'L' launch
     int stream;
     int event;    // event id; for 'r' the generation recorded, for 'w' the generation awaited
     int dev;
@@ -46,6 +49,11 @@ struct FakeApi {
     static int capturing(Stream s, bool *yes)
     {
         *yes = s == g_capturing_stream.load();
+        return 0;
+    }
+    static int sync_device()
+    {
+        log_op({'S', -1, -1, -1});
         return 0;
     }
     static int create(Event *e)
@@ -115,23 +123,26 @@ std::string kinds(const std::vector<Op> &v)
 void test_sequences()
 {
     Gate g;
-    // first launch: create the event, no wait, record after
+    // one stream: nothing but the launches
     CHECK(launch(g, 0, 1) == 0);
-    CHECK(kinds(take_log()) == "cLr");
-    // same stream again: no wait
+    CHECK(kinds(take_log()) == "L");
     CHECK(launch(g, 0, 1) == 0);
-    CHECK(kinds(take_log()) == "Lr");
-    // another stream: wait for the event of the last launch (generation 2)
+    CHECK(kinds(take_log()) == "L");
+    CHECK(!g.ordered(0));
+    // a second stream: one device wait, then ordered mode (record after)
     CHECK(launch(g, 0, 2) == 0);
-    auto v = take_log();
-    CHECK(kinds(v) == "wLr");
-    CHECK(v[0].stream == 2 && v[0].event == 2);
+    CHECK(kinds(take_log()) == "cSLr");
+    CHECK(g.ordered(0));
     int last = -1;
     CHECK(g.last_stream(0, &last) && last == 2);
-    // back to stream 1: waits for stream 2's launch (generation 3)
+    // same stream in ordered mode: no wait, record after
+    CHECK(launch(g, 0, 2) == 0);
+    CHECK(kinds(take_log()) == "Lr");
+    // back to stream 1: wait for stream 2's last launch (generation 2)
     CHECK(launch(g, 0, 1) == 0);
-    v = take_log();
-    CHECK(kinds(v) == "wLr" && v[0].event == 3);
+    auto v = take_log();
+    CHECK(kinds(v) == "wLr");
+    CHECK(v[0].stream == 1 && v[0].event == 2);
 
     // a capturing stream is neither ordered nor recorded, and does not
     // change which launch the next one waits for
@@ -143,11 +154,12 @@ void test_sequences()
     CHECK(launch(g, 0, 1) == 0);
     CHECK(kinds(take_log()) == "Lr");
 
-    // device 1 has its own event and history
+    // device 1 has its own state: one stream costs nothing there
     CHECK(launch(g, 1, 2) == 0);
-    CHECK(kinds(take_log()) == "cLr");
+    CHECK(kinds(take_log()) == "L");
     CHECK(launch(g, 1, 2) == 0);
-    CHECK(kinds(take_log()) == "Lr");
+    CHECK(kinds(take_log()) == "L");
+    CHECK(!g.ordered(1));
 
     // out-of-range devices are refused before anything happens
     Gate::Ticket t;
@@ -166,9 +178,10 @@ void test_sequences()
 }
 
 // Concurrent launchers on several streams of one device.  Replaying the log
-// in order: each launch on a stream other than the previous launch's must be
-// preceded (after that previous launch's record) by a wait on that stream for
-// the generation the previous launch recorded.
+// in order: before the device wait every launch is on one stream; after it,
+// each launch on a stream other than the previous launch's is preceded
+// (after that previous launch's record) by a wait on its stream for the
+// generation the previous launch recorded.
 void test_concurrent()
 {
     Gate g;
@@ -184,16 +197,24 @@ void test_concurrent()
         });
     for (auto &t : th) t.join();
     auto v = take_log();
+    bool ordered = false;
+    int syncs = 0, first_stream = -1;
     int prev_stream = -1, prev_gen = 0, pending_wait_gen = -1, pending_wait_stream = -1;
     int launches = 0, waits = 0;
     for (size_t i = 0; i < v.size(); ++i) {
         const Op &o = v[i];
-        if (o.kind == 'w') {
+        if (o.kind == 'S') {
+            ++syncs;
+            ordered = true;
+        } else if (o.kind == 'w') {
             pending_wait_gen = o.event;
             pending_wait_stream = o.stream;
             ++waits;
         } else if (o.kind == 'L') {
-            if (prev_stream >= 0 && o.stream != prev_stream) {
+            if (!ordered) {
+                if (first_stream < 0) first_stream = o.stream;
+                CHECK(o.stream == first_stream);
+            } else if (prev_stream >= 0 && o.stream != prev_stream) {
                 CHECK(pending_wait_stream == o.stream && pending_wait_gen == prev_gen);
             } else {
                 CHECK(pending_wait_gen == -1);
@@ -207,9 +228,10 @@ void test_concurrent()
             prev_gen = o.event;
         }
     }
+    CHECK(syncs == 1);
     CHECK(launches == kThreads * kLaunches);
     CHECK(waits > 0);
-    printf("concurrent: %d launches, %d waits\n", launches, waits);
+    printf("concurrent: %d launches, %d waits, %d device wait\n", launches, waits, syncs);
 }
 
 }  // namespace
