@@ -36,15 +36,18 @@
  * Ring launches on one device are ordered across streams.  A ring kernel's
  * workgroups wait on each other, so its grid needs the whole grid resident;
  * two ring grids dispatched side by side could each hold part of the device
- * while waiting for room the other occupies.  So before a ring launch on a
- * stream, the library makes that stream wait for the device's previous ring
- * launch if it went to another stream (an event recorded after every ring
- * launch; one event per device, created on the first ring launch).  Ring
- * collectives of different plans therefore never overlap in time, whatever
- * streams they run on; the direct algorithm's kernels are not ordered (they
- * never wait).  Launches captured into a HIP graph are not ordered this way:
- * a graph whose replays may overlap ring launches on other streams must be
- * ordered by its caller (replay it on the stream that runs the others).
+ * while waiting for room the other occupies.  While all ring launches of a
+ * device go to one stream, that stream orders them and the library adds
+ * nothing.  The first ring launch on a second stream waits (on the host)
+ * for all work of the device once, and from then on the library records an
+ * event after every ring launch of that device (one event per device) and
+ * makes a ring launch on another stream than the previous one wait for it.
+ * Ring collectives of different plans therefore never overlap in time,
+ * whatever streams they run on; the direct algorithm's kernels are not
+ * ordered (they never wait).  Launches captured into a HIP graph are not
+ * ordered this way: a graph whose replays may overlap ring launches on
+ * other streams must be ordered by its caller (replay it on the stream that
+ * runs the others).
  */
 #ifndef AR_H
 #define AR_H
