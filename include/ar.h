@@ -208,8 +208,15 @@ typedef struct ar_plan_desc {
  *                    forwarded from there (nothing moves on the last hop).
  *                    The result bits are the same either way.  The other
  *                    protocols always use their FIFOs, and the direct
- *                    algorithm has none, so they ignore the flag. */
-enum { AR_PLAN_PROFILE = 1u, AR_PLAN_FIFO_ONLY = 2u };
+ *                    algorithm has none, so they ignore the flag.
+ *   AR_PLAN_LL128_ORDERED  LL128 only: a reader uses a batch of lines only
+ *                    from loads issued after it has seen every flag of the
+ *                    batch current (it polls the 8-byte flags, then reads
+ *                    the lines), never from a load that brought data and
+ *                    flag together.  This takes no assumption about how a
+ *                    128-byte load is served, at the cost of one more round
+ *                    trip per batch.  Other protocols ignore the flag. */
+enum { AR_PLAN_PROFILE = 1u, AR_PLAN_FIFO_ONLY = 2u, AR_PLAN_LL128_ORDERED = 4u };
 
 /* Resolved plan geometry (after the tuner and defaults). */
 typedef struct ar_plan_info {

@@ -29,7 +29,7 @@ AR_PLACE_RANK_SPREAD, AR_PLACE_CHANNEL_LOCAL = 0, 1
 AR_NOALLOC_SCRATCH_BYTES = 16 << 20
 AR_DEBUG_SKIP_POST, AR_DEBUG_JITTER, AR_DEBUG_CHECK_LINES, AR_DEBUG_TRACE = 1, 2, 4, 8
 TRACE_FIELDS = ("t_begin", "t_recv", "polls", "t_issued", "t_drained", "t_posted", "msg", "kind")
-AR_PLAN_PROFILE, AR_PLAN_FIFO_ONLY = 1, 2
+AR_PLAN_PROFILE, AR_PLAN_FIFO_ONLY, AR_PLAN_LL128_ORDERED = 1, 2, 4
 AR_ALGO_AUTO, AR_ALGO_RING, AR_ALGO_DIRECT = 0, 1, 2
 ALGOS = {"auto": AR_ALGO_AUTO, "ring": AR_ALGO_RING, "direct": AR_ALGO_DIRECT}
 ALGO_NAMES = {v: k for k, v in ALGOS.items()}

@@ -51,6 +51,7 @@ struct RingArgs {
     uint64_t slot_bytes;             // bytes of one FIFO slot
     uint64_t timeout_ticks;          // watchdog, in 100 MHz real-time ticks
     uint32_t nranks, nchannels, nwaves, depth, nchunks, placement, debug;
+    uint32_t ll128_ordered;          // AR_PLAN_LL128_ORDERED: lines only from loads after their flags
     uint32_t coll;                   // AR_COLL_*: which steps of the ring run
     uint32_t full_segs;              // segments 0 .. full_segs-1 hold seg elements; segment
                                      // full_segs holds part, any later one none
@@ -85,7 +86,7 @@ int check_buffers(const ar_plan_info &g, const void *const *send, void *const *r
 // Workgroups of a ring launch that fit on the current device, per rank.
 int device_channel_capacity(int proto, int dtype, int nranks, int nwaves, int *cap);
 // Kernel arguments of one run.
-void fill_args(const ar_plan_info &g, uint32_t debug_flags, uint64_t timeout_ticks, const void *const *send,
+void fill_args(const ar_plan_info &g, const ar_plan_desc &d, uint64_t timeout_ticks, const void *const *send,
                void *const *recv, char *fifo, uint64_t *flags, uint32_t *ctl, RingArgs *out);
 // The tuner's and defaults' geometry for a description on the current device.
 int resolve_for_device(const ar_plan_desc *desc, ar_plan_desc *d_out, ar_plan_info *info_out, int *dev_out);

@@ -955,7 +955,8 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
 // that the data half of such a load is no older than its flag half is an
 // assumption (CDNA does not promise 128-byte single-copy atomicity), not a
 // guarantee.  A batch found stale is read again only after its flags alone
-// have been seen current, which orders that read after them.
+// have been seen current, which orders that read after them; plans with
+// AR_PLAN_LL128_ORDERED treat every batch that way.
 //
 // Lane 7's part is half as wide as the others.  Rather than a second, narrow
 // access for it (a whole extra instruction for one lane in eight), lane 7
@@ -973,7 +974,7 @@ constexpr uint32_t kLL128Data = 120;
 // lines: fewer instructions and registers per step, which decides a
 // latency-bound hop), 4 for longer messages (more lines in flight per
 // wait: 9-27 % less time from 64 KiB to 32 MiB per rank at 8 ranks).
-template <int DT, int KIND, bool DBG, int LU>
+template <int DT, int KIND, bool DBG, int LU, bool ORD>
 struct LL128Step {
     static constexpr uint32_t E = Elem<DT>::E;
     static constexpr bool kRecvRS = KindTraits<KIND>::kRecvRS;
@@ -1166,7 +1167,8 @@ struct LL128Step {
                                        const bool *act, uint64_t tag, uint32_t first, uint32_t nlines,
                                        bool &was_stale)
     {
-        was_stale = stale_lines<NB>(lines, act, step_lane() & 7u, tag);
+        // Ordered plans take no line from a load that also brought its flag.
+        was_stale = ORD || stale_lines<NB>(lines, act, step_lane() & 7u, tag);
         if (was_stale) {
             if (!poll_flags<NB>(a, wi, first, nlines, tag)) return false;
 #pragma unroll
@@ -1391,7 +1393,7 @@ struct LL128Step {
 
 constexpr uint32_t kLdsWordsPerWave = 240;  // 480 bf16 values
 
-template <int DT, int KIND, bool DBG, int LU>
+template <int DT, int KIND, bool DBG, int LU, bool ORD>
 __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, uint32_t len, uint32_t *lds)
 {
     const RingArgs &a = *g.a;
@@ -1411,7 +1413,8 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
     const bool skip = DBG && send && skip_this_post(g);
     // A skipped post: write the data but a flag from the previous message.
     const uint64_t tag_out = skip ? g.m_out : g.m_out + 1;
-    if (!LL128Step<DT, KIND, DBG, LU>::run(a, src, dst, rslot, wslot, len, g.m_in + 1, tag_out, lds, &g.dbg)) return false;
+    if (!LL128Step<DT, KIND, DBG, LU, ORD>::run(a, src, dst, rslot, wslot, len, g.m_in + 1, tag_out, lds, &g.dbg))
+        return false;
     if (send) advance_out(g);
     if (recv) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -1447,7 +1450,7 @@ __device__ __forceinline__ void write_trace(const Ring &g)
     put(7, t.kind);
 }
 
-template <int PROTO, int DT, bool DAG, bool DBG, int LU, int KIND>
+template <int PROTO, int DT, bool DAG, bool DBG, int LU, bool ORD, int KIND>
 __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, char *peer_dst, const char *peer_src,
                                         uint32_t len, uint32_t *lds)
 {
@@ -1463,7 +1466,7 @@ __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, cha
     bool ok;
     if (PROTO == AR_PROTO_SIMPLE) ok = simple_step<DT, KIND, DAG, DBG>(g, src, dst, peer_dst, peer_src, len);
     else if (PROTO == AR_PROTO_LL) ok = ll_step<DT, KIND, DBG>(g, src, dst, len);
-    else ok = ll128_step<DT, KIND, DBG, LU>(g, src, dst, len, lds);
+    else ok = ll128_step<DT, KIND, DBG, LU, ORD>(g, src, dst, len, lds);
     if constexpr (DBG) {
         if (g.dbg.trace) {
             write_trace(g);
@@ -1474,7 +1477,7 @@ __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, cha
 }
 
 // All steps of one run for one wave; false if the wave had to give up.
-template <int PROTO, int DT, bool DAG, bool DBG, int LU>
+template <int PROTO, int DT, bool DAG, bool DBG, int LU, bool ORD>
 __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
 {
     constexpr uint32_t E = Elem<DT>::E;
@@ -1536,29 +1539,29 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
             if constexpr (DAG) {
                 if (peer_start && k == 1) {
                     if (coll == AR_COLL_ALLREDUCE && N == 2)
-                        ok = do_step<PROTO, DT, DAG, DBG, LU, kPeerReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                        ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kPeerReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
                     else if (N == 2)
-                        ok = do_step<PROTO, DT, DAG, DBG, LU, kPeerReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                        ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kPeerReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
                     else
-                        ok = do_step<PROTO, DT, DAG, DBG, LU, kPeerReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                        ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kPeerReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
                     if (!ok) return false;
                     continue;
                 }
             }
             if (coll == AR_COLL_ALLREDUCE) {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, LU, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k == N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k == N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kRecvReduceCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < 2 * N - 2) ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             } else if (coll == AR_COLL_REDUCESCATTER) {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, LU, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kRecvReduceSend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kRecvReduceCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             } else {
-                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, LU, kCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
-                else ok = do_step<PROTO, DT, DAG, DBG, LU, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                if (k == 0) ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else if (k < N - 1) ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kRecvCopySend>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
+                else ok = do_step<PROTO, DT, DAG, DBG, LU, ORD, kRecvCopy>(g, s_ptr, d_ptr, p_ptr, q_ptr, len, lds);
             }
             if (!ok) return false;
         }
@@ -1569,7 +1572,10 @@ __device__ __forceinline__ bool ring_steps(Ring &g, uint32_t *lds)
 // DBG: the debug hooks (AR_DEBUG_*) are compiled in; a plan without debug
 // flags runs the kernel without them, whose steps carry no test-only code.
 // LU: the LL128 batch width (LL128Step); 2 for the other protocols.
-template <int PROTO, int DT, bool DAG, bool DBG, int LU>
+// ORD: LL128 reads a batch only after its flags (AR_PLAN_LL128_ORDERED); a
+// build of its own, since even an untaken test of a run-time flag costs the
+// two-access step 0.26 us per hop.
+template <int PROTO, int DT, bool DAG, bool DBG, int LU, bool ORD>
 __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
 {
     __shared__ uint32_t lds_all[(PROTO == AR_PROTO_LL128 && DT == AR_BFLOAT16) ? AR_MAX_WAVES * kLdsWordsPerWave : 1];
@@ -1638,7 +1644,7 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
     if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED,
                                                          __HIP_MEMORY_SCOPE_AGENT)) != 0)
         return;
-    ring_steps<PROTO, DT, DAG, DBG, LU>(g, lds);
+    ring_steps<PROTO, DT, DAG, DBG, LU, ORD>(g, lds);
     if constexpr (DBG) {
         // One lane adds the wave's line-check counts (nothing follows).
         if (g.dbg.check && lane_id() == 0) {
@@ -1867,22 +1873,29 @@ typedef void (*RingFn)(RingArgs);
 
 // dag: the Simple ring's direct all-gather (the other protocols always
 // carry the all-gather through their FIFOs).
-template <int DT, bool DBG>
-__host__ RingFn ring_fn_of(int proto, bool dag, bool wide)
+template <int DT, bool DBG, bool ORD>
+__host__ RingFn ll128_fn(bool wide)
 {
-    if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, DT, false, DBG, 2>;
-    if (proto == AR_PROTO_LL128)
-        return wide ? ring_kernel<AR_PROTO_LL128, DT, false, DBG, 4> : ring_kernel<AR_PROTO_LL128, DT, false, DBG, 2>;
-    return dag ? ring_kernel<AR_PROTO_SIMPLE, DT, true, DBG, 2> : ring_kernel<AR_PROTO_SIMPLE, DT, false, DBG, 2>;
+    return wide ? ring_kernel<AR_PROTO_LL128, DT, false, DBG, 4, ORD> : ring_kernel<AR_PROTO_LL128, DT, false, DBG, 2, ORD>;
+}
+
+template <int DT, bool DBG>
+__host__ RingFn ring_fn_of(int proto, bool dag, bool wide, bool ordered)
+{
+    if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, DT, false, DBG, 2, false>;
+    if (proto == AR_PROTO_LL128) return ordered ? ll128_fn<DT, DBG, true>(wide) : ll128_fn<DT, DBG, false>(wide);
+    return dag ? ring_kernel<AR_PROTO_SIMPLE, DT, true, DBG, 2, false> : ring_kernel<AR_PROTO_SIMPLE, DT, false, DBG, 2, false>;
 }
 
 // dbg: a plan with debug flags runs the instance with the debug hooks.
-// wide: LL128 with four-access batches.
-__host__ RingFn ring_fn(int proto, int dtype, bool dag, bool dbg, bool wide)
+// wide: LL128 with four-access batches; ordered: AR_PLAN_LL128_ORDERED.
+__host__ RingFn ring_fn(int proto, int dtype, bool dag, bool dbg, bool wide, bool ordered)
 {
     if (dtype == AR_FLOAT32)
-        return dbg ? ring_fn_of<AR_FLOAT32, true>(proto, dag, wide) : ring_fn_of<AR_FLOAT32, false>(proto, dag, wide);
-    return dbg ? ring_fn_of<AR_BFLOAT16, true>(proto, dag, wide) : ring_fn_of<AR_BFLOAT16, false>(proto, dag, wide);
+        return dbg ? ring_fn_of<AR_FLOAT32, true>(proto, dag, wide, ordered)
+                   : ring_fn_of<AR_FLOAT32, false>(proto, dag, wide, ordered);
+    return dbg ? ring_fn_of<AR_BFLOAT16, true>(proto, dag, wide, ordered)
+               : ring_fn_of<AR_BFLOAT16, false>(proto, dag, wide, ordered);
 }
 
 // LL128 takes four-access batches when one wave's message spans more than
@@ -1912,7 +1925,8 @@ int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
 {
     dev::RingFn fn = info.algo == AR_ALGO_DIRECT ? dev::direct_fn(info.dtype, info.nranks, info.direct_unroll)
                                                  : dev::ring_fn(info.proto, info.dtype, info.peer_direct != 0,
-                                                                args.debug != 0, dev::ll128_wide(info));
+                                                                args.debug != 0, dev::ll128_wide(info),
+                                                                args.ll128_ordered != 0);
     RingArgs a = args;
     void *kargs[] = {&a};
     hipError_t e = hipLaunchKernel((const void *)fn, dim3((unsigned)info.grid), dim3((unsigned)info.block), kargs,
@@ -1924,8 +1938,8 @@ int launch_ring(const ar_plan_info &info, const RingArgs &args, void *stream)
 int ring_occupancy(int proto, int dtype, int block, int *blocks_per_cu)
 {
     int best = 1 << 30;
-    for (int v = 0; v < 8; ++v) {
-        dev::RingFn fn = dev::ring_fn(proto, dtype, (v & 1) != 0, (v & 2) != 0, (v & 4) != 0);
+    for (int v = 0; v < 16; ++v) {
+        dev::RingFn fn = dev::ring_fn(proto, dtype, (v & 1) != 0, (v & 2) != 0, (v & 4) != 0, (v & 8) != 0);
         int n = 0;
         hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, (const void *)fn, block, 0);
         if (e != hipSuccess) return AR_ERR_HIP;

@@ -71,7 +71,7 @@ extern "C" int ar_run_noalloc(const ar_plan_desc *desc, const void *const *send,
     RingArgs a;
     if (g.algo != AR_ALGO_RING) {
         // The direct algorithm uses no memory besides the rank buffers.
-        fill_args(g, d.debug_flags, (uint64_t)tus * kTicksPerUs, send, recv, nullptr, nullptr, nullptr, &a);
+        fill_args(g, d, (uint64_t)tus * kTicksPerUs, send, recv, nullptr, nullptr, nullptr, &a);
         return ret(launch_ring(g, a, stream));
     }
     size_t flags_off = 0, fifo_off = 0;
@@ -88,7 +88,7 @@ extern "C" int ar_run_noalloc(const ar_plan_desc *desc, const void *const *send,
     // as a kernel node.
     rc = launch_fill_u32((uint32_t *)ws, need / 4, 0u, stream);
     if (rc != AR_OK) return ret(rc);
-    fill_args(g, d.debug_flags, (uint64_t)tus * kTicksPerUs, send, recv, ws + fifo_off,
+    fill_args(g, d, (uint64_t)tus * kTicksPerUs, send, recv, ws + fifo_off,
               (uint64_t *)(ws + flags_off), (uint32_t *)ws, &a);
     return ret(launch_ring(g, a, stream));
 }

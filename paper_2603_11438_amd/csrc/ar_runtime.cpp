@@ -142,7 +142,7 @@ RingGate<HipGateApi> g_ring_gate;
 namespace ar {
 
 // Everything a launch needs besides the plan's memory.
-void fill_args(const ar_plan_info &g, uint32_t debug_flags, uint64_t timeout_ticks, const void *const *send,
+void fill_args(const ar_plan_info &g, const ar_plan_desc &d, uint64_t timeout_ticks, const void *const *send,
                void *const *recv, char *fifo, uint64_t *flags, uint32_t *ctl, RingArgs *out)
 {
     RingArgs a;
@@ -174,7 +174,8 @@ void fill_args(const ar_plan_info &g, uint32_t debug_flags, uint64_t timeout_tic
     a.depth = (uint32_t)g.fifo_depth;
     a.nchunks = (uint32_t)g.nchunks;
     a.placement = (uint32_t)g.placement;
-    a.debug = debug_flags;
+    a.debug = d.debug_flags;
+    a.ll128_ordered = (d.flags & AR_PLAN_LL128_ORDERED) ? 1u : 0u;
     *out = a;
 }
 
@@ -301,7 +302,7 @@ int run_impl(ar_plan_t *p, const void *const *send, void *const *recv, void *str
         return ret(rc);
     }
     RingArgs a;
-    fill_args(g, p->desc.debug_flags, p->timeout_ticks, send, recv, p->fifo, p->flags, p->ctl, &a);
+    fill_args(g, p->desc, p->timeout_ticks, send, recv, p->fifo, p->flags, p->ctl, &a);
     a.trace = p->trace;
     a.trace_per_rank = p->trace ? p->trace_per_rank : 0;
     bool timed = false;

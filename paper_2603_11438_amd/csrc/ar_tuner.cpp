@@ -257,7 +257,7 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     if (d->direct_unroll < 0 || d->direct_unroll > 2) return AR_ERR_ARG;
     if (d->placement != AR_PLACE_RANK_SPREAD && d->placement != AR_PLACE_CHANNEL_LOCAL) return AR_ERR_ARG;
     if (d->chunk_bytes > kMaxChunkBytes) return AR_ERR_ARG;
-    if (d->flags & ~(uint32_t)(AR_PLAN_PROFILE | AR_PLAN_FIFO_ONLY)) return AR_ERR_ARG;
+    if (d->flags & ~(uint32_t)(AR_PLAN_PROFILE | AR_PLAN_FIFO_ONLY | AR_PLAN_LL128_ORDERED)) return AR_ERR_ARG;
     if (!valid_algo(d->algo)) return AR_ERR_ARG;
     if (d->coll != AR_COLL_ALLREDUCE && d->coll != AR_COLL_REDUCESCATTER && d->coll != AR_COLL_ALLGATHER)
         return AR_ERR_ARG;

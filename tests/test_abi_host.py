@@ -334,6 +334,8 @@ def test_direct_allgather_mode_in_geometry():
     assert geom("simple")["wire_bytes_per_run"] == geom("simple", flags=ar.AR_PLAN_FIFO_ONLY)["wire_bytes_per_run"]
     d = ar.make_desc(8, 1 << 16, "f32", "simple", 4, flags=8)
     assert ar.lib().ar_plan_geometry(ctypes.byref(d), ctypes.byref(ar.ar_plan_info())) == ar.AR_ERR_ARG
+    # the ordered-read flag of LL128 changes no geometry
+    assert geom("ll128", flags=ar.AR_PLAN_LL128_ORDERED) == geom("ll128")
 
 
 def test_default_fifo_depth_deepens_small_runs():

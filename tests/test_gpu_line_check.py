@@ -107,6 +107,19 @@ def test_line_check_stress(ar, proto, dtype):
     assert first > 0 and first < total
 
 
+@pytest.mark.parametrize("dtype", ("f32", "bf16"))
+def test_line_check_ll128_ordered(ar, dtype):
+    """With AR_PLAN_LL128_ORDERED no line is taken from a load that also
+    brought its flag: the checker counts no first-load acceptances, and no
+    bad line."""
+    e = 4 if dtype == "f32" else 2
+    dbg = ar.AR_DEBUG_CHECK_LINES
+    for count, ch, w, runs in (((4 << 20) // e, 32, 4, 10), (5000, 1, 1, 20), ((1 << 20) // e, 4, 1, 20)):
+        st = _run_checked(ar, 8, count, dtype, "allreduce", runs, dbg, proto="ll128", nchannels=ch, nwaves=w,
+                          flags=ar.AR_PLAN_LL128_ORDERED)
+        assert st["lines_first_read"] == 0, st
+
+
 def test_trace_records(ar):
     """AR_DEBUG_TRACE: one record per ring step of channel 0 / wave 0 of
     every rank.  Stamps inside a step are ordered; message indices advance

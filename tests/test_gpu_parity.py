@@ -77,6 +77,20 @@ def test_ll128_line_tails(ar):
                 run_case(ar, x, dtype, f"ll128-tail-{dtype}-{n}-{count}", proto="ll128", nchannels=1, nwaves=1)
 
 
+def test_ll128_ordered_reads(ar):
+    """AR_PLAN_LL128_ORDERED: every batch is read after its flags were seen
+    current.  Same bits as the oracle for both dtypes, several rank counts,
+    ragged counts, one and three channels, and both batch widths (one wave
+    per rank, so segments of 60+ elements run four-access batches)."""
+    for dtype in ("f32", "bf16"):
+        for n in (2, 3, 8):
+            for count in (1, 257, 4099, 65537):
+                x = draw(n, count, dtype, "normal", seed=3100 + 7 * n + count)
+                for nch, nw in ((1, 1), (3, 4)):
+                    run_case(ar, x, dtype, f"ll128-ordered-{dtype}-{n}-{count}-{nch}-{nw}", proto="ll128",
+                             nchannels=nch, nwaves=nw, flags=ar.AR_PLAN_LL128_ORDERED)
+
+
 def test_bound_calls(ar):
     """Plan.bind checks the buffers once and returns a single-C-call
     launcher: repeated calls out of place and a call in place give the

@@ -34,7 +34,9 @@ def _case(rng):
         cfg["chunk_bytes"] = int(rng.choice([16, 256, 1024, 4096, 65536]))
         cfg["fifo_depth"] = int(rng.choice([2, 3, 4, 8]))
         cfg["placement"] = int(rng.integers(0, 2))
-        cfg["flags"] = int(rng.choice([0, 2]))  # 2: all-gather through the FIFOs
+        # 2: Simple all-gather through the FIFOs; 4: LL128 reads lines only
+        # after their flags
+        cfg["flags"] = int(rng.choice([0, 2, 4]))
     else:
         cfg["nchannels"] = int(rng.choice([0, 1, 3, 16]))
         cfg["nwaves"] = int(rng.choice([0, 1, 4, 16]))
