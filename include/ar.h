@@ -78,8 +78,9 @@ enum { AR_FLOAT32 = 0, AR_BFLOAT16 = 1 };
  *          assumption CDNA does not document: that one 128-byte line load
  *          never returns its data half older than its flag half.  A stale
  *          first look is re-read only after the flags alone were seen
- *          current, which is ordered.  The built-in tuner table never picks
- *          LL128 on MI355X; a caller who selects it takes the assumption.
+ *          current, which is ordered; AR_PLAN_LL128_ORDERED makes every
+ *          batch take that path and removes the assumption.  The built-in
+ *          tuner table never picks LL128 on MI355X.
  *   Simple bulk chunks behind separate ready (tail) / free (head) counters. */
 enum { AR_PROTO_AUTO = -1, AR_PROTO_LL = 0, AR_PROTO_LL128 = 1, AR_PROTO_SIMPLE = 2 };
 
