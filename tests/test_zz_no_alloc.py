@@ -135,3 +135,51 @@ def test_noalloc_rejects_what_it_cannot_hold(ar):
     g = ar.ar_plan_geometry(desc)
     assert g["fifo_bytes"] > ar.AR_NOALLOC_SCRATCH_BYTES
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("cfg", [dict(proto="ll", nchannels=2), dict(proto="simple", nchannels=3),
+                                 dict(proto="ll128", nchannels=2)], ids=lambda c: c["proto"])
+def test_noalloc_graph_replay(ar, cfg):
+    """Calls captured into a HIP graph: each replay clears the scratch with
+    the captured fill kernel and runs the ring from message 0 again, so
+    every replay, on fresh input values, gives the oracle's bits; eager
+    calls with other values run between the replays."""
+    import torch
+
+    n, count = 8, 4099
+    x0 = draw(n, count, "f32", "normal", seed=810)
+    send = to_device(x0, "f32")
+    recv = [torch.full((count,), float("nan"), device="cuda:0") for _ in range(n)]
+    ar.run_noalloc(send, recv, **cfg)  # eager first (the device's scratch address is looked up here)
+    torch.cuda.synchronize()
+    assert np.array_equal(_bits(recv, "f32"), _oracle(x0, "f32", "allreduce").view(np.uint32))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        ar.run_noalloc(send, recv, stream=side, **cfg)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        for _ in range(2):
+            ar.run_noalloc(send, recv, stream=side, **cfg)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        say(f"noalloc graph {cfg} replay {rep}")
+        x = draw(n, count, "f32", "normal", seed=820 + rep)
+        host = to_device(x, "f32")
+        for r in range(n):
+            send[r].copy_(host[r])
+            recv[r].fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(_bits(recv, "f32"), _oracle(x, "f32", "allreduce").view(np.uint32)), rep
+        x2 = draw(n, count, "f32", "normal", seed=830 + rep)
+        host = to_device(x2, "f32")
+        for r in range(n):
+            send[r].copy_(host[r])
+        ar.run_noalloc(send, recv, **cfg)
+        torch.cuda.synchronize()
+        assert np.array_equal(_bits(recv, "f32"), _oracle(x2, "f32", "allreduce").view(np.uint32)), rep
+    del g
