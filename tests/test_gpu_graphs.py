@@ -179,3 +179,48 @@ def test_ring_plans_on_several_streams(ar):
             assert_ranks_equal(rounds[i], oracle_bits(xs[i], "f32"), "f32", f"stream {i} round {rep}")
     for p in plans:
         p.destroy()
+
+
+def test_ring_plans_from_two_host_threads(ar):
+    """Two host threads, each with its own ring plan and stream, launch 40
+    runs each at the same time (the C calls run concurrently: ctypes
+    releases the interpreter lock).  The launch gate's per-device lock and
+    event keep the sequence consistent; every run's result is checked."""
+    import threading
+
+    import torch
+
+    n = 8
+    specs = [(30011, dict(proto="ll", nchannels=2)), (20000, dict(proto="simple", nchannels=3))]
+    results, errors = {}, []
+
+    def worker(i, count, cfg):
+        try:
+            torch.cuda.set_device(0)
+            x = draw(n, count, "f32", "uniform", seed=90 + i)
+            send = to_device(x, "f32")
+            plan = ar.Plan(n, count, "f32", **cfg)
+            stream = torch.cuda.Stream()
+            fn_recv = [[torch.empty_like(t) for t in send] for _ in range(40)]
+            with torch.cuda.stream(stream):
+                for k in range(40):
+                    plan.run_oop(send, fn_recv[k], stream=stream)
+            stream.synchronize()
+            results[i] = (plan.status(), x, fn_recv)
+            plan.destroy()
+        except Exception as e:  # reported below
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=worker, args=(i, c, cfg)) for i, (c, cfg) in enumerate(specs)]
+    say("two host threads, two streams")
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for i, (st, x, recvs) in results.items():
+        assert st == ar.AR_OK
+        want = oracle_bits(x, "f32")
+        for k, recv in enumerate(recvs):
+            assert_ranks_equal(recv, want, "f32", f"thread {i} run {k}")
