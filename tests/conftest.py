@@ -10,14 +10,4 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
-    config.addinivalue_line("markers", "slow: long CPU test")
 
-
-def pytest_collection_modifyitems(config, items):
-    """Tests marked ``slow`` run only when AR_RUN_SLOW=1 (they take minutes)."""
-    if os.environ.get("AR_RUN_SLOW") == "1":
-        return
-    skip = pytest.mark.skip(reason="slow test; set AR_RUN_SLOW=1 to run")
-    for item in items:
-        if "slow" in item.keywords:
-            item.add_marker(skip)
