@@ -68,7 +68,7 @@ constexpr int kFifoLd = kPolSc1;  // device-coherent FIFO reads
 constexpr int kFifoSt = kPolSc1;  // device-coherent FIFO writes
 constexpr int kInPol = kPolNt;    // rank inputs: read once, streamed
 constexpr int kOutPol = kPolNt;   // rank outputs: written once, streamed
-static_assert((kFifoLd & kPolSc1) && (kFifoSt & kPolSc1), "FIFO accesses must be device-coherent");
+static_assert((kFifoLd & kPolSc1) != 0 && (kFifoSt & kPolSc1) != 0, "FIFO accesses must be device-coherent");
 
 enum Kind : int {
     kSend = 0,            // own input -> wire (reduce-scatter start)
@@ -578,7 +578,7 @@ struct SimpleStep {
     __device__ static void run(const RingArgs &a, const char *src, char *dst, const char *rslot,
                                char *wslot, uint32_t len)
     {
-        if (DAG && KIND == kRecvCopy) return;  // the data is already in place
+        if (DAG && KIND == kRecvCopy) return;  // the data is already in place (simple_step skips it)
         const uint32_t lane = step_lane();
         const uint32_t nfull = len / A, rem = len % A;
         const uint32_t nunits = nfull + (rem ? 1u : 0u);
@@ -626,6 +626,17 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
                                             const char *peer_src, uint32_t len)
 {
     const RingArgs &a = *g.a;
+    if constexpr (DAG && KIND == kRecvCopy) {
+        // The last hop of a peer-direct all-gather: the predecessor writes
+        // the values straight into this rank's output, and nothing else in
+        // this run reads or writes them, so there is nothing to wait for;
+        // they are in place when the kernel ends.  The message is
+        // acknowledged at once: it occupies no FIFO slot, and every earlier
+        // message of the link has been consumed, in order.
+        flag_store(g.head_in, g.m_in + 1);
+        advance_in(g);
+        return true;
+    }
     // A peer read needs no message: the chain start's input is in place
     // before the kernel starts and stays there until the chain is done.
     constexpr bool recv = KindTraits<KIND>::kRecvRS || KindTraits<KIND>::kRecvAG;
@@ -1618,8 +1629,14 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
     // in its timeout state, which only ar_plan_reset clears, zeroing every
     // epoch.)
     uint64_t *epoch_p = g.tail_out + kEpochU64;
-    const uint64_t epoch = uniform64(flag_load(epoch_p));
-    g.head_seen = uniform64(flag_load(g.head_out));
+    // The abort word goes out with them: a wave that tested it only after
+    // the first two had arrived would start every run one round trip later.
+    const uint64_t epoch_word = flag_load(epoch_p);
+    const uint64_t head_word = flag_load(g.head_out);
+    const uint32_t abort_word = __hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t epoch = uniform64(epoch_word);
+    g.head_seen = uniform64(head_word);
+    const bool aborted = __builtin_amdgcn_readfirstlane(abort_word) != 0;
     after_observe();
     {
         // messages per chunk: 2N-2 (AllReduce) or N-1, one fewer when a
@@ -1641,9 +1658,7 @@ __global__ __launch_bounds__(1024) void ring_kernel(RingArgs a)
     }
 
     // A previous run that timed out leaves the abort word raised: do nothing.
-    if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(a.ctl + kCtlAbort, __ATOMIC_RELAXED,
-                                                         __HIP_MEMORY_SCOPE_AGENT)) != 0)
-        return;
+    if (aborted) return;
     ring_steps<PROTO, DT, DAG, DBG, LU, ORD>(g, lds);
     if constexpr (DBG) {
         // One lane adds the wave's line-check counts (nothing follows).
