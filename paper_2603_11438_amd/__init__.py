@@ -574,7 +574,11 @@ def ring_bytes(msg_bytes: int, nranks: int, dtype="f32", proto="simple", peer_di
     and its input and writes its own and the next rank's output (4 + 3e);
     each of the N-2 forwarding ranks reads its output and writes the next
     rank's (2e); the last rank moves nothing.  With two ranks the owner is
-    the second rank: it reads both inputs and writes both outputs (4e)."""
+    the second rank: it reads both inputs and writes both outputs (4e).
+
+    The peer-direct LL ring only starts its chains with the peer read: the
+    first hop's partial line is neither written nor read, 2 * 4 * 2 bytes
+    fewer per element than through the FIFOs.  LL128 always uses its FIFOs."""
     e = 4 if dtype == "f32" else 2
     count = msg_bytes // e
     if peer_direct and proto == "simple" and nranks >= 2:
@@ -584,7 +588,10 @@ def ring_bytes(msg_bytes: int, nranks: int, dtype="f32", proto="simple", peer_di
         return float(count * per_elem)
     wf = {"simple": 1.0, "ll": 2.0, "ll128": 128.0 / 120.0}[proto]
     wire = count * (nranks - 1) * (4 + e) * wf
-    return 2.0 * nranks * msg_bytes + 2.0 * wire
+    total = 2.0 * nranks * msg_bytes + 2.0 * wire
+    if peer_direct and proto == "ll" and nranks >= 2:
+        total -= count * 2 * 4 * wf
+    return total
 
 
 def compulsory_bytes(msg_bytes: int, nranks: int) -> float:

@@ -22,9 +22,9 @@
 //   N-1 < k < 2N-2  recv y; write y, send y     (recvCopySend)
 //   k = 2N-2      recv y; write y               (recvCopy)
 // so segment s is summed x_s + x_{s+1} + ... + x_{s+N-1} in that order.  In
-// the Simple ring's peer-direct mode step 0 becomes a read of the chain
-// start's input by the second rank, and all-gather chunks are written into
-// the next rank's output instead of a FIFO slot.
+// the peer-direct mode (Simple and LL rings) step 0 becomes a read of the
+// chain start's input by the second rank, and the Simple ring writes
+// all-gather chunks into the next rank's output instead of a FIFO slot.
 //
 // Memory model.  A FIFO slot written by one wave is read by a wave that can
 // sit on another XCD, i.e. behind another L2.  Every FIFO access therefore
@@ -690,7 +690,10 @@ __device__ __forceinline__ bool simple_step(Ring &g, const char *src, char *dst,
 // lines.  Reduce-scatter lines carry one fp32 partial each; all-gather lines
 // carry one fp32 or two bf16 values.  Lanes take "groups" of 8 data bytes (2
 // fp32 or 4 bf16): input/output 8 bytes, RS wire G lines (placed by
-// wide_off), AG wire 2 lines (16 bytes).
+// wide_off), AG wire 2 lines (16 bytes).  In the peer-direct mode a
+// reduction chain starts as in the Simple ring: its second rank reads the
+// chain start's input (8 bytes per group, no flags) from that rank's buffer;
+// the all-gather keeps its lines, whose flags cannot live in a user buffer.
 
 template <int DT, int KIND, bool DBG>
 struct LLStep {
@@ -705,6 +708,7 @@ struct LLStep {
     static constexpr bool kWriteOut = KindTraits<KIND>::kWriteOut;
     static constexpr bool kReduceToY = KindTraits<KIND>::kReduceToY;
     static constexpr bool kCopyInToY = KindTraits<KIND>::kCopyInToY;
+    static constexpr bool kRecvPeer = KindTraits<KIND>::kRecvPeer;
     static constexpr int U = 4;
 
     // A partial group (valid < G elements) moves element by element; ok =
@@ -732,7 +736,7 @@ struct LLStep {
     // of range (a lane past the end of the message).  chk (debug builds
     // only): the wire carries check words instead of data.
     __device__ static void group(Rsrc rout, Rsrc wo, uint32_t q, bool ok, uint32_t valid, uint32_t ng,
-                                 u32x2 in, const u32x4 *rs, const u32x4 &ag, uint32_t tag_out, bool chk)
+                                 u32x2 in, const u32x4 *rs, const u32x4 &ag, u32x2 pe, uint32_t tag_out, bool chk)
     {
         float acc[G];
         if (kSendRS || kReduceToY) {
@@ -749,6 +753,17 @@ struct LLStep {
                 for (uint32_t v = 0; v < RSV; ++v) {
                     acc[2 * v] = as_f32(rs[v][0]) + acc[2 * v];
                     acc[2 * v + 1] = as_f32(rs[v][2]) + acc[2 * v + 1];
+                }
+            }
+            if (kRecvPeer) {  // the chain start's elements, in the data type
+                if (E == 4) {
+                    acc[0] = as_f32(pe[0]) + acc[0];
+                    acc[1] = as_f32(pe[1]) + acc[1];
+                } else {
+                    acc[0] = bf16_lo(pe[0]) + acc[0];
+                    acc[1] = bf16_hi(pe[0]) + acc[1];
+                    acc[2] = bf16_lo(pe[1]) + acc[2];
+                    acc[3] = bf16_hi(pe[1]) + acc[3];
                 }
             }
         }
@@ -806,16 +821,19 @@ struct LLStep {
         const uint32_t ng = nfg + (rem ? 1u : 0u);
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
-        const Rsrc wi = make_rsrc(rslot, a.slot_bytes);
+        // rslot: the incoming FIFO slot, or for a peer read the chain
+        // start's input at this message's elements
+        const Rsrc wi = make_rsrc(rslot, kRecvPeer ? (uint64_t)len * E : a.slot_bytes);
         const Rsrc wo = make_rsrc(wslot, a.slot_bytes);
         for (uint32_t base = 0; base < nfg; base += 64 * U) {
-            u32x2 in[U];
+            u32x2 in[U], pe[U];
             u32x4 rs[U][RSV], ag[U];
 #pragma unroll
             for (int t = 0; t < U; ++t) {
                 const uint32_t q = base + 64 * t + lane;
                 const bool ok = q < nfg;
                 if (kLoadIn) in[t] = ld64<kInPol>(rin, in_range(ok, q * 8));
+                if (kRecvPeer) pe[t] = ld64<kInPol>(wi, in_range(ok, q * 8));
                 if (kRecvRS)
                     for (uint32_t v = 0; v < RSV; ++v)
                         rs[t][v] = ld128<kFifoLd>(wi, in_range(ok, wide_off(q, v, RSV, ng)));
@@ -871,7 +889,8 @@ struct LLStep {
 #pragma unroll
             for (int t = 0; t < U; ++t) {
                 const uint32_t q = base + 64 * t + lane;
-                group(rout, wo, q, q < nfg, G, ng, in[t], rs[t], ag[t], tag_out, chk);
+                group(rout, wo, q, q < nfg, G, ng, in[t], rs[t], ag[t], kRecvPeer ? pe[t] : u32x2{0, 0}, tag_out,
+                      chk);
             }
         }
         if (rem) {
@@ -879,9 +898,10 @@ struct LLStep {
             // of the partial group has its accesses in range.
             const uint32_t q = nfg;
             const bool me = lane == (nfg & 63u);
-            u32x2 in = {0, 0};
+            u32x2 in = {0, 0}, pe = {0, 0};
             u32x4 rs[RSV], ag = {0, 0, 0, 0};
             if (kLoadIn) in = load_part(rin, q, rem, me);
+            if (kRecvPeer) pe = load_part(wi, q, rem, me);
             if (kRecvRS || kRecvAG) {
                 Watchdog wd;
                 uint32_t reloads = 0;
@@ -914,14 +934,15 @@ struct LLStep {
                     }
                 }
             }
-            group(rout, wo, q, me, rem, ng, in, rs, ag, tag_out, chk);
+            group(rout, wo, q, me, rem, ng, in, rs, ag, pe, tag_out, chk);
         }
         return true;
     }
 };
 
+// peer_src: the chain start's input at this step's elements (peer reads).
 template <int DT, int KIND, bool DBG>
-__device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uint32_t len)
+__device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, const char *peer_src, uint32_t len)
 {
     const RingArgs &a = *g.a;
     constexpr bool recv = KindTraits<KIND>::kRecvRS || KindTraits<KIND>::kRecvAG;
@@ -929,6 +950,7 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, uin
     const char *rslot = nullptr;
     char *wslot = nullptr;
     if (recv) rslot = slot_ptr(const_cast<char *>(g.fifo_in), g.slot_in, a);
+    if (KindTraits<KIND>::kRecvPeer) rslot = peer_src;
     if (send) {
         if (!acquire_send_slot(g)) return false;
         wslot = slot_ptr(g.fifo_out, g.slot_out, a);
@@ -1476,7 +1498,7 @@ __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, cha
     }
     bool ok;
     if (PROTO == AR_PROTO_SIMPLE) ok = simple_step<DT, KIND, DAG, DBG>(g, src, dst, peer_dst, peer_src, len);
-    else if (PROTO == AR_PROTO_LL) ok = ll_step<DT, KIND, DBG>(g, src, dst, len);
+    else if (PROTO == AR_PROTO_LL) ok = ll_step<DT, KIND, DBG>(g, src, dst, peer_src, len);
     else ok = ll128_step<DT, KIND, DBG, LU, ORD>(g, src, dst, len, lds);
     if constexpr (DBG) {
         if (g.dbg.trace) {
@@ -1897,7 +1919,8 @@ __host__ RingFn ll128_fn(bool wide)
 template <int DT, bool DBG>
 __host__ RingFn ring_fn_of(int proto, bool dag, bool wide, bool ordered)
 {
-    if (proto == AR_PROTO_LL) return ring_kernel<AR_PROTO_LL, DT, false, DBG, 2, false>;
+    if (proto == AR_PROTO_LL)
+        return dag ? ring_kernel<AR_PROTO_LL, DT, true, DBG, 2, false> : ring_kernel<AR_PROTO_LL, DT, false, DBG, 2, false>;
     if (proto == AR_PROTO_LL128) return ordered ? ll128_fn<DT, DBG, true>(wide) : ll128_fn<DT, DBG, false>(wide);
     return dag ? ring_kernel<AR_PROTO_SIMPLE, DT, true, DBG, 2, false> : ring_kernel<AR_PROTO_SIMPLE, DT, false, DBG, 2, false>;
 }

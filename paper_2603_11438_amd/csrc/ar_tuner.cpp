@@ -320,7 +320,10 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     g.placement = d->placement;
     g.count = d->count;
     g.block = 64 * nw;
-    g.peer_direct = proto == AR_PROTO_SIMPLE && !(d->flags & AR_PLAN_FIFO_ONLY);
+    // Peer-direct mode: Simple and LL chains start with a peer read (and
+    // the Simple all-gather writes into the next rank's output); LL128 and
+    // AR_PLAN_FIFO_ONLY plans keep every hop in the FIFOs.
+    g.peer_direct = (proto == AR_PROTO_SIMPLE || proto == AR_PROTO_LL) && !(d->flags & AR_PLAN_FIFO_ONLY);
 
     const uint64_t N = (uint64_t)d->nranks;
     g.seg_elems = d->coll == AR_COLL_ALLREDUCE ? round_up(ceil_div(d->count, N), A) : d->count;
@@ -349,8 +352,8 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     }
     g.slot_bytes = round_up(slot, 256);
     const uint64_t conns = (uint64_t)nch * N * (uint64_t)nw;
-    // Messages per connection: 2N-2 per chunk (AllReduce) or N-1; with the
-    // peer-direct Simple ring a reduction chain starts with a peer read, one
+    // Messages per connection: 2N-2 per chunk (AllReduce) or N-1; in the
+    // peer-direct mode a reduction chain starts with a peer read, one
     // message fewer.
     g.msgs_per_run = g.nchunks * ((d->coll == AR_COLL_ALLREDUCE ? 2 * N - 2 : N - 1) -
                                   (g.peer_direct && d->coll != AR_COLL_ALLGATHER ? 1 : 0));
@@ -375,20 +378,24 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     // ReduceScatter: each of N blocks crosses N-1 links as fp32 partials;
     // AllGather: each of N blocks crosses N-1 links as data.
     const double ag_e = (double)e;
-    double rs_bytes = 0, ag_bytes = 0;
-    // With the peer-direct Simple ring the first link of a chain carries the
-    // chain start's input in the data type (a peer read), not a partial.
-    const double rs_link = g.peer_direct ? 4.0 * (double)(N - 2) + (double)e : 4.0 * (double)(N - 1);
+    double rs_bytes = 0, ag_bytes = 0, peer_bytes = 0;
+    // In the peer-direct mode the first link of a chain carries the chain
+    // start's input in the data type (a peer read, without line flags), not
+    // a partial.
+    const double rs_link = g.peer_direct ? 4.0 * (double)(N - 2) : 4.0 * (double)(N - 1);
+    const double rs_peer = g.peer_direct ? (double)e : 0.0;
     if (d->coll == AR_COLL_ALLREDUCE) {
         rs_bytes = (double)d->count * rs_link;
+        peer_bytes = (double)d->count * rs_peer;
         ag_bytes = (double)d->count * ag_e * (double)(N - 1);
     } else if (d->coll == AR_COLL_REDUCESCATTER) {
         rs_bytes = (double)d->count * (double)N * rs_link;
+        peer_bytes = (double)d->count * (double)N * rs_peer;
     } else {
         ag_bytes = (double)d->count * (double)N * ag_e * (double)(N - 1);
     }
     double w = proto == AR_PROTO_LL ? 2.0 : (proto == AR_PROTO_LL128 ? 128.0 / 120.0 : 1.0);
-    g.wire_bytes_per_run = (uint64_t)((rs_bytes + ag_bytes) * w);
+    g.wire_bytes_per_run = (uint64_t)((rs_bytes + ag_bytes) * w + peer_bytes);
 
     // Sanity limits: 32-bit byte offsets inside a slot, bounded FIFO memory.
     if (g.slot_bytes > (1ull << 31)) return AR_ERR_ARG;

@@ -578,7 +578,7 @@ def trace(args):
                     side.wait_stream(torch.cuda.current_stream())
                     t = _timer(plan, send, side, graph=True)
                     info = plan.info
-                    hops = info["nchunks"] * (2 * n - 2)
+                    hops = info["msgs_per_run"]  # messages of one link per run
                     per_hop[label] = statistics.median(t) / hops * 1e6
                     if not dbg:
                         plan.destroy()

@@ -283,7 +283,10 @@ def test_ring_byte_counts():
     assert ar.ring_bytes(S, 2, "f32", "simple", peer_direct=True) == 4 * S
     # 3 ranks fp32: second rank 12 B, owner 16 B, forwarder 8 B per element
     assert ar.ring_bytes(S, 3, "f32", "simple", peer_direct=True) == 9 * S
-    assert ar.ring_bytes(S, 8, "f32", "ll", peer_direct=True) == 72 * S  # LL has no direct mode
+    # The peer-direct LL ring only starts its chains with a peer read: the
+    # first hop's fp32 partial line (8 B) is neither written nor read.
+    assert ar.ring_bytes(S, 8, "f32", "ll", peer_direct=True) == 68 * S
+    assert ar.ring_bytes(S, 8, "bf16", "ll", peer_direct=True) == ar.ring_bytes(S, 8, "bf16", "ll") - 8 * S
 
 
 def test_direct_unroll_resolution():
@@ -324,14 +327,24 @@ def test_direct_allgather_mode_in_geometry():
     assert geom("simple", "allgather")["peer_direct"] == 1
     assert geom("simple", "reducescatter")["peer_direct"] == 1
     assert geom("simple", flags=ar.AR_PLAN_FIFO_ONLY)["peer_direct"] == 0
-    assert geom("ll")["peer_direct"] == 0 and geom("ll128")["peer_direct"] == 0
+    assert geom("ll")["peer_direct"] == 1 and geom("ll", flags=ar.AR_PLAN_FIFO_ONLY)["peer_direct"] == 0
+    assert geom("ll", "allgather")["peer_direct"] == 1
+    assert geom("ll128")["peer_direct"] == 0
     # one message fewer per chunk when a chain starts with a peer read
-    for coll, per_chunk in (("allreduce", 2 * 8 - 2), ("reducescatter", 8 - 1), ("allgather", 8 - 1)):
-        d, f = geom("simple", coll), geom("simple", coll, flags=ar.AR_PLAN_FIFO_ONLY)
-        assert f["msgs_per_run"] == f["nchunks"] * per_chunk
-        assert d["msgs_per_run"] == d["nchunks"] * (per_chunk - (coll != "allgather"))
+    for proto in ("simple", "ll"):
+        for coll, per_chunk in (("allreduce", 2 * 8 - 2), ("reducescatter", 8 - 1), ("allgather", 8 - 1)):
+            d, f = geom(proto, coll), geom(proto, coll, flags=ar.AR_PLAN_FIFO_ONLY)
+            assert f["msgs_per_run"] == f["nchunks"] * per_chunk
+            assert d["msgs_per_run"] == d["nchunks"] * (per_chunk - (coll != "allgather"))
     # fp32: the same link bytes either way (the first link carries 4 bytes either way)
     assert geom("simple")["wire_bytes_per_run"] == geom("simple", flags=ar.AR_PLAN_FIFO_ONLY)["wire_bytes_per_run"]
+    # LL: the first link carries the chain start's 4 bytes without line flags
+    # instead of a 4-byte partial in an 8-byte line (count elements per run)
+    assert (geom("ll", flags=ar.AR_PLAN_FIFO_ONLY)["wire_bytes_per_run"] - geom("ll")["wire_bytes_per_run"]
+            == (1 << 16) * 4)
+    # AllGather has no chain start: the same link bytes either way
+    assert geom("ll", "allgather")["wire_bytes_per_run"] == geom("ll", "allgather",
+                                                                  flags=ar.AR_PLAN_FIFO_ONLY)["wire_bytes_per_run"]
     d = ar.make_desc(8, 1 << 16, "f32", "simple", 4, flags=8)
     assert ar.lib().ar_plan_geometry(ctypes.byref(d), ctypes.byref(ar.ar_plan_info())) == ar.AR_ERR_ARG
     # the ordered-read flag of LL128 changes no geometry

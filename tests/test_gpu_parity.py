@@ -205,9 +205,10 @@ def _metamorphic_configs():
     cfgs += [dict(proto="simple", nchannels=8, nwaves=w) for w in (1, 2, 8, 16)]
     cfgs += [dict(proto=p, nchannels=16, placement=1) for p in PROTOS]
     cfgs += [dict(proto=p, nchannels=4, fifo_depth=d) for p in PROTOS for d in (2, 3, 8)]
-    # the Simple ring's all-gather through the FIFOs instead of direct writes
-    cfgs += [dict(proto="simple", nchannels=nch, chunk_bytes=chunk, flags=2) for nch in (1, 5, 64)
-             for chunk in (16, 4096)]
+    # every hop through the FIFOs instead of the peer-direct mode: the Simple
+    # ring's all-gather and the Simple and LL chain starts
+    cfgs += [dict(proto=p, nchannels=nch, chunk_bytes=chunk, flags=2) for p in ("simple", "ll")
+             for nch in (1, 5, 64) for chunk in (16, 4096)]
     cfgs += [dict(proto="auto")]
     return cfgs
 
