@@ -199,17 +199,18 @@ typedef struct ar_plan_desc {
  *                    run's sample is harvested without blocking by a later
  *                    ar_run, or by ar_plan_status; a run whose predecessor's
  *                    events are still pending is not timed.
- *   AR_PLAN_FIFO_ONLY  Simple ring only: carry every hop through the FIFOs.
- *                    By default the Simple ring accesses its neighbours'
- *                    buffers directly where that saves a copy: the second
+ *   AR_PLAN_FIFO_ONLY  Simple and LL rings: carry every hop through the
+ *                    FIFOs.  By default (the peer-direct mode) the second
  *                    rank of each reduce-scatter chain reads the chain
  *                    start's input from that rank's buffer (one hop and its
- *                    flag fewer), and each finished all-gather chunk is
- *                    written straight into the next rank's output buffer and
- *                    forwarded from there (nothing moves on the last hop).
- *                    The result bits are the same either way.  The other
- *                    protocols always use their FIFOs, and the direct
- *                    algorithm has none, so they ignore the flag.
+ *                    flag fewer), and the Simple ring also writes each
+ *                    finished all-gather chunk straight into the next
+ *                    rank's output buffer and forwards it from there
+ *                    (nothing moves on the last hop); LL's all-gather keeps
+ *                    its lines, whose flags cannot live in a user buffer.
+ *                    The result bits are the same either way.  LL128 always
+ *                    uses its FIFOs, and the direct algorithm has none, so
+ *                    they ignore the flag.
  *   AR_PLAN_LL128_ORDERED  LL128 only: a reader uses a batch of lines only
  *                    from loads issued after it has seen every flag of the
  *                    batch current (it polls the 8-byte flags, then reads
@@ -239,13 +240,15 @@ typedef struct ar_plan_info {
                               AllReduce and ReduceScatter */
     uint64_t wire_bytes_per_run; /* bytes that cross ring links per run (all
                               connections): written to a FIFO with flags, or,
-                              with peer_direct, all-gather chunks written into
-                              the next rank's output */
+                              with peer_direct, the chain starts' inputs read
+                              by the second ranks and (Simple) all-gather
+                              chunks written into the next rank's output */
     int algo;              /* AR_ALGO_RING or AR_ALGO_DIRECT */
     int coll;              /* AR_COLL_* */
-    int peer_direct;       /* 1: the Simple ring reads the chain start's input
-                              and writes all-gather chunks into the next
-                              rank's output directly (see AR_PLAN_FIFO_ONLY) */
+    int peer_direct;       /* 1: the Simple or LL ring reads the chain start's
+                              input directly, and the Simple ring writes
+                              all-gather chunks into the next rank's output
+                              (see AR_PLAN_FIFO_ONLY) */
     int direct_unroll;     /* direct algorithm: units per thread and iteration */
 } ar_plan_info;
 
