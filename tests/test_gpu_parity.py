@@ -177,14 +177,14 @@ def test_order_revealing_brute_force(ar):
 def test_order_revealing_bf16(ar):
     """bf16 with fp32 accumulation on order-revealing inputs: the chain of
     every 8-element-aligned segment must start at its own rank and run in
-    ring order, on the ring under each protocol (the Simple ring both
-    peer-direct and FIFO only) and on the direct algorithm.  The inputs are
-    checked to be informative: starting every chain one rank earlier
+    ring order, on the ring under each protocol (the Simple and LL rings
+    both peer-direct and FIFO only) and on the direct algorithm.  The inputs
+    are checked to be informative: starting every chain one rank earlier
     changes many rounded results."""
     informative = 0
     cfgs = [dict(proto=p, nchannels=2, chunk_bytes=64) for p in PROTOS]
-    cfgs += [dict(proto="simple", nchannels=3, chunk_bytes=32, flags=2), dict(algo="direct"),
-             dict(algo="direct", nchannels=3, nwaves=1)]
+    cfgs += [dict(proto=p, nchannels=3, chunk_bytes=32, flags=2) for p in ("simple", "ll")]
+    cfgs += [dict(algo="direct"), dict(algo="direct", nchannels=3, nwaves=1)]
     for n in (2, 3, 4, 8):
         for count in (16, 40, 64, 264, 1001):
             x = order_input(n, count, "bf16", seed=900 + 17 * n + count)
@@ -192,6 +192,35 @@ def test_order_revealing_bf16(ar):
             for cfg in cfgs:
                 run_case(ar, x, "bf16", f"order-bf16-{n}-{count}-{cfg}", **cfg)
     assert informative > 200, informative
+
+
+def test_order_revealing_bf16_full_size(ar):
+    """The bf16 chain order at the 32 MiB bf16 workload's size (8 ranks x
+    16 Mi elements): order-revealing values, compared on the device under
+    the table's ring and overall choices, the fixed default, LL and LL128."""
+    import torch
+
+    n, count = 8, 16 << 20
+    x = order_input(n, count, "bf16", seed=4711)
+    want = ro.allreduce_bf16(x)
+    changed = int(np.count_nonzero(want != ro.allreduce_bf16(np.roll(x, 1, axis=0))))
+    assert changed > count // 20, changed  # about 8.6 % of the elements
+    want_dev = to_device(want[None, :], "bf16")[0]
+    base = to_device(x, "bf16")
+    del x
+    for cfg in (dict(proto="auto", algo="ring"), dict(proto="auto"), dict(proto="simple", nchannels=16),
+                dict(proto="ll", nchannels=64), dict(proto="ll128", nchannels=64)):
+        say(f"order bf16 full size {cfg}")
+        out = [torch.empty_like(t) for t in base]
+        plan = ar.Plan(n, count, "bf16", **cfg)
+        plan.run_oop(base, out)
+        torch.cuda.synchronize()
+        assert plan.status() == ar.AR_OK, cfg
+        plan.destroy()
+        for r in range(n):
+            if not torch.equal(out[r].view(torch.int16), want_dev.view(torch.int16)):
+                bad = (out[r].view(torch.int16) != want_dev.view(torch.int16)).nonzero()
+                raise AssertionError(f"{cfg} rank {r}: {bad.numel()} elements differ, first {int(bad[0])}")
 
 
 # ------------------------------------------------- layout independence (U1)
