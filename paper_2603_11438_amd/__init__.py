@@ -576,9 +576,9 @@ def ring_bytes(msg_bytes: int, nranks: int, dtype="f32", proto="simple", peer_di
     rank's (2e); the last rank moves nothing.  With two ranks the owner is
     the second rank: it reads both inputs and writes both outputs (4e).
 
-    The peer-direct LL ring only starts its chains with the peer read: the
-    first hop's partial line is neither written nor read, 2 * 4 * 2 bytes
-    fewer per element than through the FIFOs.  LL128 always uses its FIFOs."""
+    The peer-direct LL and LL128 rings only start their chains with the
+    peer read: the first hop's partial line is neither written nor read,
+    2 * 4 * w bytes fewer per element than through the FIFOs."""
     e = 4 if dtype == "f32" else 2
     count = msg_bytes // e
     if peer_direct and proto == "simple" and nranks >= 2:
@@ -589,7 +589,7 @@ def ring_bytes(msg_bytes: int, nranks: int, dtype="f32", proto="simple", peer_di
     wf = {"simple": 1.0, "ll": 2.0, "ll128": 128.0 / 120.0}[proto]
     wire = count * (nranks - 1) * (4 + e) * wf
     total = 2.0 * nranks * msg_bytes + 2.0 * wire
-    if peer_direct and proto == "ll" and nranks >= 2:
+    if peer_direct and proto in ("ll", "ll128") and nranks >= 2:
         total -= count * 2 * 4 * wf
     return total
 

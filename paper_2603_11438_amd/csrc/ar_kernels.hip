@@ -1018,6 +1018,7 @@ struct LL128Step {
     static constexpr bool kWriteOut = KindTraits<KIND>::kWriteOut;
     static constexpr bool kReduceToY = KindTraits<KIND>::kReduceToY;
     static constexpr bool kCopyInToY = KindTraits<KIND>::kCopyInToY;
+    static constexpr bool kRecvPeer = KindTraits<KIND>::kRecvPeer;
     // bf16 recvReduceCopySend changes the line format on the way through.
     static constexpr bool kRelayout = DT == AR_BFLOAT16 && KIND == kRecvReduceCopySend;
     // Wave-wide line accesses (8 lines each) per batch.  Two batches are in
@@ -1149,6 +1150,7 @@ struct LL128Step {
     }
 
     // Reduce-scatter arithmetic for one lane part: up to 4 fp32 partials
+    // (or, for a peer read, the chain start's 4 elements in the data type)
     // plus the lane's input elements.
     __device__ static u32x4 rs_reduce(const u32x4 &wire, const u32x4 &in)
     {
@@ -1159,7 +1161,23 @@ struct LL128Step {
         }
         if (kRecvRS)
             for (int i = 0; i < 4; ++i) acc[i] = as_f32(wire[i]) + acc[i];
+        if (kRecvPeer) {
+            for (int i = 0; i < 4; ++i) {
+                const float w = E == 4 ? as_f32(wire[i]) : ((i & 1) ? bf16_hi(wire[i >> 1]) : bf16_lo(wire[i >> 1]));
+                acc[i] = w + acc[i];
+            }
+        }
         return u32x4{as_u32(acc[0]), as_u32(acc[1]), as_u32(acc[2]), as_u32(acc[3])};
+    }
+    // A two-rank chain's owner in bf16 (peer read, no reduce-scatter line):
+    // 8 elements per lane part in the all-gather format, the chain start's
+    // plus the own, rounded once.
+    __device__ static u32x4 peer_y8(const u32x4 &peer, const u32x4 &in)
+    {
+        u32x4 y;
+        for (int i = 0; i < 4; ++i)
+            y[i] = pack_bf16(bf16_lo(peer[i]) + bf16_lo(in[i]), bf16_hi(peer[i]) + bf16_hi(in[i]));
+        return y;
     }
 
     // Wait until the lines held in lines[] (the batch's lines first..first +
@@ -1246,7 +1264,10 @@ struct LL128Step {
         const bool chk = DBG && dbg->check;
         const Rsrc rin = make_rsrc(src, (uint64_t)len * E);
         const Rsrc rout = make_rsrc(dst, (uint64_t)len * E);
-        const Rsrc wi = make_rsrc(rslot, a.slot_bytes);
+        // rslot: the incoming FIFO slot, or for a peer read the chain
+        // start's input at this message's elements (then `wire` holds it in
+        // the data type)
+        const Rsrc wi = make_rsrc(rslot, kRecvPeer ? (uint64_t)len * E : a.slot_bytes);
         const Rsrc wo = make_rsrc(wslot, a.slot_bytes);
         if constexpr (!kRelayout) {
             // One line format in and out: the lane part maps to the same elements.
@@ -1270,6 +1291,7 @@ struct LL128Step {
                     unit(base, t, line, act, nval);
                     if (kLoadIn) in[t] = load_whole<epart>(rin, (line * epl + p * epart) * E, p, nval, full);
                     if (kRecvRS || kRecvAG) wire[t] = ld128<kFifoLd>(wi, in_range(act, line * 128 + 16 * p));
+                    if (kRecvPeer) wire[t] = load_whole<epart>(wi, (line * epl + p * epart) * E, p, nval, full);
                 }
             };
             // Lines are written in groups of kGroup batches; one drain per
@@ -1303,6 +1325,12 @@ struct LL128Step {
                         for (int t = 0; t < U; ++t)
                             in[t] = part_value<epart>(rin, (line_of[t] * epl + p * epart) * E, p, nval[t], full, in[t]);
                     }
+                    if (kRecvPeer) {
+#pragma unroll
+                        for (int t = 0; t < U; ++t)
+                            wire[t] = part_value<epart>(wi, (line_of[t] * epl + p * epart) * E, p, nval[t], full,
+                                                        wire[t]);
+                    }
                     // The next batch's loads go out before this batch's
                     // stores: the vector memory counter retires in issue
                     // order, so a load issued after a store cannot be waited
@@ -1315,7 +1343,8 @@ struct LL128Step {
                     for (int t = 0; t < U; ++t) {
                         const uint32_t e0 = line_of[t] * epl + p * epart;
                         u32x4 out;
-                        if (kSendRS || kReduceToY) out = rs_reduce(wire[t], in[t]);
+                        if (kRecvPeer && E == 2 && !kSendRS) out = peer_y8(wire[t], in[t]);
+                        else if (kSendRS || kReduceToY) out = rs_reduce(wire[t], in[t]);
                         else if (kCopyInToY) out = in[t];
                         else out = wire[t];
                         if (kWriteOut) {
@@ -1427,7 +1456,8 @@ struct LL128Step {
 constexpr uint32_t kLdsWordsPerWave = 240;  // 480 bf16 values
 
 template <int DT, int KIND, bool DBG, int LU, bool ORD>
-__device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, uint32_t len, uint32_t *lds)
+__device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, const char *peer_src, uint32_t len,
+                                           uint32_t *lds)
 {
     const RingArgs &a = *g.a;
     constexpr bool recv = KindTraits<KIND>::kRecvRS || KindTraits<KIND>::kRecvAG;
@@ -1437,6 +1467,7 @@ __device__ __forceinline__ bool ll128_step(Ring &g, const char *src, char *dst, 
     // LL128 runs out of vector registers first, so it derives the slot from
     // the message index instead of carrying the slot counters.
     if (recv) rslot = slot_ptr(const_cast<char *>(g.fifo_in), (uint32_t)(g.m_in % a.depth), a);
+    if (KindTraits<KIND>::kRecvPeer) rslot = peer_src;
     if (send) {
         if (!acquire_send_slot(g)) return false;
         wslot = slot_ptr(g.fifo_out, (uint32_t)(g.m_out % a.depth), a);
@@ -1499,7 +1530,7 @@ __device__ __forceinline__ bool do_step(Ring &g, const char *src, char *dst, cha
     bool ok;
     if (PROTO == AR_PROTO_SIMPLE) ok = simple_step<DT, KIND, DAG, DBG>(g, src, dst, peer_dst, peer_src, len);
     else if (PROTO == AR_PROTO_LL) ok = ll_step<DT, KIND, DBG>(g, src, dst, peer_src, len);
-    else ok = ll128_step<DT, KIND, DBG, LU, ORD>(g, src, dst, len, lds);
+    else ok = ll128_step<DT, KIND, DBG, LU, ORD>(g, src, dst, peer_src, len, lds);
     if constexpr (DBG) {
         if (g.dbg.trace) {
             write_trace(g);
@@ -1908,12 +1939,12 @@ __global__ void bf16_round_kernel(const float *in, uint16_t *out, size_t n)
 
 typedef void (*RingFn)(RingArgs);
 
-// dag: the Simple ring's direct all-gather (the other protocols always
-// carry the all-gather through their FIFOs).
-template <int DT, bool DBG, bool ORD>
+// dag: the peer-direct mode (chains start with a peer read; the Simple
+// ring also writes its all-gather into the next rank's output).
+template <int DT, bool DBG, bool ORD, bool DAG>
 __host__ RingFn ll128_fn(bool wide)
 {
-    return wide ? ring_kernel<AR_PROTO_LL128, DT, false, DBG, 4, ORD> : ring_kernel<AR_PROTO_LL128, DT, false, DBG, 2, ORD>;
+    return wide ? ring_kernel<AR_PROTO_LL128, DT, DAG, DBG, 4, ORD> : ring_kernel<AR_PROTO_LL128, DT, DAG, DBG, 2, ORD>;
 }
 
 template <int DT, bool DBG>
@@ -1921,7 +1952,10 @@ __host__ RingFn ring_fn_of(int proto, bool dag, bool wide, bool ordered)
 {
     if (proto == AR_PROTO_LL)
         return dag ? ring_kernel<AR_PROTO_LL, DT, true, DBG, 2, false> : ring_kernel<AR_PROTO_LL, DT, false, DBG, 2, false>;
-    if (proto == AR_PROTO_LL128) return ordered ? ll128_fn<DT, DBG, true>(wide) : ll128_fn<DT, DBG, false>(wide);
+    if (proto == AR_PROTO_LL128) {
+        if (dag) return ordered ? ll128_fn<DT, DBG, true, true>(wide) : ll128_fn<DT, DBG, false, true>(wide);
+        return ordered ? ll128_fn<DT, DBG, true, false>(wide) : ll128_fn<DT, DBG, false, false>(wide);
+    }
     return dag ? ring_kernel<AR_PROTO_SIMPLE, DT, true, DBG, 2, false> : ring_kernel<AR_PROTO_SIMPLE, DT, false, DBG, 2, false>;
 }
 

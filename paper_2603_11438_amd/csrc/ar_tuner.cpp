@@ -320,10 +320,10 @@ int resolve_geometry(const ar_plan_desc *d, int max_channels, ar_plan_info *out)
     g.placement = d->placement;
     g.count = d->count;
     g.block = 64 * nw;
-    // Peer-direct mode: Simple and LL chains start with a peer read (and
-    // the Simple all-gather writes into the next rank's output); LL128 and
+    // Peer-direct mode: reduction chains start with a peer read (and the
+    // Simple all-gather writes into the next rank's output);
     // AR_PLAN_FIFO_ONLY plans keep every hop in the FIFOs.
-    g.peer_direct = (proto == AR_PROTO_SIMPLE || proto == AR_PROTO_LL) && !(d->flags & AR_PLAN_FIFO_ONLY);
+    g.peer_direct = !(d->flags & AR_PLAN_FIFO_ONLY);
 
     const uint64_t N = (uint64_t)d->nranks;
     g.seg_elems = d->coll == AR_COLL_ALLREDUCE ? round_up(ceil_div(d->count, N), A) : d->count;

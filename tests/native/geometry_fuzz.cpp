@@ -46,9 +46,9 @@ int main(int argc, char **argv)
             ok = ok && g.chunk_elems >= A && g.chunk_elems <= g.chan_elems && g.chunk_elems % A == 0;
             ok = ok && g.nchunks * g.chunk_elems >= g.chan_elems;
             ok = ok && g.wave_elems * (uint64_t)g.nwaves >= g.chunk_elems;
-            // the peer-direct Simple and LL rings start each chain with a peer read
+            // a ring plan without AR_PLAN_FIFO_ONLY starts each chain with a peer read
             ok = ok && g.msgs_per_run == g.nchunks * (2 * N - 2 - (uint64_t)g.peer_direct);
-            ok = ok && g.peer_direct == (g.proto == AR_PROTO_SIMPLE || g.proto == AR_PROTO_LL ? 1 : 0);
+            ok = ok && g.peer_direct == 1;
             ok = ok && g.slot_bytes % 256 == 0 && g.slot_bytes >= g.wave_elems * 4;
             ok = ok && g.fifo_bytes == (uint64_t)g.nchannels * N * g.nwaves * g.fifo_depth * g.slot_bytes;
             ok = ok && g.fifo_depth >= 2 && g.fifo_depth <= 16 && g.nwaves >= 1 && g.nwaves <= AR_MAX_WAVES;

@@ -287,6 +287,9 @@ def test_ring_byte_counts():
     # first hop's fp32 partial line (8 B) is neither written nor read.
     assert ar.ring_bytes(S, 8, "f32", "ll", peer_direct=True) == 68 * S
     assert ar.ring_bytes(S, 8, "bf16", "ll", peer_direct=True) == ar.ring_bytes(S, 8, "bf16", "ll") - 8 * S
+    # LL128 likewise: its first partial line (8 B per element x 128/120)
+    assert abs(ar.ring_bytes(S, 8, "f32", "ll128", peer_direct=True)
+               - (ar.ring_bytes(S, 8, "f32", "ll128") - 2 * S * 128 / 120)) < 1
 
 
 def test_direct_unroll_resolution():
@@ -327,11 +330,11 @@ def test_direct_allgather_mode_in_geometry():
     assert geom("simple", "allgather")["peer_direct"] == 1
     assert geom("simple", "reducescatter")["peer_direct"] == 1
     assert geom("simple", flags=ar.AR_PLAN_FIFO_ONLY)["peer_direct"] == 0
-    assert geom("ll")["peer_direct"] == 1 and geom("ll", flags=ar.AR_PLAN_FIFO_ONLY)["peer_direct"] == 0
-    assert geom("ll", "allgather")["peer_direct"] == 1
-    assert geom("ll128")["peer_direct"] == 0
+    for proto in ("ll", "ll128"):
+        assert geom(proto)["peer_direct"] == 1 and geom(proto, flags=ar.AR_PLAN_FIFO_ONLY)["peer_direct"] == 0
+        assert geom(proto, "allgather")["peer_direct"] == 1
     # one message fewer per chunk when a chain starts with a peer read
-    for proto in ("simple", "ll"):
+    for proto in ("simple", "ll", "ll128"):
         for coll, per_chunk in (("allreduce", 2 * 8 - 2), ("reducescatter", 8 - 1), ("allgather", 8 - 1)):
             d, f = geom(proto, coll), geom(proto, coll, flags=ar.AR_PLAN_FIFO_ONLY)
             assert f["msgs_per_run"] == f["nchunks"] * per_chunk

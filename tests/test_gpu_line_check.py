@@ -81,9 +81,9 @@ def test_line_check_collectives(ar, proto, dtype):
     the slots and must never be accepted for later messages)."""
     a = 4 if dtype == "f32" else 8
     dbg = ar.AR_DEBUG_CHECK_LINES
-    # LL also with every hop through the FIFOs (by default its reduction
-    # chains start with a peer read)
-    modes = (0, ar.AR_PLAN_FIFO_ONLY) if proto == "ll" else (0,)
+    # also with every hop through the FIFOs (by default the reduction chains
+    # start with a peer read)
+    modes = (0, ar.AR_PLAN_FIFO_ONLY)
     for n in (2, 3, 8):
         for flags in modes:
             for count, nch in ((1000 * a + 3, 1), (4099, 3), (24 * a, 2)):
@@ -140,7 +140,7 @@ def test_trace_records(ar):
     n, count = 8, 8 * 4096
     for proto in ("simple", "ll", "ll128"):
         plan = ar.Plan(n, count, "f32", proto=proto, nchannels=2, nwaves=1, debug_flags=ar.AR_DEBUG_TRACE,
-                       flags=ar.AR_PLAN_FIFO_ONLY if proto != "ll128" else 0)
+                       flags=ar.AR_PLAN_FIFO_ONLY)
         per_rank = 64
         buf = torch.zeros(n * per_rank * 8, dtype=torch.int64, device="cuda:0")
         plan.set_trace(buf)

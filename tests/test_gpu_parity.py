@@ -68,13 +68,18 @@ def test_ll128_line_tails(ar):
     lane.  One channel and one wave, so a message is a whole segment and
     the last segment's length walks through every remainder.  Segments of
     about 240 elements (8 to 17 reduce-scatter lines) run the two-access
-    batches; about 1200 elements (40 lines), the four-access ones."""
+    batches; about 1200 elements (40 lines), the four-access ones.  Two
+    ranks run both ways: peer-direct (the owner reads the chain start's
+    input and sends all-gather lines) and through the FIFOs (a
+    reduce-scatter line hop)."""
     for dtype in ("f32", "bf16"):
         for n, step, hi, base in ((2, 1, 124, 240), (3, 3, 190, 240), (2, 1, 124, 1200), (3, 5, 190, 1200)):
-            for r in range(0, hi, step):
-                count = n * base + r
-                x = draw(n, count, dtype, "normal", seed=5000 + 7 * n + r)
-                run_case(ar, x, dtype, f"ll128-tail-{dtype}-{n}-{count}", proto="ll128", nchannels=1, nwaves=1)
+            for flags in ((0, ar.AR_PLAN_FIFO_ONLY) if n == 2 else (0,)):
+                for r in range(0, hi, step):
+                    count = n * base + r
+                    x = draw(n, count, dtype, "normal", seed=5000 + 7 * n + r)
+                    run_case(ar, x, dtype, f"ll128-tail-{dtype}-{n}-{count}-{flags}", proto="ll128", nchannels=1,
+                             nwaves=1, flags=flags)
 
 
 def test_ll128_ordered_reads(ar):
@@ -177,13 +182,13 @@ def test_order_revealing_brute_force(ar):
 def test_order_revealing_bf16(ar):
     """bf16 with fp32 accumulation on order-revealing inputs: the chain of
     every 8-element-aligned segment must start at its own rank and run in
-    ring order, on the ring under each protocol (the Simple and LL rings
-    both peer-direct and FIFO only) and on the direct algorithm.  The inputs
+    ring order, on the ring under each protocol (each both peer-direct and
+    FIFO only) and on the direct algorithm.  The inputs
     are checked to be informative: starting every chain one rank earlier
     changes many rounded results."""
     informative = 0
     cfgs = [dict(proto=p, nchannels=2, chunk_bytes=64) for p in PROTOS]
-    cfgs += [dict(proto=p, nchannels=3, chunk_bytes=32, flags=2) for p in ("simple", "ll")]
+    cfgs += [dict(proto=p, nchannels=3, chunk_bytes=32, flags=2) for p in PROTOS]
     cfgs += [dict(algo="direct"), dict(algo="direct", nchannels=3, nwaves=1)]
     for n in (2, 3, 4, 8):
         for count in (16, 40, 64, 264, 1001):
@@ -235,8 +240,8 @@ def _metamorphic_configs():
     cfgs += [dict(proto=p, nchannels=16, placement=1) for p in PROTOS]
     cfgs += [dict(proto=p, nchannels=4, fifo_depth=d) for p in PROTOS for d in (2, 3, 8)]
     # every hop through the FIFOs instead of the peer-direct mode: the Simple
-    # ring's all-gather and the Simple and LL chain starts
-    cfgs += [dict(proto=p, nchannels=nch, chunk_bytes=chunk, flags=2) for p in ("simple", "ll")
+    # ring's all-gather and every protocol's chain starts
+    cfgs += [dict(proto=p, nchannels=nch, chunk_bytes=chunk, flags=2) for p in PROTOS
              for nch in (1, 5, 64) for chunk in (16, 4096)]
     cfgs += [dict(proto="auto")]
     return cfgs
