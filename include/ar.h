@@ -199,18 +199,17 @@ typedef struct ar_plan_desc {
  *                    run's sample is harvested without blocking by a later
  *                    ar_run, or by ar_plan_status; a run whose predecessor's
  *                    events are still pending is not timed.
- *   AR_PLAN_FIFO_ONLY  Simple and LL rings: carry every hop through the
- *                    FIFOs.  By default (the peer-direct mode) the second
- *                    rank of each reduce-scatter chain reads the chain
- *                    start's input from that rank's buffer (one hop and its
- *                    flag fewer), and the Simple ring also writes each
- *                    finished all-gather chunk straight into the next
- *                    rank's output buffer and forwards it from there
- *                    (nothing moves on the last hop); LL's all-gather keeps
- *                    its lines, whose flags cannot live in a user buffer.
- *                    The result bits are the same either way.  LL128 always
- *                    uses its FIFOs, and the direct algorithm has none, so
- *                    they ignore the flag.
+ *   AR_PLAN_FIFO_ONLY  ring plans: carry every hop through the FIFOs.  By
+ *                    default (the peer-direct mode) the second rank of each
+ *                    reduce-scatter chain reads the chain start's input
+ *                    from that rank's buffer (one hop and its flag fewer),
+ *                    and the Simple ring also writes each finished
+ *                    all-gather chunk straight into the next rank's output
+ *                    buffer and forwards it from there (nothing moves on
+ *                    the last hop); the LL and LL128 all-gathers keep their
+ *                    lines, whose flags cannot live in a user buffer.  The
+ *                    result bits are the same either way.  The direct
+ *                    algorithm has no FIFOs and ignores the flag.
  *   AR_PLAN_LL128_ORDERED  LL128 only: a reader uses a batch of lines only
  *                    from loads issued after it has seen every flag of the
  *                    batch current (it polls the 8-byte flags, then reads
@@ -245,10 +244,10 @@ typedef struct ar_plan_info {
                               chunks written into the next rank's output */
     int algo;              /* AR_ALGO_RING or AR_ALGO_DIRECT */
     int coll;              /* AR_COLL_* */
-    int peer_direct;       /* 1: the Simple or LL ring reads the chain start's
-                              input directly, and the Simple ring writes
-                              all-gather chunks into the next rank's output
-                              (see AR_PLAN_FIFO_ONLY) */
+    int peer_direct;       /* 1: the ring reads the chain start's input
+                              directly, and the Simple ring writes all-gather
+                              chunks into the next rank's output (see
+                              AR_PLAN_FIFO_ONLY) */
     int direct_unroll;     /* direct algorithm: units per thread and iteration */
 } ar_plan_info;
 

@@ -22,9 +22,9 @@
 //   N-1 < k < 2N-2  recv y; write y, send y     (recvCopySend)
 //   k = 2N-2      recv y; write y               (recvCopy)
 // so segment s is summed x_s + x_{s+1} + ... + x_{s+N-1} in that order.  In
-// the peer-direct mode (Simple and LL rings) step 0 becomes a read of the
-// chain start's input by the second rank, and the Simple ring writes
-// all-gather chunks into the next rank's output instead of a FIFO slot.
+// the peer-direct mode step 0 becomes a read of the chain start's input by
+// the second rank, and the Simple ring writes all-gather chunks into the
+// next rank's output instead of a FIFO slot.
 //
 // Memory model.  A FIFO slot written by one wave is read by a wave that can
 // sit on another XCD, i.e. behind another L2.  Every FIFO access therefore
@@ -998,7 +998,9 @@ __device__ __forceinline__ bool ll_step(Ring &g, const char *src, char *dst, con
 // in front of its own, so lanes 6 and 7 write those bytes with equal values.
 // Reduce-scatter lines hold 30 fp32 partials; all-gather lines hold 30 fp32
 // or 60 bf16 values.  A bf16 recvReduceCopySend re-lays its results from the
-// 30-per-line to the 60-per-line format through LDS.
+// 30-per-line to the 60-per-line format through LDS.  In the peer-direct
+// mode a chain's second rank reads the chain start's input (no flags) in
+// the layout of its own input.
 
 constexpr uint32_t kLL128Data = 120;
 
