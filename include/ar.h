@@ -454,9 +454,12 @@ int ar_tune(const ar_tune_ctx *ctx, ar_tune_out *out);
 /* ar_tuner_table: measured MI355X tables, one row per power-of-two size
  * bucket of msg_bytes (4 KiB .. 128 MiB), one table per collective and data
  * type (bf16 reduce-scatter hops carry fp32 partials, which moves the best
- * geometry).  Every row was measured with 8 ranks; other rank counts get
- * the same row (results are identical, the choice is unmeasured there).
- * Collectives outside the tables defer to the default. */
+ * geometry).  Every row was measured with 8 ranks.  For N ranks a row's
+ * channel and direct part counts are scaled by 8 / N (rounded, at least
+ * 1), so that the grid keeps the workgroup count the row was measured
+ * with; with two ranks the LL rows defer to the default, whose peer-direct
+ * Simple ring waits for no flag at all there.  Results are identical for
+ * every choice.  Collectives outside the tables defer to the default. */
 int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);
 int ar_tuner_fixed_default(const ar_tune_ctx *ctx, ar_tune_out *out, void *user); /* Simple, 16 channels */
 int ar_tuner_noop(const ar_tune_ctx *ctx, ar_tune_out *out, void *user);          /* defers: no opinion */

@@ -444,6 +444,20 @@ int ar_tuner_noop(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
     return 0;
 }
 
+// The table rows were measured with kTableRanks ranks.  A launch has
+// nchannels * N ring workgroups (direct: parts * N), so for another rank
+// count N a row's channel and part counts are scaled by kTableRanks / N:
+// the grid keeps the workgroup count the row was measured with.  0 (the
+// library's own rule) stays 0.
+constexpr int kTableRanks = 8;
+
+static int scale_to_ranks(int v, int nranks)
+{
+    if (v <= 0 || nranks <= 0 || nranks == kTableRanks) return v;
+    const int s = (v * kTableRanks + nranks / 2) / nranks;
+    return s < 1 ? 1 : s;
+}
+
 int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
 {
     (void)user;
@@ -490,13 +504,22 @@ int ar_tuner_table(const ar_tune_ctx *ctx, ar_tune_out *out, void *user)
         if (table[i].log2_bytes >= lg) break;
     }
     out->proto = row->proto;
-    out->nchannels = row->nchannels;
+    out->nchannels = scale_to_ranks(row->nchannels, ctx->nranks);
     out->chunk_bytes = row->chunk_bytes;
     out->nwaves = row->nwaves;
     out->algo = row->algo;
-    out->direct_parts = row->direct_parts;
+    out->direct_parts = scale_to_ranks(row->direct_parts, ctx->nranks);
     out->direct_nwaves = row->direct_nwaves;
     out->direct_unroll = row->direct_unroll;
+    if (ctx->nranks == 2 && out->proto == AR_PROTO_LL) {
+        // With two ranks the peer-direct Simple ring waits for no flag at
+        // all (its one reduction hop is a peer read, its one all-gather hop
+        // waits for nothing), so the LL rows defer to the default there.
+        out->proto = AR_PROTO_AUTO;
+        out->nchannels = 0;
+        out->chunk_bytes = 0;
+        out->nwaves = 0;
+    }
     return 0;
 }
 

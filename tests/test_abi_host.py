@@ -403,3 +403,24 @@ def test_direct_geometry_and_algorithm_choice():
     ar.ar_set_tuner(lambda ctx: {"algo": 9, "proto": ar.AR_PROTO_LL, "nchannels": 5})
     assert ar.ar_tune(4096)["algo"] == ar.AR_ALGO_RING and ar.ar_tune(4096)["nchannels"] == 16
     ar.ar_set_tuner(None)
+
+
+def test_table_rows_scale_with_rank_count():
+    """Rows measured with 8 ranks keep their workgroup count at other rank
+    counts: channels and direct parts scale by 8/N (at least 1, 0 stays the
+    library's rule); with two ranks LL rows defer to the default."""
+    for size in (4096, 1 << 20, 4 << 20, 128 << 20):
+        base = ar.ar_tuner_raw("table", size, nranks=8)
+        for n in (2, 3, 4, 5, 16):
+            t = ar.ar_tuner_raw("table", size, nranks=n)
+            assert t["rc"] == 0 and t["algo"] == base["algo"]
+            assert t["direct_nwaves"] == base["direct_nwaves"] and t["direct_unroll"] == base["direct_unroll"]
+            want_parts = max(1, (base["direct_parts"] * 8 + n // 2) // n) if base["direct_parts"] else 0
+            assert t["direct_parts"] == want_parts, (size, n, t, base)
+            if n == 2 and base["proto"] == ar.AR_PROTO_LL:
+                assert t["proto"] == ar.AR_PROTO_AUTO and t["nchannels"] == 0
+            else:
+                assert t["proto"] == base["proto"] and t["chunk_bytes"] == base["chunk_bytes"]
+                assert t["nchannels"] == max(1, (base["nchannels"] * 8 + n // 2) // n), (size, n, t, base)
+    # 8 ranks: the rows as tabulated
+    assert ar.ar_tuner_raw("table", 128 << 20, nranks=8)["nchannels"] == 64
