@@ -480,6 +480,19 @@ class Plan:
 
 
 _plan_cache = {}
+_PLAN_CACHE_MAX = 64
+
+
+def release_plans() -> None:
+    """Free every plan `allreduce` has cached (after waiting for the device,
+    since a cached plan may still be in flight on some stream)."""
+    import torch
+
+    if _plan_cache:
+        torch.cuda.synchronize()
+    for plan in _plan_cache.values():
+        plan.destroy()
+    _plan_cache.clear()
 
 
 def allreduce(tensors: Sequence, proto="auto", nchannels: int = 0, chunk_bytes: int = 0, stream=None, **kw):
@@ -487,7 +500,9 @@ def allreduce(tensors: Sequence, proto="auto", nchannels: int = 0, chunk_bytes: 
 
     Plans are cached per shape, settings and stream: a plan must never be in
     flight on two streams at once (its FIFOs and flags are shared by all its
-    runs), so calls on different streams use different plans."""
+    runs), so calls on different streams use different plans.  The cache
+    holds at most 64 plans; a call that would add one more first frees them
+    all (release_plans), which waits for the device."""
     if not tensors:
         raise ValueError("need at least one tensor")
     t0 = tensors[0]
@@ -496,6 +511,8 @@ def allreduce(tensors: Sequence, proto="auto", nchannels: int = 0, chunk_bytes: 
            _stream_ptr(stream))
     plan = _plan_cache.get(key)
     if plan is None:
+        if len(_plan_cache) >= _PLAN_CACHE_MAX:
+            release_plans()
         plan = Plan(len(tensors), t0.numel(), dt, proto, nchannels, chunk_bytes, **kw)
         _plan_cache[key] = plan
     plan.run(tensors, stream)
